@@ -1,0 +1,289 @@
+"""P4Q CPU oracle -- TEST INFRASTRUCTURE, not part of the product.
+
+A plain, slow, obviously-correct CPU implementation of what the P4Q hot path
+computes, written from the paper's definitions.  Only the test-suite, the
+smoke check and the benchmark's CPU-baseline leg may import or call it; the
+HIP library never does, and this module shares no code with it.
+
+Conventions
+-----------
+* fl32(.) is IEEE binary32 with round-to-nearest-even.  NumPy float32 array
+  arithmetic (x / s, a * b) is exactly that on x86-64 (SSE, no fast-math); the
+  self-tests pin it against exact rational arithmetic.
+* rne(.) rounds half to even (``np.rint``).
+* Integers (codes, dot products, accumulators) are exact: int64 or Python int.
+* fp16 data are numpy float16; bf16 data are uint16 bit patterns.
+
+Paper anchors (P4Q, "Co-designing Token Pruning and Quantization for VLM
+Acceleration"):
+* Sec. 3.2, Eq. (p4q_progressive_selection): the selector ranks visual tokens
+  by CosSim between fake-quantized copies of the projector features and of the
+  query-concept embeddings; the original FP16 rows go forward.
+* Sec. 3.2 (Query Relevance paragraph): per-concept ranking, each concept keeps
+  its highest-scoring tokens within its quota.
+* Appendix A (experimental details) and Appendix B.3 (PTQ calibration
+  details): W4A4 = symmetric round-to-nearest, per-output-channel 4-bit
+  weights, per-token 4-bit activations, group size -1, activation clip 1.0.
+* Appendix B.3: after calibration the weights are quantized with RTN for W4A4
+  inference -- an integer GEMM on codes followed by dequantization.
+
+Readings where the paper is silent (each is listed in the design doc):
+* code range [-8, 7], scale = fl32(fl32(c*absmax)/7); ties round half to even;
+  x/s is a correctly rounded fp32 division; an all-zero row has scale 0;
+* the selector's fake quant uses the same per-token 4-bit quantizer (clip 1);
+* cosine similarity is taken on the real-valued fake-quantized vectors, which
+  equals the cosine of the integer codes exactly (the scales cancel);
+* equal scores are broken by the lower token index;
+* the Query-Relevance budget is split evenly across concepts (remainder to the
+  earliest), concepts are processed in order, already-kept tokens are skipped;
+* retained rows are emitted in ascending index order, text rows after them;
+* epilogue y = out_rne(fl32(fl32(float(acc) * s_a[m]) * s_w[n])).
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+from typing import List, Sequence, Tuple
+
+import numpy as np
+
+QMIN, QMAX = -8, 7          # two's-complement int4
+QDIV = np.float32(7.0)      # symmetric range divisor (2^(4-1) - 1)
+
+
+# --------------------------------------------------------------------------
+# storage helpers (dtype decoding / encoding)
+# --------------------------------------------------------------------------
+def as_f32(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Decode fp16 (float16 array) or bf16 (uint16 bit patterns) exactly."""
+    if dtype == "fp16":
+        return np.asarray(x, dtype=np.float16).astype(np.float32)
+    if dtype == "bf16":
+        u = np.asarray(x, dtype=np.uint16).astype(np.uint32) << 16
+        return u.view(np.float32)
+    raise ValueError(f"unknown dtype {dtype}")
+
+
+def f32_to_bf16_rne(y: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (nearest, ties to even) -> uint16 bits.
+
+    Finite inputs only (the epilogue never produces NaN).  Overflow past the
+    largest bf16 carries into the exponent and yields +-inf, as IEEE rounding
+    does."""
+    u = np.ascontiguousarray(y, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    return ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
+
+
+def round_out(y32: np.ndarray, out_dtype: str) -> np.ndarray:
+    """Final RNE rounding of the fp32 epilogue value to the output dtype."""
+    if out_dtype == "fp16":
+        return y32.astype(np.float16)          # IEEE RNE conversion
+    if out_dtype == "bf16":
+        return f32_to_bf16_rne(y32)
+    raise ValueError(out_dtype)
+
+
+# --------------------------------------------------------------------------
+# O1: the symmetric 4-bit round-to-nearest quantizer (per row)
+# --------------------------------------------------------------------------
+def quantize_rows(x: np.ndarray, dtype: str = "fp16", clip: float = 1.0
+                  ) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-row symmetric int4 RTN quantization (Appendix A / B.3 W4A4 setting).
+
+    For every row (a token for activations, an output channel for weights):
+      a      = max_k |x_k|                       (exact)
+      s      = fl32(fl32(clip * a) / 7)
+      code_k = clamp(rne(fl32(x_k / s)), -8, 7)   (s > 0)
+      code_k = 0, s = 0                           (s == 0)
+    Returns (codes int8 [..., L], scales float32 [...]).
+    """
+    xf = as_f32(x, dtype)
+    lead = xf.shape[:-1]
+    rows = xf.reshape(-1, xf.shape[-1])
+    codes = np.zeros(rows.shape, dtype=np.int8)
+    scales = np.zeros(rows.shape[0], dtype=np.float32)
+    c = np.float32(clip)
+    for r in range(rows.shape[0]):
+        row = rows[r]
+        if not np.all(np.isfinite(row)):
+            raise ValueError("non-finite input row")
+        a = np.max(np.abs(row))                       # exact in fp32
+        s = np.float32(np.float32(c * a) / QDIV)      # two fp32 roundings
+        scales[r] = s
+        if s == 0:
+            continue
+        q = row / s                                   # correctly rounded fp32
+        codes[r] = np.clip(np.rint(q), QMIN, QMAX).astype(np.int8)
+    return codes.reshape(xf.shape), scales.reshape(lead)
+
+
+def dequantize_rows(codes: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """The fake-quantized copy s * code, exactly, in float64."""
+    return codes.astype(np.float64) * scales.astype(np.float64)[..., None]
+
+
+# --------------------------------------------------------------------------
+# O2: nibble packing (low nibble = even k)
+# --------------------------------------------------------------------------
+def pack_int4(codes: np.ndarray) -> np.ndarray:
+    """byte_t = (code_{2t} & 0xF) | ((code_{2t+1} & 0xF) << 4)."""
+    c = np.asarray(codes, dtype=np.int16)
+    assert c.shape[-1] % 2 == 0
+    lo = c[..., 0::2] & 0xF
+    hi = c[..., 1::2] & 0xF
+    return (lo | (hi << 4)).astype(np.uint8)
+
+
+def unpack_int4(packed: np.ndarray) -> np.ndarray:
+    """Inverse of pack_int4: sign-extend each nibble back to int8."""
+    p = np.asarray(packed, dtype=np.int16)
+    lo = p & 0xF
+    hi = (p >> 4) & 0xF
+    lo = np.where(lo >= 8, lo - 16, lo)
+    hi = np.where(hi >= 8, hi - 16, hi)
+    out = np.empty(p.shape[:-1] + (p.shape[-1] * 2,), dtype=np.int8)
+    out[..., 0::2] = lo
+    out[..., 1::2] = hi
+    return out
+
+
+def quant_act(x: np.ndarray, dtype: str = "fp16", clip: float = 1.0
+              ) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-token activation quantize + pack: (packed uint8 [M, L/2], scales [M])."""
+    codes, scales = quantize_rows(x, dtype, clip)
+    return pack_int4(codes), scales
+
+
+# --------------------------------------------------------------------------
+# O3: quantization-aware Query-Relevance selection (Sec. 3.2)
+# --------------------------------------------------------------------------
+def concept_dots(cv: np.ndarray, cq: np.ndarray) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Exact integer statistics of the fake-quantized copies.
+
+    D[i, j] = sum_k cv[i,k] * cq[j,k],  Nv[i] = sum_k cv[i,k]^2,
+    Nq[j] = sum_k cq[j,k]^2.  With v~_i = s_v cv_i and q~_j = s_q cq_j,
+    CosSim(q~_j, v~_i) = D[i,j] / sqrt(Nv[i] * Nq[j]) exactly (scales cancel).
+    """
+    cv64 = cv.astype(np.int64)
+    cq64 = cq.astype(np.int64)
+    D = cv64 @ cq64.T
+    Nv = np.sum(cv64 * cv64, axis=1)
+    Nq = np.sum(cq64 * cq64, axis=1)
+    return D, Nv, Nq
+
+
+def signed_cos2(D: int, Nv: int, Nq: int) -> Fraction:
+    """sgn(cos) * cos^2 as an exact rational; 0 when a vector is all-zero.
+
+    x -> x|x| is strictly increasing, so it orders tokens exactly as the
+    cosine does while staying rational."""
+    den = int(Nv) * int(Nq)
+    if den == 0:
+        return Fraction(0)
+    D = int(D)
+    return Fraction(D * abs(D), den)
+
+
+def concept_order(D: np.ndarray, Nv: np.ndarray, Nq: np.ndarray, j: int) -> List[int]:
+    """Token indices in concept j's ranking: higher cosine first, equal
+    cosines by lower index."""
+    N = D.shape[0]
+    keys = [signed_cos2(D[i, j], Nv[i], Nq[j]) for i in range(N)]
+    return sorted(range(N), key=lambda i: (-keys[i], i))
+
+
+def concept_quotas(K: int, J: int) -> List[int]:
+    """Even split of the Query-Relevance budget, remainder to the first concepts."""
+    return [K // J + (1 if j < K % J else 0) for j in range(J)]
+
+
+def select_query_relevance(cv: np.ndarray, cq: np.ndarray, K: int) -> np.ndarray:
+    """Concept-wise top-K on the fake-quantized copies; returns sorted indices."""
+    D, Nv, Nq = concept_dots(cv, cq)
+    J = cq.shape[0]
+    kept: List[int] = []
+    in_set = set()
+    for j, quota in enumerate(concept_quotas(K, J)):
+        taken = 0
+        for i in concept_order(D, Nv, Nq, j):
+            if taken == quota:
+                break
+            if i in in_set:
+                continue
+            kept.append(i)
+            in_set.add(i)
+            taken += 1
+    return np.array(sorted(kept), dtype=np.int32)
+
+
+def select(vis: np.ndarray, concepts: np.ndarray, text: np.ndarray, K: int,
+           dtype: str = "fp16", clip: float = 1.0):
+    """The hot-path selector for one sample (Query Relevance holds all of K).
+
+    vis [N, d], concepts [J, d], text [T, d] (storage arrays of `dtype`).
+    Returns (idx int32 [K] ascending, tokens [K+T, d] storage dtype,
+             D int64 [N, J], Nv int64 [N]).
+    The fake-quantized copies decide *which* rows are kept; the rows that go
+    forward are the original, unquantized ones.
+    """
+    N = vis.shape[0]
+    if not (1 <= K <= N):
+        raise ValueError("need 1 <= K <= N")
+    cv, _ = quantize_rows(vis, dtype, clip)
+    cq, _ = quantize_rows(concepts, dtype, clip)
+    idx = select_query_relevance(cv, cq, K)
+    tokens = np.concatenate([np.asarray(vis)[idx], np.asarray(text)], axis=0)
+    D, Nv, _ = concept_dots(cv, cq)
+    return idx, tokens, D, Nv
+
+
+def select_batch(vis: np.ndarray, concepts: np.ndarray, text: np.ndarray, K: int,
+                 dtype: str = "fp16", clip: float = 1.0):
+    """select() for every sample of a batch [B, ...]."""
+    outs = [select(vis[b], concepts[b], text[b], K, dtype, clip) for b in range(vis.shape[0])]
+    idx = np.stack([o[0] for o in outs])
+    tok = np.stack([o[1] for o in outs])
+    D = np.stack([o[2] for o in outs])
+    Nv = np.stack([o[3] for o in outs])
+    return idx, tok, D, Nv
+
+
+# --------------------------------------------------------------------------
+# O4: the W4A4 linear (integer GEMM on codes + dequant epilogue)
+# --------------------------------------------------------------------------
+def int_gemm(a_codes: np.ndarray, w_codes: np.ndarray) -> np.ndarray:
+    """acc[m, n] = sum_k A[m, k] * W[n, k], exact.
+
+    Computed as a float64 matmul of the codes: every product is an integer of
+    magnitude <= 64 and every partial sum an integer below 2^24, so each one is
+    exactly representable and the result is exact whatever the summation
+    order."""
+    acc = a_codes.astype(np.float64) @ w_codes.astype(np.float64).T
+    return acc.astype(np.int64)
+
+
+def epilogue(acc: np.ndarray, a_scales: np.ndarray, w_scales: np.ndarray,
+             out_dtype: str) -> np.ndarray:
+    """y = out_rne(fl32(fl32(float(acc) * s_a[m]) * s_w[n]))."""
+    t = acc.astype(np.float32) * a_scales.astype(np.float32)[:, None]
+    t = t.astype(np.float32)
+    y = t * w_scales.astype(np.float32)[None, :]
+    return round_out(y.astype(np.float32), out_dtype)
+
+
+def w4a4_linear(a_packed: np.ndarray, a_scales: np.ndarray, w_packed: np.ndarray,
+                w_scales: np.ndarray, out_dtype: str):
+    """W4A4 linear on packed operands. Returns (acc int64 [M, N], y [M, N])."""
+    acc = int_gemm(unpack_int4(a_packed), unpack_int4(w_packed))
+    return acc, epilogue(acc, a_scales, w_scales, out_dtype)
+
+
+def w4a4_linear_entry(a_packed: np.ndarray, a_scales: np.ndarray, w_packed: np.ndarray,
+                      w_scales: np.ndarray, m: int, n: int, out_dtype: str):
+    """One output element (m, n) computed on its own, for sampled full-size checks."""
+    a = unpack_int4(a_packed[m]).astype(np.int64)
+    w = unpack_int4(w_packed[n]).astype(np.int64)
+    acc = int(np.dot(a, w))
+    y = epilogue(np.array([[acc]], dtype=np.int64), a_scales[m:m + 1], w_scales[n:n + 1],
+                 out_dtype)
+    return acc, y[0, 0]

@@ -1,0 +1,231 @@
+"""Seeded synthetic inputs with the shapes of P4Q's LLaVA workloads.
+
+This module only *draws* inputs. It holds none of the method's arithmetic (no
+quantizer, no scoring, no selection, no GEMM), so both the CPU oracle and the
+HIP path can be fed from it without sharing any of the computation under test.
+
+Shapes follow the paper's evaluation setting (Sec. 4.1 and Table 1): LLaVA-1.5
+feeds 576 visual tokens to the LLM, LLaVA-NeXT feeds 2880 (five AnyRes tiles of
+576, row-newline tokens excluded), retained budgets are 64 / 192 / 320 / 640,
+the 7B decoder has hidden 4096 and MLP 11008, and the 13B decoder 5120 / 13824.
+The benchmarks themselves (MMMU, GQA, ...) are not used; only their shapes are.
+
+Value recipe (identical for every config):
+  * visual features: N(0, 1), then 8 outlier channels (drawn once per config,
+    without replacement, shared by all tokens and samples) scaled by 20;
+  * text tokens: N(0, 1);
+  * query concepts (stand-in for the mean subword embedding of noun j,
+    Sec. 3.2): C_j = fp16(0.5 * (text_{2j} + text_{2j+1})), summed in fp32;
+  * weights: N(0, 0.02^2), one independent stream per linear;
+  * inputs of o_proj / down_proj (stand-ins for the attention output and the
+    gated MLP activation): drawn like the visual features, each with its own
+    outlier channels.
+All values are drawn in float32 with numpy's PCG64 and cast to fp16 with
+round-to-nearest-even.  The seed of every tensor is
+SeedSequence([42, config_id, tensor_id, sample]); 42 echoes the paper's seed.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+SEED = 42
+
+# tensor ids of the seed tree
+_T_VIS, _T_TEXT, _T_OUTLIER, _T_OPROJ_IN, _T_DOWN_IN = 0, 1, 2, 3, 4
+_T_OPROJ_OUTLIER, _T_DOWN_OUTLIER = 5, 6
+_T_WEIGHT0 = 16          # weights use tensor ids 16 + linear index
+_T_GEMV_IN = 32          # decode-step activations
+
+N_OUTLIER = 8
+OUTLIER_SCALE = 20.0
+WEIGHT_STD = 0.02
+
+
+@dataclass(frozen=True)
+class Linear:
+    """One linear layer: y[M, n_out] = x[M, k_in] @ W[n_out, k_in]^T."""
+    name: str
+    n_out: int
+    k_in: int
+    # which activation feeds it: "x" (selector output), "attn" (o_proj stand-in)
+    # or "mlp" (down_proj stand-in)
+    source: str
+
+
+@dataclass(frozen=True)
+class Config:
+    cfg_id: int
+    name: str
+    B: int            # images (samples)
+    N: int            # visual tokens per sample
+    d: int            # LLM hidden size (= projector output width)
+    K: int            # retained visual tokens per sample
+    T: int            # text tokens per sample
+    J: int            # query concepts per sample
+    linears: Tuple[Linear, ...]
+    out_dtype: str    # "fp16" | "bf16"
+    in_dtype: str = "fp16"
+    gemv_M: Tuple[int, ...] = ()
+
+    @property
+    def M(self) -> int:
+        """Rows of the pruned sequence that the linears run on."""
+        return self.B * (self.K + self.T)
+
+    def linear_ops(self) -> int:
+        """2*M*n_out*k_in summed over the layer's linears."""
+        return sum(2 * self.M * l.n_out * l.k_in for l in self.linears)
+
+
+def decoder_linears(h: int, f: int) -> Tuple[Linear, ...]:
+    """The seven linears of one LLaMA-family decoder layer."""
+    return (
+        Linear("q_proj", h, h, "x"),
+        Linear("k_proj", h, h, "x"),
+        Linear("v_proj", h, h, "x"),
+        Linear("o_proj", h, h, "attn"),
+        Linear("gate_proj", f, h, "x"),
+        Linear("up_proj", f, h, "x"),
+        Linear("down_proj", h, f, "mlp"),
+    )
+
+
+CONFIGS: Dict[str, Config] = {
+    "tiny": Config(0, "tiny-576x4096-k64", B=1, N=576, d=4096, K=64, T=32, J=4,
+                   linears=(Linear("proj", 4096, 4096, "x"),), out_dtype="fp16"),
+    "llava15_7b": Config(1, "llava1.5-7b-layer", B=1, N=576, d=4096, K=192, T=64, J=4,
+                         linears=decoder_linears(4096, 11008), out_dtype="bf16"),
+    "next7b_b1_k320": Config(2, "llava-next-7b-b1-k320", B=1, N=2880, d=4096, K=320, T=64,
+                             J=4, linears=decoder_linears(4096, 11008), out_dtype="bf16"),
+    "next7b_b1_k640": Config(2, "llava-next-7b-b1-k640", B=1, N=2880, d=4096, K=640, T=64,
+                             J=4, linears=decoder_linears(4096, 11008), out_dtype="bf16"),
+    "next7b_b16": Config(3, "llava-next-7b-b16", B=16, N=2880, d=4096, K=640, T=64, J=4,
+                         linears=decoder_linears(4096, 11008), out_dtype="bf16"),
+    "stress13b_b8": Config(4, "13b-shape-b8", B=8, N=2880, d=5120, K=640, T=64, J=4,
+                           linears=decoder_linears(5120, 13824), out_dtype="bf16",
+                           gemv_M=(1, 4, 16)),
+}
+
+
+def _rng(cfg_id: int, tensor_id: int, sample: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(
+        np.random.SeedSequence([SEED, cfg_id, tensor_id, sample])))
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Encode float32 values as bfloat16 bit patterns (round to nearest even).
+
+    Input encoding only (used to hand bf16 tensors to both sides)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def encode(x32: np.ndarray, dtype: str) -> np.ndarray:
+    """fp32 -> storage array: float16 array, or uint16 bf16 bit patterns."""
+    if dtype == "fp16":
+        return x32.astype(np.float16)
+    if dtype == "bf16":
+        return f32_to_bf16_bits(x32)
+    raise ValueError(dtype)
+
+
+def outlier_channels(cfg_id: int, tensor_id: int, d: int) -> np.ndarray:
+    return np.sort(_rng(cfg_id, tensor_id).choice(d, size=N_OUTLIER, replace=False))
+
+
+def outlier_features(cfg_id: int, tensor_id: int, outlier_tid: int, rows: int, d: int,
+                     sample: int = 0, dtype: str = "fp16") -> np.ndarray:
+    """rows x d features: N(0,1) with 8 shared outlier channels scaled x20."""
+    x = _rng(cfg_id, tensor_id, sample).standard_normal((rows, d), dtype=np.float32)
+    x[:, outlier_channels(cfg_id, outlier_tid, d)] *= np.float32(OUTLIER_SCALE)
+    return encode(x, dtype)
+
+
+def visual_features(cfg: Config, sample: int) -> np.ndarray:
+    """[N, d] projector-output stand-in for one image."""
+    return outlier_features(cfg.cfg_id, _T_VIS, _T_OUTLIER, cfg.N, cfg.d, sample, cfg.in_dtype)
+
+
+def text_tokens(cfg: Config, sample: int) -> np.ndarray:
+    """[T, d] text-token embeddings stand-in for one question."""
+    x = _rng(cfg.cfg_id, _T_TEXT, sample).standard_normal((cfg.T, cfg.d), dtype=np.float32)
+    return encode(x, cfg.in_dtype)
+
+
+def concepts_from_text(text_f32: np.ndarray, J: int, dtype: str) -> np.ndarray:
+    """[J, d] concept rows: mean of two consecutive text rows, summed in fp32."""
+    assert text_f32.shape[0] >= 2 * J, "need two text rows per concept"
+    c = (text_f32[0:2 * J:2] + text_f32[1:2 * J:2]) * np.float32(0.5)
+    return encode(c.astype(np.float32), dtype)
+
+
+def to_f32(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Decode a storage array (fp16, or bf16 bit patterns) to float32 exactly."""
+    if dtype == "fp16":
+        return a.astype(np.float32)
+    return (a.astype(np.uint32) << 16).view(np.float32)
+
+
+@dataclass
+class SelectorInputs:
+    vis: np.ndarray        # [B, N, d]
+    concepts: np.ndarray   # [B, J, d]
+    text: np.ndarray       # [B, T, d]
+    dtype: str
+
+
+def selector_inputs(cfg: Config, samples: Optional[List[int]] = None) -> SelectorInputs:
+    samples = list(range(cfg.B)) if samples is None else samples
+    vis, con, txt = [], [], []
+    for b in samples:
+        vis.append(visual_features(cfg, b))
+        t = text_tokens(cfg, b)
+        txt.append(t)
+        con.append(concepts_from_text(to_f32(t, cfg.in_dtype), cfg.J, cfg.in_dtype))
+    return SelectorInputs(np.stack(vis), np.stack(con), np.stack(txt), cfg.in_dtype)
+
+
+def weight(cfg: Config, li: int, dtype: str = "fp16") -> np.ndarray:
+    """[n_out, k_in] weight of linear li: N(0, 0.02^2)."""
+    lin = cfg.linears[li]
+    w = _rng(cfg.cfg_id, _T_WEIGHT0 + li).standard_normal((lin.n_out, lin.k_in),
+                                                          dtype=np.float32)
+    w *= np.float32(WEIGHT_STD)
+    return encode(w, dtype)
+
+
+def attn_standin(cfg: Config, rows: Optional[int] = None) -> np.ndarray:
+    """[M, d] input of o_proj (attention-output stand-in)."""
+    rows = cfg.M if rows is None else rows
+    return outlier_features(cfg.cfg_id, _T_OPROJ_IN, _T_OPROJ_OUTLIER, rows, cfg.d, 0,
+                            cfg.in_dtype)
+
+
+def mlp_standin(cfg: Config, rows: Optional[int] = None) -> np.ndarray:
+    """[M, f] input of down_proj (gated-MLP-activation stand-in)."""
+    rows = cfg.M if rows is None else rows
+    f = [l.k_in for l in cfg.linears if l.source == "mlp"]
+    width = f[0] if f else cfg.d
+    return outlier_features(cfg.cfg_id, _T_DOWN_IN, _T_DOWN_OUTLIER, rows, width, 0,
+                            cfg.in_dtype)
+
+
+def gemv_activations(cfg: Config, M: int, k_in: int) -> np.ndarray:
+    """[M, k_in] decode-step activations with the same outlier recipe."""
+    return outlier_features(cfg.cfg_id, _T_GEMV_IN + M, _T_OUTLIER, M, k_in, 0, cfg.in_dtype)
+
+
+def random_features(seed: int, rows: int, cols: int, dtype: str = "fp16",
+                    outliers: int = N_OUTLIER, scale: float = OUTLIER_SCALE,
+                    std: float = 1.0) -> np.ndarray:
+    """Free-form seeded features for edge-case tests: N(0, std^2) with outliers."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([SEED, 1000, seed])))
+    x = g.standard_normal((rows, cols), dtype=np.float32) * np.float32(std)
+    if outliers and cols >= outliers:
+        ch = g.choice(cols, size=outliers, replace=False)
+        x[:, ch] *= np.float32(scale)
+    return encode(x, dtype)
