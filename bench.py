@@ -1,0 +1,230 @@
+"""Benchmark of the P4Q hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch:
+  1. quantization-aware selection: B x N visual tokens -> K kept + T text
+     (p4q_select), the pruned sequence X [M = B(K+T), h];
+  2. per-token int4 quantization of X, of the attention-output stand-in and
+     of the MLP-activation stand-in (p4q_quant_act);
+  3. the seven W4A4 linears of one decoder layer on those codes
+     (p4q_w4a4_linear): q/k/v/gate/up on X, o_proj, down_proj.
+Weights are quantized once, before timing (offline RTN, as in the paper).
+Four copies of the layer's weights rotate across steps so that successive
+steps read weights like successive decoder layers would (101 MB per layer at
+7B, i.e. not resident in the 256 MB MALL across the rotation).
+
+Prints ONE JSON line.  value = W4A4 linear ops of the step / step time (TOPS);
+the selector's token rate and the GEMM-only rate are reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+INT8_PEAK_TOPS = 5000.0      # MI355X dense int8 MFMA
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+N_WEIGHT_SETS = 4
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="next7b_b16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def setup(cfg, dev):
+    import torch
+    import paper_2609_34867_amd as p4q
+    from workload import selector_inputs, weight, attn_standin, mlp_standin
+
+    si = selector_inputs(cfg)
+    t = lambda a: torch.from_numpy(a).to(dev)
+    st = {
+        "vis": t(si.vis), "con": t(si.concepts), "text": t(si.text),
+        "attn": t(attn_standin(cfg)), "mlp": t(mlp_standin(cfg)),
+    }
+    st["idx"] = torch.empty((cfg.B, cfg.K), dtype=torch.int32, device=dev)
+    st["tok"] = torch.empty((cfg.B, cfg.K + cfg.T, cfg.d), dtype=torch.float16, device=dev)
+    st["ws"] = p4q.select_workspace(cfg.B, cfg.N, cfg.d, cfg.J, dev)
+    M = cfg.M
+    st["xq"] = (torch.empty((M, cfg.d // 2), dtype=torch.uint8, device=dev),
+                torch.empty((M,), dtype=torch.float32, device=dev))
+    st["aq"] = (torch.empty((M, cfg.d // 2), dtype=torch.uint8, device=dev),
+                torch.empty((M,), dtype=torch.float32, device=dev))
+    f = st["mlp"].shape[1]
+    st["mq"] = (torch.empty((M, f // 2), dtype=torch.uint8, device=dev),
+                torch.empty((M,), dtype=torch.float32, device=dev))
+    out_dt = torch.bfloat16 if cfg.out_dtype == "bf16" else torch.float16
+    weights = []
+    for li, lin in enumerate(cfg.linears):
+        wc, ws = p4q.quant_act(t(weight(cfg, li)))          # offline weight RTN
+        weights.append((wc, ws))
+    torch.cuda.synchronize()
+    st["weights"] = [[(wc.clone(), ws.clone()) for (wc, ws) in weights]
+                     for _ in range(N_WEIGHT_SETS)]
+    st["y"] = [torch.empty((M, lin.n_out), dtype=out_dt, device=dev) for lin in cfg.linears]
+    del weights
+    torch.cuda.synchronize()
+    return st
+
+
+def step(cfg, st, layer, ev=None):
+    """One hot-path pass.  With `ev`, records an event pair around each call."""
+    import paper_2609_34867_amd as p4q
+
+    def rec(name, fn):
+        if ev is None:
+            return fn()
+        e0, e1 = ev.pair(name)
+        e0.record()
+        r = fn()
+        e1.record()
+        return r
+
+    rec("select", lambda: p4q.select(st["vis"], st["con"], st["text"], cfg.K,
+                                     idx_out=st["idx"], tokens_out=st["tok"],
+                                     workspace=st["ws"]))
+    x = st["tok"].view(cfg.M, cfg.d)
+    rec("quant_act", lambda: p4q.quant_act(x, codes=st["xq"][0], scales=st["xq"][1]))
+    rec("quant_act", lambda: p4q.quant_act(st["attn"], codes=st["aq"][0], scales=st["aq"][1]))
+    rec("quant_act", lambda: p4q.quant_act(st["mlp"], codes=st["mq"][0], scales=st["mq"][1]))
+    W = st["weights"][layer % N_WEIGHT_SETS]
+    src = {"x": st["xq"], "attn": st["aq"], "mlp": st["mq"]}
+    for li, lin in enumerate(cfg.linears):
+        a = src[lin.source]
+        rec("gemm", lambda: p4q.w4a4_linear(a[0], a[1], W[li][0], W[li][1],
+                                            y=st["y"][li]))
+
+
+class Events:
+    def __init__(self):
+        self.pairs = []
+
+    def pair(self, name):
+        import torch
+        e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        self.pairs.append((name, e))
+        return e
+
+    def totals_ms(self):
+        out = {}
+        for name, (a, b) in self.pairs:
+            out[name] = out.get(name, 0.0) + a.elapsed_time(b)
+        return out
+
+
+def cpu_baseline(cfg):
+    """The oracle on a bounded sample of the same workload, scaled to the step:
+    one image's selection and 32 rows of every quantize + linear."""
+    import oracle
+    from workload import selector_inputs, weight, attn_standin, mlp_standin
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    si = selector_inputs(cfg, samples=[0])
+    t0 = time.perf_counter()
+    _, tok, _, _ = oracle.select(si.vis[0], si.concepts[0], si.text[0], cfg.K)
+    t_sel = time.perf_counter() - t0
+    rows = 32
+    xs = {"x": tok[:rows],
+          "attn": attn_standin(cfg, rows), "mlp": mlp_standin(cfg, rows)}
+    t_lin = 0.0
+    for li, lin in enumerate(cfg.linears):
+        wp, sw = oracle.quant_act(weight(cfg, li))        # offline, untimed
+        t0 = time.perf_counter()
+        ap, sa = oracle.quant_act(xs[lin.source])
+        oracle.w4a4_linear(ap, sa, wp, sw, cfg.out_dtype)
+        t_lin += time.perf_counter() - t0
+    t_full = cfg.B * t_sel + (cfg.M / rows) * t_lin
+    return {"value": round(cfg.linear_ops() / t_full / 1e12, 6), "unit": "TOPS",
+            "cores": threads, "kind": "oracle",
+            "sample": (f"1 of {cfg.B} images through the selector ({t_sel:.2f}s) and {rows} of "
+                       f"{cfg.M} rows through quantize + all 7 linears ({t_lin:.2f}s), "
+                       f"scaled to the full step ({t_full:.1f}s)")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU sharding is described in DESIGN.md, not run)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_34867_amd as p4q
+    from workload import CONFIGS
+
+    cfg = CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    st = setup(cfg, dev)
+    for i in range(args.warmup):
+        step(cfg, st, i)
+    torch.cuda.synchronize()
+
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step(cfg, st, i)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+
+    # per-call breakdown with HIP events on the launch stream (separate pass)
+    ev = Events()
+    for i in range(args.steps):
+        step(cfg, st, i, ev)
+    torch.cuda.synchronize()
+    tot = {k: v / args.steps for k, v in ev.totals_ms().items()}
+
+    ops = cfg.linear_ops()
+    gemm_ms = tot["gemm"]
+    gemm_tops = ops / (gemm_ms * 1e-3) / 1e12
+    sel_tokens = cfg.B * cfg.N
+    sel_bytes = (cfg.B * cfg.N * cfg.d * 2                      # read features once
+                 + cfg.B * cfg.K * cfg.d * 2                    # re-read kept rows
+                 + cfg.B * cfg.T * cfg.d * 2                    # text rows
+                 + cfg.M * cfg.d * 2)                           # write pruned sequence
+    sel_gbs = sel_bytes / (tot["select"] * 1e-3) / 1e9
+    res = {
+        "metric": "W4A4 GEMM TOPS (% int8 MFMA peak) + selector tokens/s, LLaVA-NeXT-7B shape",
+        "value": round(ops / (ms * 1e-3) / 1e12, 3),
+        "unit": "TOPS",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int4 (int8 MFMA, int32 acc)", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: select K={cfg.K} of N={cfg.N} tokens x d={cfg.d} "
+                               f"fp16 for B={cfg.B} images + T={cfg.T} text, then 7 W4A4 "
+                               f"linears (h={cfg.d}, f={cfg.linears[4].n_out}) at M={cfg.M}, "
+                               f"{cfg.out_dtype} out",
+                   "B": cfg.B, "N": cfg.N, "d": cfg.d, "K": cfg.K, "T": cfg.T, "J": cfg.J,
+                   "M": cfg.M, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
+                     "unit": "TOPS", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
+                     "traffic": None, "kernel": "k_w4a4_gemm",
+                     "per_launch": "2*M*n_out*k_in int ops; 7 launches per step"},
+        "gemm_tops": round(gemm_tops, 2),
+        "selector_tokens_per_s": round(sel_tokens / (tot["select"] * 1e-3), 1),
+        "selector_gbs": round(sel_gbs, 1),
+        "selector_hbm_frac": round(sel_gbs / HBM_PEAK_GBS, 4),
+        "breakdown_ms": {k: round(v, 4) for k, v in tot.items()},
+        "lib": p4q.version(),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

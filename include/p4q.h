@@ -1,0 +1,146 @@
+/*
+ * p4q.h -- C ABI of the P4Q hot path on MI355X (gfx950).
+ *
+ * P4Q (co-designed visual-token pruning and W4A4 quantization) has two
+ * data-parallel steps on its inference path:
+ *   1. a quantization-aware visual-token selector placed before the LLM
+ *      (Sec. 3.2, Eq. p4q_progressive_selection): projector features and
+ *      query-concept embeddings are fake-quantized, visual tokens are ranked
+ *      per concept by the cosine similarity of those copies, the top tokens
+ *      within each concept's quota are kept, and the ORIGINAL feature rows of
+ *      the kept tokens are forwarded with the text tokens;
+ *   2. the W4A4 linear layers of the LLM on that pruned sequence (Appendix A
+ *      and B.3: symmetric round-to-nearest, per-output-channel 4-bit weights,
+ *      per-token 4-bit activations, no groups, activation clip 1.0).
+ *
+ * Conventions shared by every entry point
+ *   - Every call is asynchronous and ordered on the caller's `stream`.
+ *     Argument checks run on the host before any HIP call; a failing check
+ *     returns a status and enqueues nothing.  A launch failure returns
+ *     P4Q_ERR_HIP.  No call synchronizes the device.
+ *   - All pointers are device pointers owned by the caller.  The library
+ *     keeps no pointer after it returns and allocates no device memory.
+ *   - Matrices are row-major.  fp16 / bf16 tensors are IEEE binary16 /
+ *     bfloat16 bit patterns.
+ *   - The 4-bit quantizer Q4(x; c) of a row x (Appendix A, B.3):
+ *         a = max_k |x_k|,  s = fl32(fl32(c * a) / 7),
+ *         code_k = clamp(rne(fl32(x_k / s)), -8, 7)  (correctly rounded
+ *         division, ties to even);  s == 0  =>  all codes 0.
+ *     Packed codes hold two's-complement nibbles, the even k in the low
+ *     nibble: byte t = (code[2t] & 0xF) | (code[2t+1] & 0xF) << 4.
+ *   - The last error message of the calling thread is p4q_last_error().
+ */
+#ifndef P4Q_H
+#define P4Q_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum p4q_status {
+    P4Q_OK = 0,
+    P4Q_ERR_INVALID_ARG = 1,   /* null pointer, bad size, misalignment, bad clip */
+    P4Q_ERR_UNSUPPORTED = 2,   /* valid request outside what the kernels handle */
+    P4Q_ERR_WORKSPACE = 3,     /* workspace missing or too small */
+    P4Q_ERR_HIP = 4            /* a HIP launch or runtime call failed */
+} p4q_status;
+
+typedef enum p4q_dtype {
+    P4Q_FP16 = 0,
+    P4Q_BF16 = 1
+} p4q_dtype;
+
+/* Library version string, e.g. "p4q 0.1.0 gfx950". */
+const char *p4q_version(void);
+
+/* Human-readable name of a status code. */
+const char *p4q_status_string(int status);
+
+/* Message describing the last failing call on this thread ("" if none). */
+const char *p4q_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Quantization-aware visual-token selection (Sec. 3.2, Query Relevance).
+ *
+ * For each sample b < B:
+ *   - cv_i = Q4(vis[b][i]; clip) and cq_j = Q4(concepts[b][j]; clip) are the
+ *     fake-quantized copies (only their integer codes are needed: with
+ *     v~ = s_v cv and q~ = s_q cq, CosSim(q~_j, v~_i) = D_ij / sqrt(Nv_i Nq_j)
+ *     with D_ij = <cv_i, cq_j> and Nv_i = |cv_i|^2, exactly);
+ *   - concept j ranks tokens by that cosine, higher first, equal cosines by
+ *     lower token index (a zero code vector has cosine 0);
+ *   - quotas k_j = floor(K/J) + (j < K mod J); for j = 0..J-1 in order, the
+ *     first k_j tokens of concept j's ranking not already kept are kept
+ *     (the Query-Relevance stage holding the whole budget);
+ *   - idx_out[b][0..K) = kept token indices in ascending order;
+ *   - tokens_out[b] = [vis[b][idx_out[b][0]], ..., vis[b][idx_out[b][K-1]],
+ *                      text[b][0], ..., text[b][T-1]]  (bitwise copies of the
+ *     original rows: the quantized copies are never materialized).
+ *
+ * Layouts:  vis [B, N, d], concepts [B, J, d], text [B, T, d] (dtype dt),
+ *           idx_out int32 [B, K], tokens_out [B, K + T, d] (dtype dt).
+ * Workspace: at least p4q_select_workspace_bytes(B, N, d, J) bytes, 256-byte
+ *   aligned.  Its first B*N*(J+1) int32 hold, per token, D_i0 .. D_i(J-1)
+ *   then Nv_i (layout [B][N][J+1]); the rest is internal.
+ * Limits: 1 <= K <= N <= 8192, 1 <= J <= 8, J * d <= 65536, T >= 0 (text
+ *   may be NULL iff T == 0), d % 32 == 0, 32 <= d <= 16384, clip in
+ *   [2^-16, 1]; pointers 16-byte aligned.
+ * Errors: P4Q_ERR_INVALID_ARG / P4Q_ERR_UNSUPPORTED / P4Q_ERR_WORKSPACE as
+ *   above; nothing is enqueued on error.
+ * ---------------------------------------------------------------------- */
+size_t p4q_select_workspace_bytes(int B, int N, int d, int J);
+
+int p4q_select(p4q_dtype dt, int B, int N, int d,
+               const void *vis, const void *concepts, int J,
+               const void *text, int T, int K, float clip,
+               int32_t *idx_out, void *tokens_out,
+               void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Per-row activation quantization + packing (Appendix A / B.3: per-token
+ * int4 activations; the same call quantizes weight rows per output channel).
+ *
+ *   (codes[m], scales[m]) = Q4(x[m, 0..K_in); clip)   for m < M
+ *
+ * Layouts: x [M, ldx] (dtype dt, only the first K_in columns are read),
+ *          codes uint8 [M, K_in/2] packed (see above), scales fp32 [M].
+ * Limits: M >= 1, K_in % 32 == 0, 32 <= K_in <= 65536, ldx >= K_in,
+ *   ldx % 8 == 0, clip in [2^-16, 1]; x and codes 16-byte aligned, scales
+ *   4-byte aligned.
+ * ---------------------------------------------------------------------- */
+int p4q_quant_act(p4q_dtype dt, int M, int K_in, const void *x, int64_t ldx,
+                  float clip, uint8_t *codes, float *scales, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * W4A4 linear (Appendix B.3: RTN int4 weights and activations for W4A4
+ * inference): an integer GEMM on the codes and a dequant epilogue.
+ *
+ *   acc[m][n] = sum_k A[m][k] * W[n][k]                (exact int32)
+ *   y[m][n]   = out_rne(fl32(fl32(float(acc) * a_scales[m]) * w_scales[n]))
+ *
+ * Layouts: a_codes uint8 [M, K_in/2] and w_codes uint8 [N_out, K_in/2]
+ *   packed as above (both K-contiguous); a_scales fp32 [M]; w_scales fp32
+ *   [N_out]; y [M, ldy] of out_dt; acc_out int32 [M, N_out] or NULL (when
+ *   given, the raw accumulators are stored too).
+ * Workspace: p4q_w4a4_linear_workspace_bytes(M, N_out, K_in) bytes (may be
+ *   0; ws may then be NULL).
+ * Limits: M >= 1, N_out >= 1, K_in % 32 == 0, 32 <= K_in <= 131072,
+ *   ldy >= N_out; code pointers 16-byte aligned, y 4-byte aligned.
+ * ---------------------------------------------------------------------- */
+size_t p4q_w4a4_linear_workspace_bytes(int M, int N_out, int K_in);
+
+int p4q_w4a4_linear(int M, int N_out, int K_in,
+                    const uint8_t *a_codes, const float *a_scales,
+                    const uint8_t *w_codes, const float *w_scales,
+                    p4q_dtype out_dt, void *y, int64_t ldy, int32_t *acc_out,
+                    void *ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* P4Q_H */

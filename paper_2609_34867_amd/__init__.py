@@ -1,0 +1,11 @@
+"""P4Q hot path on MI355X: quantization-aware visual-token selection and W4A4
+linear layers, as hand-written gfx950 HIP kernels behind the C ABI in
+include/p4q.h.  This package only marshals torch tensors (device memory and
+the current stream) into those calls; every step runs in libp4q.so.
+"""
+from ._lib import P4QError, lib, LIB_PATH  # noqa: F401
+from .api import (select, select_workspace, quant_act, w4a4_linear,  # noqa: F401
+                  w4a4_linear_workspace, version)
+
+__all__ = ["select", "select_workspace", "quant_act", "w4a4_linear", "w4a4_linear_workspace",
+           "version", "P4QError", "lib", "LIB_PATH"]

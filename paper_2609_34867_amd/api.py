@@ -1,0 +1,135 @@
+"""torch-facing wrappers of the libp4q C ABI.
+
+Only argument marshalling happens here: shape / dtype checks, output
+allocation with torch (device memory), and passing the current HIP stream.
+All computation runs in the library's kernels.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Tuple
+
+import torch
+
+from ._lib import P4Q_BF16, P4Q_FP16, check, lib
+
+
+def version() -> str:
+    return lib().p4q_version().decode()
+
+
+def _dtype_code(t: torch.dtype) -> int:
+    if t == torch.float16:
+        return P4Q_FP16
+    if t == torch.bfloat16:
+        return P4Q_BF16
+    raise TypeError(f"unsupported dtype {t} (fp16 or bf16)")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(dev: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def _need_gpu(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("p4q tensors must live on the GPU")
+
+
+# --------------------------------------------------------------------------- selector
+def select_workspace(B: int, N: int, d: int, J: int, device) -> torch.Tensor:
+    """Workspace for select(); its first B*N*(J+1) int32 hold D and Nv per token."""
+    n = lib().p4q_select_workspace_bytes(B, N, d, J)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def select(vis: torch.Tensor, concepts: torch.Tensor, text: Optional[torch.Tensor], K: int,
+           clip: float = 1.0, idx_out: Optional[torch.Tensor] = None,
+           tokens_out: Optional[torch.Tensor] = None,
+           workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Quantization-aware Query-Relevance selection (p4q_select).
+
+    vis [B, N, d], concepts [B, J, d], text [B, T, d] or None; returns
+    (idx int32 [B, K] ascending, tokens [B, K+T, d] = kept original rows + text)."""
+    _need_gpu(vis, concepts, text)
+    B, N, d = vis.shape
+    J = concepts.shape[1]
+    T = 0 if text is None else text.shape[1]
+    if concepts.shape != (B, J, d) or (text is not None and text.shape != (B, T, d)):
+        raise ValueError("shape mismatch between vis, concepts and text")
+    for t in (vis, concepts, text):
+        if t is not None and (t.dtype != vis.dtype or not t.is_contiguous()):
+            raise ValueError("vis/concepts/text must be contiguous and share a dtype")
+    dev = vis.device
+    if idx_out is None:
+        idx_out = torch.empty((B, K), dtype=torch.int32, device=dev)
+    if tokens_out is None:
+        tokens_out = torch.empty((B, K + T, d), dtype=vis.dtype, device=dev)
+    if workspace is None:
+        workspace = select_workspace(B, N, d, J, dev)
+    st = lib().p4q_select(_dtype_code(vis.dtype), B, N, d, _ptr(vis), _ptr(concepts), J,
+                          _ptr(text) if T > 0 else None, T, K, ctypes.c_float(clip),
+                          _ptr(idx_out), _ptr(tokens_out), _ptr(workspace),
+                          workspace.numel() * workspace.element_size(), _stream(dev))
+    check(st)
+    return idx_out, tokens_out
+
+
+# --------------------------------------------------------------------------- quantizer
+def quant_act(x: torch.Tensor, clip: float = 1.0, codes: Optional[torch.Tensor] = None,
+              scales: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Per-row int4 quantize + pack (p4q_quant_act): x [M, K_in] (row stride may
+    exceed K_in) -> (codes uint8 [M, K_in/2], scales fp32 [M])."""
+    _need_gpu(x)
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be 2-D with unit column stride")
+    M, K_in = x.shape
+    if codes is None:
+        codes = torch.empty((M, K_in // 2), dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty((M,), dtype=torch.float32, device=x.device)
+    st = lib().p4q_quant_act(_dtype_code(x.dtype), M, K_in, _ptr(x), x.stride(0),
+                             ctypes.c_float(clip), _ptr(codes), _ptr(scales),
+                             _stream(x.device))
+    check(st)
+    return codes, scales
+
+
+# --------------------------------------------------------------------------- W4A4 linear
+def w4a4_linear_workspace(M: int, N_out: int, K_in: int, device) -> Optional[torch.Tensor]:
+    n = lib().p4q_w4a4_linear_workspace_bytes(M, N_out, K_in)
+    return None if n == 0 else torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def w4a4_linear(a_codes: torch.Tensor, a_scales: torch.Tensor, w_codes: torch.Tensor,
+                w_scales: torch.Tensor, out_dtype: torch.dtype = torch.bfloat16,
+                y: Optional[torch.Tensor] = None, acc_out: Optional[torch.Tensor] = None,
+                return_acc: bool = False, workspace: Optional[torch.Tensor] = None):
+    """W4A4 linear (p4q_w4a4_linear): a_codes [M, K_in/2], w_codes [N_out, K_in/2]
+    -> y [M, N_out] (out_dtype); also the int32 accumulators when return_acc."""
+    _need_gpu(a_codes, a_scales, w_codes, w_scales)
+    M, kb = a_codes.shape
+    N_out, kb2 = w_codes.shape
+    if kb != kb2:
+        raise ValueError("a_codes and w_codes disagree on K_in")
+    for t in (a_codes, w_codes, a_scales, w_scales):
+        if not t.is_contiguous():
+            raise ValueError("operands must be contiguous")
+    K_in = 2 * kb
+    dev = a_codes.device
+    if y is None:
+        y = torch.empty((M, N_out), dtype=out_dtype, device=dev)
+    if return_acc and acc_out is None:
+        acc_out = torch.empty((M, N_out), dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = w4a4_linear_workspace(M, N_out, K_in, dev)
+    ws_bytes = 0 if workspace is None else workspace.numel()
+    st = lib().p4q_w4a4_linear(M, N_out, K_in, _ptr(a_codes), _ptr(a_scales), _ptr(w_codes),
+                               _ptr(w_scales), _dtype_code(y.dtype), _ptr(y), y.stride(0),
+                               _ptr(acc_out), _ptr(workspace), ws_bytes, _stream(dev))
+    check(st)
+    return (y, acc_out) if return_acc else y

@@ -1,0 +1,139 @@
+// C ABI of libp4q (declared in include/p4q.h): argument validation, workspace
+// sizing and dispatch.  Every check runs on the host before any HIP call, so a
+// rejected call enqueues nothing; launch failures map to P4Q_ERR_HIP.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "p4q_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int ok() {
+    g_last_error[0] = '\0';
+    return P4Q_OK;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool valid_dtype(int dt) { return dt == P4Q_FP16 || dt == P4Q_BF16; }
+
+// clip in [2^-16, 1]; NaN fails both comparisons
+bool valid_clip(float c) { return c >= 0x1p-16f && c <= 1.0f; }
+
+int hip_status(hipError_t e, const char *what) {
+    if (e != hipSuccess)
+        return fail(P4Q_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *p4q_version(void) { return "p4q 0.1.0 gfx950"; }
+
+const char *p4q_status_string(int status) {
+    switch (status) {
+        case P4Q_OK: return "P4Q_OK";
+        case P4Q_ERR_INVALID_ARG: return "P4Q_ERR_INVALID_ARG";
+        case P4Q_ERR_UNSUPPORTED: return "P4Q_ERR_UNSUPPORTED";
+        case P4Q_ERR_WORKSPACE: return "P4Q_ERR_WORKSPACE";
+        case P4Q_ERR_HIP: return "P4Q_ERR_HIP";
+        default: return "P4Q_ERR_UNKNOWN";
+    }
+}
+
+const char *p4q_last_error(void) { return g_last_error; }
+
+size_t p4q_select_workspace_bytes(int B, int N, int d, int J) {
+    if (B <= 0 || N <= 0 || d <= 0 || J <= 0) return 0;
+    return p4q::select_workspace_bytes(B, N, d, J);
+}
+
+int p4q_select(p4q_dtype dt, int B, int N, int d, const void *vis, const void *concepts, int J,
+               const void *text, int T, int K, float clip, int32_t *idx_out, void *tokens_out,
+               void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: dtype %d", (int)dt);
+    if (B <= 0 || N <= 0 || d <= 0 || J <= 0 || K <= 0 || T < 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select: sizes must be positive (B=%d N=%d d=%d J=%d K=%d T=%d)",
+                    B, N, d, J, K, T);
+    if (K > N) return fail(P4Q_ERR_INVALID_ARG, "p4q_select: K=%d > N=%d", K, N);
+    if (!vis || !concepts || !idx_out || !tokens_out)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select: null pointer");
+    if ((T > 0) != (text != nullptr))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select: text must be given iff T > 0");
+    if (!valid_clip(clip)) return fail(P4Q_ERR_INVALID_ARG, "p4q_select: clip %g outside [2^-16, 1]", clip);
+    if (d % 32 != 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_select: d=%d not a multiple of 32", d);
+    if (!aligned(vis, 16) || !aligned(concepts, 16) || !aligned(tokens_out, 16) ||
+        (text && !aligned(text, 16)) || !aligned(idx_out, 4))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select: misaligned pointer");
+    if (N > 8192) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: N=%d > 8192", N);
+    if (J > 8) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: J=%d > 8", J);
+    if (d > 16384) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: d=%d > 16384", d);
+    if ((int64_t)J * d > 65536) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: J*d > 65536");
+    const size_t need = p4q::select_workspace_bytes(B, N, d, J);
+    if (!ws || ws_bytes < need)
+        return fail(P4Q_ERR_WORKSPACE, "p4q_select: workspace %zu < %zu bytes", ws_bytes, need);
+    if (!aligned(ws, 256)) return fail(P4Q_ERR_INVALID_ARG, "p4q_select: workspace not 256-byte aligned");
+    const p4q::SelectWorkspace w = p4q::select_workspace_carve(ws, B, N, d, J);
+    return hip_status(p4q::launch_select(dt, B, N, d, vis, concepts, J, text, T, K, clip, idx_out,
+                                         tokens_out, w, stream),
+                      "p4q_select");
+}
+
+int p4q_quant_act(p4q_dtype dt, int M, int K_in, const void *x, int64_t ldx, float clip,
+                  uint8_t *codes, float *scales, hipStream_t stream) {
+    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_quant_act: dtype %d", (int)dt);
+    if (M <= 0 || K_in <= 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_act: M=%d K_in=%d", M, K_in);
+    if (K_in % 32 != 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_act: K_in=%d not a multiple of 32", K_in);
+    if (K_in > 65536) return fail(P4Q_ERR_UNSUPPORTED, "p4q_quant_act: K_in=%d > 65536", K_in);
+    if (ldx < K_in || ldx % 8 != 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_act: ldx=%lld (need >= K_in, multiple of 8)", (long long)ldx);
+    if (!x || !codes || !scales) return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_act: null pointer");
+    if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_act: misaligned pointer");
+    if (!valid_clip(clip)) return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_act: clip %g outside [2^-16, 1]", clip);
+    return hip_status(p4q::launch_quant_act(dt, M, K_in, x, ldx, clip, codes, scales, stream),
+                      "p4q_quant_act");
+}
+
+size_t p4q_w4a4_linear_workspace_bytes(int M, int N_out, int K_in) {
+    if (M <= 0 || N_out <= 0 || K_in <= 0) return 0;
+    return p4q::gemm_workspace_bytes(M, N_out, K_in);
+}
+
+int p4q_w4a4_linear(int M, int N_out, int K_in, const uint8_t *a_codes, const float *a_scales,
+                    const uint8_t *w_codes, const float *w_scales, p4q_dtype out_dt, void *y,
+                    int64_t ldy, int32_t *acc_out, void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (!valid_dtype(out_dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_w4a4_linear: dtype %d", (int)out_dt);
+    if (M <= 0 || N_out <= 0 || K_in <= 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_w4a4_linear: M=%d N_out=%d K_in=%d", M, N_out, K_in);
+    if (K_in % 32 != 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_w4a4_linear: K_in=%d not a multiple of 32", K_in);
+    if (K_in > 131072) return fail(P4Q_ERR_UNSUPPORTED, "p4q_w4a4_linear: K_in=%d > 131072", K_in);
+    if (ldy < N_out) return fail(P4Q_ERR_INVALID_ARG, "p4q_w4a4_linear: ldy=%lld < N_out", (long long)ldy);
+    if (!a_codes || !a_scales || !w_codes || !w_scales || !y)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_w4a4_linear: null pointer");
+    if (!aligned(a_codes, 16) || !aligned(w_codes, 16) || !aligned(y, 4) || !aligned(a_scales, 4) ||
+        !aligned(w_scales, 4) || (acc_out && !aligned(acc_out, 4)))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_w4a4_linear: misaligned pointer");
+    if ((int64_t)M > 65535LL * 128) return fail(P4Q_ERR_UNSUPPORTED, "p4q_w4a4_linear: M too large");
+    const size_t need = p4q::gemm_workspace_bytes(M, N_out, K_in);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(P4Q_ERR_WORKSPACE, "p4q_w4a4_linear: workspace %zu < %zu bytes", ws_bytes, need);
+    return hip_status(p4q::launch_w4a4_gemm(M, N_out, K_in, a_codes, a_scales, w_codes, w_scales,
+                                            out_dt, y, ldy, acc_out, ws, ws_bytes, stream),
+                      "p4q_w4a4_linear");
+}
+
+}  // extern "C"

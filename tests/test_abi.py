@@ -1,0 +1,133 @@
+"""The C ABI library loads, exports every symbol include/p4q.h declares, and
+rejects bad arguments on the host before any HIP call (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_34867_amd import _lib as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "p4q.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH),
+                                reason="libp4q.so not built (run __graft_entry__.build())")
+
+ALIGNED = 0x10000       # fake device addresses: only validated, never dereferenced
+F = ctypes.c_float
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(p4q_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    lib = L.lib()
+    names = declared_functions()
+    assert len(names) >= 8
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(L.SIGNATURES), "binding signatures out of sync with the header"
+
+
+def test_version_and_status_strings():
+    lib = L.lib()
+    assert b"gfx950" in lib.p4q_version()
+    assert lib.p4q_status_string(0) == b"P4Q_OK"
+    assert lib.p4q_status_string(3) == b"P4Q_ERR_WORKSPACE"
+    assert lib.p4q_status_string(99) == b"P4Q_ERR_UNKNOWN"
+
+
+def quant(**kw):
+    a = dict(dt=0, M=4, K=64, x=ALIGNED, ldx=64, clip=1.0, codes=ALIGNED, scales=ALIGNED)
+    a.update(kw)
+    return L.lib().p4q_quant_act(a["dt"], a["M"], a["K"], a["x"], a["ldx"], F(a["clip"]),
+                                 a["codes"], a["scales"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(M=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=48), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=65536 + 32, ldx=65568), L.P4Q_ERR_UNSUPPORTED),
+    (dict(ldx=32), L.P4Q_ERR_INVALID_ARG),
+    (dict(ldx=68), L.P4Q_ERR_INVALID_ARG),
+    (dict(x=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(x=ALIGNED + 8), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip=0.0), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip=1.5), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip=float("nan")), L.P4Q_ERR_INVALID_ARG),
+    (dict(dt=7), L.P4Q_ERR_UNSUPPORTED),
+])
+def test_quant_act_validation(kw, status):
+    assert quant(**kw) == status
+    assert L.lib().p4q_last_error() != b""
+
+
+def select(**kw):
+    a = dict(dt=0, B=1, N=64, d=64, vis=ALIGNED, con=ALIGNED, J=2, text=ALIGNED, T=4, K=8,
+             clip=1.0, idx=ALIGNED, tok=ALIGNED, ws=ALIGNED, ws_bytes=1 << 30)
+    a.update(kw)
+    return L.lib().p4q_select(a["dt"], a["B"], a["N"], a["d"], a["vis"], a["con"], a["J"],
+                              a["text"], a["T"], a["K"], F(a["clip"]), a["idx"], a["tok"],
+                              a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(K=65), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(J=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(J=9), L.P4Q_ERR_UNSUPPORTED),
+    (dict(d=48), L.P4Q_ERR_INVALID_ARG),
+    (dict(N=9000, K=8), L.P4Q_ERR_UNSUPPORTED),
+    (dict(text=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(T=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(vis=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(vis=ALIGNED + 4), L.P4Q_ERR_INVALID_ARG),
+    (dict(ws=None), L.P4Q_ERR_WORKSPACE),
+    (dict(ws_bytes=100), L.P4Q_ERR_WORKSPACE),
+    (dict(ws=ALIGNED + 16), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip=2.0), L.P4Q_ERR_INVALID_ARG),
+    (dict(dt=2), L.P4Q_ERR_UNSUPPORTED),
+    (dict(J=8, d=16384), L.P4Q_ERR_UNSUPPORTED),
+])
+def test_select_validation(kw, status):
+    assert select(**kw) == status
+
+
+def test_select_workspace_size_covers_documented_stats():
+    n = L.lib().p4q_select_workspace_bytes(16, 2880, 4096, 4)
+    assert n >= 16 * 2880 * 5 * 4
+    assert L.lib().p4q_select_workspace_bytes(0, 1, 1, 1) == 0
+
+
+def linear(**kw):
+    a = dict(M=4, N=8, K=64, a=ALIGNED, sa=ALIGNED, w=ALIGNED, sw=ALIGNED, dt=1, y=ALIGNED,
+             ldy=8, acc=None, ws=None, ws_bytes=0)
+    a.update(kw)
+    return L.lib().p4q_w4a4_linear(a["M"], a["N"], a["K"], a["a"], a["sa"], a["w"], a["sw"],
+                                   a["dt"], a["y"], a["ldy"], a["acc"], a["ws"], a["ws_bytes"],
+                                   None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(M=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(N=-1), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=40), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=131072 + 32), L.P4Q_ERR_UNSUPPORTED),
+    (dict(ldy=4), L.P4Q_ERR_INVALID_ARG),
+    (dict(a=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(w=ALIGNED + 1), L.P4Q_ERR_INVALID_ARG),
+    (dict(y=ALIGNED + 2), L.P4Q_ERR_INVALID_ARG),
+    (dict(dt=5), L.P4Q_ERR_UNSUPPORTED),
+])
+def test_linear_validation(kw, status):
+    assert linear(**kw) == status
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    import paper_2609_34867_amd as p4q
+    with pytest.raises(ValueError):
+        p4q.quant_act(torch.zeros(4, 64, dtype=torch.float16))

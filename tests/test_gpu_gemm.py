@@ -1,0 +1,107 @@
+"""GPU parity of p4q_w4a4_linear against the oracle: int32 accumulators and
+fp16/bf16 outputs must match bit for bit (the epilogue's operation order is
+fixed, so 'within 1e-3 relative' is met with zero error)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_34867_amd as p4q
+from workload import CONFIGS, random_features, weight, attn_standin
+from gpu_util import to_gpu, to_np, bits, first_mismatch
+
+pytestmark = pytest.mark.gpu
+
+
+def codes_for(M, N, K, seed, extreme=None):
+    rng = np.random.default_rng(seed)
+    if extreme is None:
+        a = rng.integers(-8, 8, size=(M, K)).astype(np.int8)
+        w = rng.integers(-8, 8, size=(N, K)).astype(np.int8)
+    else:
+        a = np.full((M, K), extreme, dtype=np.int8)
+        w = np.full((N, K), extreme, dtype=np.int8)
+    sa = rng.uniform(1e-3, 4, size=M).astype(np.float32)
+    sw = rng.uniform(1e-4, 3e-2, size=N).astype(np.float32)
+    return oracle.pack_int4(a), sa, oracle.pack_int4(w), sw
+
+
+def run_gpu(ap, sa, wp, sw, out_dtype):
+    tdt = torch.float16 if out_dtype == "fp16" else torch.bfloat16
+    y, acc = p4q.w4a4_linear(to_gpu(ap), to_gpu(sa), to_gpu(wp), to_gpu(sw), tdt,
+                             return_acc=True)
+    torch.cuda.synchronize()
+    return to_np(y), to_np(acc)
+
+
+def check_full(ap, sa, wp, sw, out_dtype):
+    y, acc = run_gpu(ap, sa, wp, sw, out_dtype)
+    racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, out_dtype)
+    assert (m := first_mismatch(acc, racc.astype(np.int32))) is None, m
+    assert (m := first_mismatch(bits(y), bits(ry))) is None, m
+
+
+@pytest.mark.parametrize("out_dtype", ["fp16", "bf16"])
+@pytest.mark.parametrize("shape", [(1, 1, 32), (5, 17, 96), (16, 16, 128), (130, 250, 288),
+                                   (127, 129, 4096), (256, 384, 1024), (1, 4096, 4096),
+                                   (4, 300, 11008), (300, 64, 13824), (257, 129, 5120)])
+def test_shapes(shape, out_dtype):
+    M, N, K = shape
+    check_full(*codes_for(M, N, K, M * 7 + N), out_dtype)
+
+
+@pytest.mark.parametrize("extreme", [-8, 7])
+def test_extreme_codes_large_K(extreme):
+    """|acc| = 64 * K at K = 65536 (and 49 K with +7): checks the int32 range of
+    the scaled MFMA accumulation."""
+    check_full(*codes_for(40, 36, 65536, 3, extreme), "bf16")
+
+
+def test_strided_output():
+    ap, sa, wp, sw = codes_for(33, 40, 256, 9)
+    y = torch.full((33, 48), -1.0, dtype=torch.bfloat16, device="cuda")
+    p4q.w4a4_linear(to_gpu(ap), to_gpu(sa), to_gpu(wp), to_gpu(sw), y=y)
+    torch.cuda.synchronize()
+    _, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
+    got = to_np(y)
+    assert np.array_equal(bits(got[:, :40]), bits(ry))
+    assert np.all(bits(got[:, 40:]) == 0xBF80)           # -1.0 untouched
+
+
+def test_quantized_pipeline_tiny():
+    """quant_act -> w4a4_linear on the tiny config's real recipe (fp16 out)."""
+    cfg = CONFIGS["tiny"]
+    x = random_features(5, cfg.M, 4096)
+    w = weight(cfg, 0)
+    xq = p4q.quant_act(to_gpu(x))
+    wq = p4q.quant_act(to_gpu(w))
+    y, acc = p4q.w4a4_linear(*xq, *wq, torch.float16, return_acc=True)
+    torch.cuda.synchronize()
+    ap, sa = oracle.quant_act(x)
+    wp, sw = oracle.quant_act(w)
+    racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, "fp16")
+    assert np.array_equal(to_np(acc), racc.astype(np.int32))
+    assert np.array_equal(bits(to_np(y)), bits(ry))
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("li", [0, 4, 6])
+def test_llava_next_b16_linears_sampled(li):
+    """q_proj (4096x4096), gate_proj (11008x4096) and down_proj (4096x11008) at
+    M = 11264 in one launch each; rows 0..63, the last 64 rows and 1024 random
+    entries are checked against the oracle."""
+    cfg = CONFIGS["next7b_b16"]
+    lin = cfg.linears[li]
+    rng = np.random.default_rng(li)
+    ap = rng.integers(0, 256, size=(cfg.M, lin.k_in // 2), dtype=np.uint8)
+    sa = rng.uniform(1e-3, 4, size=cfg.M).astype(np.float32)
+    wp, sw = oracle.quant_act(weight(cfg, li))
+    y, acc = run_gpu(ap, sa, wp, sw, "bf16")
+    for rows in (slice(0, 64), slice(cfg.M - 64, cfg.M)):
+        racc, ry = oracle.w4a4_linear(ap[rows], sa[rows], wp, sw, "bf16")
+        assert (m := first_mismatch(acc[rows], racc.astype(np.int32))) is None, m
+        assert (m := first_mismatch(bits(y[rows]), bits(ry))) is None, m
+    for _ in range(1024):
+        m, n = int(rng.integers(cfg.M)), int(rng.integers(lin.n_out))
+        racc, ry = oracle.w4a4_linear_entry(ap, sa, wp, sw, m, n, "bf16")
+        assert acc[m, n] == racc and bits(y)[m, n] == ry
