@@ -212,7 +212,7 @@ def main():
                    "M": cfg.M, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
                      "unit": "TOPS", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
-                     "traffic": None, "kernel": "k_w4a4_gemm",
+                     "traffic": None, "kernel": "k_w4a4_gemm_t256",
                      "per_launch": "2*M*n_out*k_in int ops; 7 launches per step"},
         "gemm_tops": round(gemm_tops, 2),
         "selector_tokens_per_s": round(sel_tokens / (tot["select"] * 1e-3), 1),

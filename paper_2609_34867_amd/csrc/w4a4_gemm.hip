@@ -19,6 +19,8 @@ namespace p4q {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
 
 constexpr int BM = 128, BN = 128;
 constexpr int BKB = 64;            // packed bytes of k per stage (128 k values)
@@ -153,6 +155,271 @@ __global__ __launch_bounds__(kThreads) void k_w4a4_gemm(const uint8_t *__restric
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Large-M kernel: 256 x 256 block tile, 4 wavefronts of 128 x 128 (8 x 8 MFMA
+// tiles, 256 accumulator registers per lane).
+//  * Packed int4 tiles go straight from HBM to LDS (buffer_load ... lds): no
+//    staging registers and no LDS store instructions.  Out-of-range rows and
+//    k-chunks are zero-filled by the buffer's range check.  A ring of 4 LDS
+//    stages (32 KB each) keeps 3 k-tiles in flight; waits are explicit
+//    (vmcnt + a bare s_barrier).
+//  * After the LDS read each wave unpacks its fragments to int8 in registers.
+//  * The weight fragment is the MFMA's first operand: lane l then owns four
+//    consecutive output columns n of one row m, stored as one 8-byte write.
+//  * Work-group ids are remapped so that each XCD (ids are dealt round-robin
+//    over 8 XCDs) walks a contiguous, M-grouped range of tiles, sharing A and
+//    W panels in its own L2.
+// ---------------------------------------------------------------------------
+constexpr int L_BM = 256, L_BN = 256;
+constexpr int L_STAGES = 4;
+constexpr int L_STAGE = (L_BM + L_BN) * BKB;     // 32 KB of packed codes
+constexpr int kXcds = 8;
+constexpr int kGroupM = 8;
+
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+
+// Buffer descriptor of a raw byte range (stride 0, range-checked: loads past
+// `bytes` return zeros).
+__device__ __forceinline__ v4i buffer_desc(const void *base, uint32_t bytes) {
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    return v4i{(int)(uint32_t)b, (int)((b >> 32) & 0xFFFFu), (int)bytes, 0x00020000};
+}
+
+// 16 bytes per lane from a buffer straight into LDS at lds + 16 * lane.  Issued
+// as inline asm so the compiler does not add its conservative vmcnt(0) before
+// every LDS read (it cannot tell the ring slots apart); the kernel waits with
+// explicit vmcnt counts instead.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(v4i desc, uint32_t voffset, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voffset), "s"(desc), "s"(lds_addr)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)(size_t)(lds_ptr_t)p;
+}
+
+__device__ __forceinline__ void tile_coords(int wg, int tiles_m, int tiles_n, int &tm, int &tn) {
+    const int T = tiles_m * tiles_n;
+    const int q = T / kXcds, r = T % kXcds;
+    const int x = wg % kXcds, i = wg / kXcds;
+    const int logical = (x < r) ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+    const int per_group = kGroupM * tiles_n;
+    const int g = logical / per_group;
+    const int first_m = g * kGroupM;
+    const int gsize = min(tiles_m - first_m, kGroupM);
+    const int in_g = logical - g * per_group;
+    tm = first_m + in_g % gsize;
+    tn = in_g / gsize;
+}
+
+template <bool BF16OUT>
+__global__ __launch_bounds__(256, 1) void k_w4a4_gemm_t256(const uint8_t *__restrict__ A,
+                                                           const float *__restrict__ sa,
+                                                           const uint8_t *__restrict__ W,
+                                                           const float *__restrict__ sw, int M,
+                                                           int N, int Kb, void *__restrict__ y,
+                                                           int64_t ldy,
+                                                           int32_t *__restrict__ acc_out,
+                                                           int tiles_m, int tiles_n) {
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[L_STAGES * L_STAGE];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * L_BM, n0 = tn * L_BN;
+    const int ktiles = (Kb + BKB - 1) / BKB;
+
+    // buffer views of this block's 256 A rows and 256 W rows
+    const v4i dA = buffer_desc(A + (int64_t)m0 * Kb, (uint32_t)(min(M - m0, L_BM) * Kb));
+    const v4i dW = buffer_desc(W + (int64_t)n0 * Kb, (uint32_t)(min(N - n0, L_BN) * Kb));
+
+    // DMA mapping: instruction i of wave w fills LDS bytes [(4w+i)*1024, +1024)
+    // = rows 16(4w+i) .. +16; lane L -> row 16(4w+i) + L/4, slot L%4, which
+    // holds k-chunk c = slot ^ ((row >> 1) & 3) of that row.
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    uint32_t voff[4];
+    int kc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = 16 * (4 * wave + i) + (lane >> 2);
+        kc[i] = ((lane & 3) ^ ((row >> 1) & 3)) * 16;
+        voff[i] = (uint32_t)(row * Kb + kc[i]);
+    }
+    const uint32_t lds0 = lds_addr(smem) + wave_u * 4096;
+    auto issue = [&](int slot, int kt) {
+        const uint32_t base = lds0 + slot * L_STAGE;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const bool kin = kt * BKB + kc[i] < Kb;
+            const uint32_t o = kin ? voff[i] + (uint32_t)(kt * BKB) : 0x80000000u;
+            dma16(dA, o, base + i * 1024);
+            dma16(dW, o, base + L_BM * BKB + i * 1024);
+        }
+    };
+
+    v4i acc[8][8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f)
+#pragma unroll
+        for (int g = 0; g < 8; ++g) acc[f][g] = v4i{0, 0, 0, 0};
+
+    // fragment addresses inside a stage: frags 0..7 = W rows, 8..15 = A rows
+    const int c = lane >> 4;
+    uint32_t foff[16];
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+        const int wr = wn * 128 + f * 16 + (lane & 15);
+        foff[f] = L_BM * BKB + wr * BKB + ((c ^ ((wr >> 1) & 3)) << 4);
+        const int ar = wm * 128 + f * 16 + (lane & 15);
+        foff[8 + f] = ar * BKB + ((c ^ ((ar >> 1) & 3)) << 4);
+    }
+    auto read_frags = [&](int slot, uint4 *p) {
+        const uint8_t *base = smem + slot * L_STAGE;
+#pragma unroll
+        for (int f = 0; f < 16; ++f) p[f] = *reinterpret_cast<const uint4 *>(base + foff[f]);
+    };
+    auto unpack = [&](uint32_t w0, uint32_t w1) {
+        return v4i{(int)nib_lo(w0), (int)nib_hi(w0), (int)nib_lo(w1), (int)nib_hi(w1)};
+    };
+    auto mfma_step = [&](const v4i *u) {
+#pragma unroll
+        for (int f = 0; f < 8; ++f)
+#pragma unroll
+            for (int g = 0; g < 8; ++g)
+                acc[f][g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(u[f], u[8 + g], acc[f][g], 0,
+                                                                  0, 0);
+    };
+
+#pragma unroll
+    for (int s = 0; s < L_STAGES - 1; ++s)
+        if (s < ktiles) issue(s, s);
+
+    // Software pipeline.  Entering iteration kt, u0 holds the unpacked step-0
+    // operands of tile kt and pc the packed step-1 words.  Phase A runs the
+    // step-0 MFMAs while the next tile's fragments are read from LDS and the
+    // step-1 operands are unpacked; phase B runs the step-1 MFMAs while the
+    // next tile's step-0 operands are unpacked.
+    v4i u0[16], u1[16];
+    uint2 pc[16];
+    uint4 pn[16];
+    if (ktiles > 2) asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
+    else if (ktiles == 2) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+    read_frags(0, pn);
+#pragma unroll
+    for (int f = 0; f < 16; ++f) {
+        u0[f] = unpack(pn[f].x, pn[f].y);
+        pc[f] = make_uint2(pn[f].z, pn[f].w);
+    }
+    for (int kt = 0; kt + 1 < ktiles; ++kt) {
+        // tile kt+1 must have landed (from every wave) before phase A reads it
+        if (kt + 2 < ktiles) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+        else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+        if (kt + L_STAGES - 1 < ktiles) issue((kt + L_STAGES - 1) % L_STAGES, kt + L_STAGES - 1);
+        // phase A
+        read_frags((kt + 1) % L_STAGES, pn);
+#pragma unroll
+        for (int f = 0; f < 16; ++f) u1[f] = unpack(pc[f].x, pc[f].y);
+        mfma_step(u0);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // 1 LDS read
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // 1 MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // 2 VALU
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+        // phase B
+#pragma unroll
+        for (int f = 0; f < 16; ++f) {
+            u0[f] = unpack(pn[f].x, pn[f].y);
+            pc[f] = make_uint2(pn[f].z, pn[f].w);
+        }
+        mfma_step(u1);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+    }
+    // last tile
+#pragma unroll
+    for (int f = 0; f < 16; ++f) u1[f] = unpack(pc[f].x, pc[f].y);
+    mfma_step(u0);
+    mfma_step(u1);
+
+    // epilogue: acc[f][g] lane l, reg e -> n = n0 + wn*128 + f*16 + 4*(l>>4) + e,
+    //                                       m = m0 + wm*128 + g*16 + (l&15)
+    float sam[8];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        const int m = m0 + wm * 128 + g * 16 + (lane & 15);
+        sam[g] = (m < M) ? sa[m] : 0.0f;
+    }
+    const bool vec_ok = ((ldy & 3) == 0) && ((reinterpret_cast<uintptr_t>(y) & 7) == 0);
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+        const int nb = n0 + wn * 128 + f * 16 + 4 * (lane >> 4);
+        float swn[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) swn[e] = (nb + e < N) ? sw[nb + e] : 0.0f;
+#pragma unroll
+        for (int g = 0; g < 8; ++g) {
+            const int m = m0 + wm * 128 + g * 16 + (lane & 15);
+            if (m >= M) continue;
+            int v[4];
+            float o[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v[e] = acc[f][g][e] >> 8;
+                o[e] = __fmul_rn(__fmul_rn((float)v[e], sam[g]), swn[e]);
+            }
+            const int64_t off = (int64_t)m * ldy + nb;
+            if (vec_ok && nb + 3 < N) {
+                uint2 packed;
+                if constexpr (BF16OUT) {
+                    // v_cvt_pk_bf16_f32: two fp32 -> bf16, round to nearest even
+                    packed.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{o[0], o[1]}, bf2));
+                    packed.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{o[2], o[3]}, bf2));
+                } else {
+                    uint32_t h[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        float ov = o[e];
+                        asm volatile("" : "+v"(ov));
+                        h[e] = __builtin_bit_cast(uint16_t, (_Float16)ov);
+                    }
+                    packed = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                }
+                *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(y) + off) = packed;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (nb + e < N) store_out<BF16OUT>(y, off + e, o[e]);
+            }
+            if (acc_out) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (nb + e < N) acc_out[(int64_t)m * N + nb + e] = v[e];
+            }
+        }
+    }
+}
+
 }  // namespace
 
 size_t gemm_workspace_bytes(int, int, int) { return 0; }
@@ -160,8 +427,20 @@ size_t gemm_workspace_bytes(int, int, int) { return 0; }
 hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *sa,
                             const uint8_t *w, const float *sw, p4q_dtype out_dt, void *y,
                             int64_t ldy, int32_t *acc_out, void *, size_t, hipStream_t stream) {
+    const bool bf16 = (out_dt == P4Q_BF16);
+    if (M >= 1024 && N >= 1024) {
+        const int tiles_m = (M + L_BM - 1) / L_BM, tiles_n = (N + L_BN - 1) / L_BN;
+        const dim3 grid(tiles_m * tiles_n);
+        if (bf16)
+            hipLaunchKernelGGL(k_w4a4_gemm_t256<true>, grid, dim3(256), 0, stream, a, sa, w, sw,
+                               M, N, K / 2, y, ldy, acc_out, tiles_m, tiles_n);
+        else
+            hipLaunchKernelGGL(k_w4a4_gemm_t256<false>, grid, dim3(256), 0, stream, a, sa, w, sw,
+                               M, N, K / 2, y, ldy, acc_out, tiles_m, tiles_n);
+        return hipGetLastError();
+    }
     const dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
-    if (out_dt == P4Q_BF16)
+    if (bf16)
         hipLaunchKernelGGL(k_w4a4_gemm<true>, grid, dim3(kThreads), 0, stream, a, sa, w, sw, M, N,
                            K / 2, y, ldy, acc_out);
     else

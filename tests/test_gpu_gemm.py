@@ -50,11 +50,20 @@ def test_shapes(shape, out_dtype):
     check_full(*codes_for(M, N, K, M * 7 + N), out_dtype)
 
 
+@pytest.mark.parametrize("shape", [(1030, 1100, 512), (1024, 1024, 4128), (1500, 2100, 96),
+                                   (2304, 1280, 11008), (1024, 4096, 32)])
+def test_large_tile_shapes(shape):
+    """Shapes served by the 256 x 256 kernel, with ragged M, N and K tails."""
+    M, N, K = shape
+    check_full(*codes_for(M, N, K, M + N + K), "bf16")
+
+
 @pytest.mark.parametrize("extreme", [-8, 7])
 def test_extreme_codes_large_K(extreme):
     """|acc| = 64 * K at K = 65536 (and 49 K with +7): checks the int32 range of
     the scaled MFMA accumulation."""
     check_full(*codes_for(40, 36, 65536, 3, extreme), "bf16")
+    check_full(*codes_for(1040, 1030, 65536, 3, extreme), "fp16")
 
 
 def test_strided_output():
