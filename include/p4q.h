@@ -86,8 +86,8 @@ const char *p4q_last_error(void);
  * Workspace: at least p4q_select_workspace_bytes(B, N, d, J) bytes, 256-byte
  *   aligned.  Its first B*N*(J+1) int32 hold, per token, D_i0 .. D_i(J-1)
  *   then Nv_i (layout [B][N][J+1]); the rest is internal.
- * Limits: 1 <= K <= N <= 8192, 1 <= J <= 8, J * d <= 65536, T >= 0 (text
- *   may be NULL iff T == 0), d % 32 == 0, 32 <= d <= 16384, clip in
+ * Limits: 1 <= K <= N <= 8192, 1 <= J <= 8 (J <= 4 when d > 8192), T >= 0
+ *   (text may be NULL iff T == 0), d % 32 == 0, 32 <= d <= 16384, clip in
  *   [2^-16, 1]; pointers 16-byte aligned.
  * Errors: P4Q_ERR_INVALID_ARG / P4Q_ERR_UNSUPPORTED / P4Q_ERR_WORKSPACE as
  *   above; nothing is enqueued on error.

@@ -81,7 +81,7 @@ int p4q_select(p4q_dtype dt, int B, int N, int d, const void *vis, const void *c
     if (N > 8192) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: N=%d > 8192", N);
     if (J > 8) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: J=%d > 8", J);
     if (d > 16384) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: d=%d > 16384", d);
-    if ((int64_t)J * d > 65536) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: J*d > 65536");
+    if (J > 4 && d > 8192) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: J > 4 needs d <= 8192");
     const size_t need = p4q::select_workspace_bytes(B, N, d, J);
     if (!ws || ws_bytes < need)
         return fail(P4Q_ERR_WORKSPACE, "p4q_select: workspace %zu < %zu bytes", ws_bytes, need);

@@ -107,48 +107,74 @@ __device__ __forceinline__ int reduce8(const int *v, int lane) {
     return y;
 }
 
-template <int CH, bool BF16, bool CLIP1>
-__global__ __launch_bounds__(256) void k_select_score(const uint8_t *__restrict__ vis, int N, int d,
-                                                      int J, float clip, int rows_per_wave,
-                                                      int LS,
+typedef int v4i_t __attribute__((ext_vector_type(4)));
+
+// Range-checked 16-byte load: offsets at or past `bytes` read as zeros.
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
+}
+
+constexpr int kRowsPerWave = 4;   // rows per wavefront (sums gathered for one key per lane)
+
+template <int CH, int JMAX, bool BF16, bool CLIP1>
+__global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uint8_t *__restrict__ vis, int N, int d,
+                                                      int J, float clip, int LS,
                                                       const int8_t *__restrict__ ccodes,
                                                       int32_t *__restrict__ stats,
                                                       int64_t *__restrict__ keys) {
-    extern __shared__ uint2 s_cc[];          // [J][d/8] uint2 (8 int8 codes each)
+    extern __shared__ uint2 s_cc[];          // [JMAX][64*CH] uint2, zero-padded
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    // wave-uniform (keeps the row buffer descriptor in SGPRs)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int nchunk = d / 8;
+    constexpr int kChunks = 64 * CH;
 
-    // stage this sample's concept codes in LDS
+    // stage this sample's concept codes in LDS; absent concepts and chunks
+    // past the row end are zeros, so the dot products below need no guards
     {
-        const uint4 *g = reinterpret_cast<const uint4 *>(ccodes + (int64_t)b * J * d);
-        uint4 *l = reinterpret_cast<uint4 *>(s_cc);
-        const int n16 = J * d / 16;
-        for (int q = threadIdx.x; q < n16; q += 256) l[q] = g[q];
+        const uint2 *g = reinterpret_cast<const uint2 *>(ccodes + (int64_t)b * J * d);
+        for (int q = threadIdx.x; q < JMAX * kChunks; q += 256) {
+            const int j = q / kChunks, c = q - j * kChunks;
+            s_cc[q] = (j < J && c < nchunk) ? g[j * nchunk + c] : make_uint2(0, 0);
+        }
     }
     __syncthreads();
 
-    const int row0 = (blockIdx.x * 4 + wave) * rows_per_wave;
-    const int row_end = min(row0 + rows_per_wave, N);
-    const uint8_t *vb = vis + (int64_t)b * N * d * 2;
-
-    uint4 nxt[CH];
-    auto load_row = [&](int i, uint4 *v) {
-        const uint4 *src = reinterpret_cast<const uint4 *>(vb + (int64_t)i * d * 2);
+    const int row0 = (blockIdx.x * 4 + wave) * kRowsPerWave;
+    if (row0 >= N) return;                                   // wave-uniform
+    const int nrows = min(kRowsPerWave, N - row0);
+    const uint8_t *vb = vis + ((int64_t)b * N + row0) * d * 2;
+    const __amdgpu_buffer_rsrc_t rv =
+        __builtin_amdgcn_make_buffer_rsrc((void *)vb, 0, nrows * d * 2, 0x00020000);
+    uint32_t coff[CH];
 #pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int q = lane + 64 * c;
-            v[c] = (q < nchunk) ? load_nt(src + q) : make_uint4(0, 0, 0, 0);
-        }
+    for (int c = 0; c < CH; ++c) {
+        const int q = lane + 64 * c;
+        coff[c] = (q < nchunk) ? (uint32_t)q * 16u : 0x80000000u;
+    }
+    auto load_row = [&](int r, uint4 *v) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) v[c] = buf_load16(rv, coff[c] + (uint32_t)(r * d * 2));
     };
-    if (row0 < row_end) load_row(row0, nxt);
 
-    for (int i = row0; i < row_end; ++i) {
+    // one-row prefetch only for short rows; wide rows rely on occupancy
+    constexpr bool kPrefetch = CH <= 4;
+    uint4 nxt[kPrefetch ? CH : 1];
+    if constexpr (kPrefetch) load_row(0, nxt);
+    int myval = 0, mynv = 0;        // lane 8v + r: value v (D_v, or Nv at v = J) of row r
+    for (int r = 0; r < nrows; ++r) {
+        // keeps the concept-code LDS reads inside the loop (hoisting them
+        // would cost JMAX * 2 * CH registers and halve the occupancy)
+        asm volatile("" ::: "memory");
         uint4 v[CH];
+        if constexpr (kPrefetch) {
 #pragma unroll
-        for (int c = 0; c < CH; ++c) v[c] = nxt[c];
-        if (i + 1 < row_end) load_row(i + 1, nxt);          // prefetch next token
+            for (int c = 0; c < CH; ++c) v[c] = nxt[c];
+            if (r + 1 < nrows) load_row(r + 1, nxt);       // prefetch next token
+        } else {
+            load_row(r, v);
+        }
 
         uint32_t m2 = 0;
 #pragma unroll
@@ -157,103 +183,160 @@ __global__ __launch_bounds__(256) void k_select_score(const uint8_t *__restrict_
         const float s = row_scale<CLIP1>(mag_to_f32<BF16>(mbits), clip);
 
         uint2 cv[CH];                                        // int8 codes, 8 per chunk
-        if (s == 0.0f) {
 #pragma unroll
-            for (int c = 0; c < CH; ++c) cv[c] = make_uint2(0, 0);
-        } else {
+        for (int c = 0; c < CH; ++c) cv[c] = make_uint2(0, 0);
+        if (s != 0.0f) {
             uint32_t near = 0;
             const bool tiny = !(s >= kTinyScale);
             if (!tiny) {
-                const float r = 1.0f / s;
+                const float rc = 1.0f / s;
 #pragma unroll
                 for (int c = 0; c < CH; ++c) {
                     uint32_t w[8];
-                    q4_chunk_fast<BF16, CLIP1>(v[c], r, w, near);
+                    q4_chunk_fast<BF16, CLIP1>(v[c], rc, w, near);
                     cv[c] = make_uint2(bytes4(w[0], w[1], w[2], w[3]), bytes4(w[4], w[5], w[6], w[7]));
                 }
             }
-            if (tiny || __any((int)near)) {
+            if (tiny || __any((int)near)) {                  // wave-uniform, rare
 #pragma unroll
                 for (int c = 0; c < CH; ++c) {
                     uint32_t w[8];
-                    q4_chunk_exact<BF16>(v[c], s, w);
+                    uint4 vc = v[c];
+                    // opaque copy: keeps the exact path's fp16 -> fp32 conversions
+                    // from being hoisted into (and paid on) the fast path
+                    asm volatile("" : "+v"(vc.x), "+v"(vc.y), "+v"(vc.z), "+v"(vc.w));
+                    q4_chunk_exact<BF16>(vc, s, w);
                     cv[c] = make_uint2(bytes4(w[0], w[1], w[2], w[3]), bytes4(w[4], w[5], w[6], w[7]));
                 }
             }
         }
 
-        int part[8];                                         // D_0..D_{J-1}, Nv at [J]
         int nv = 0;
-        int dj[kMaxJ] = {0, 0, 0, 0, 0, 0, 0, 0};
+        int dj[JMAX];
+#pragma unroll
+        for (int j = 0; j < JMAX; ++j) dj[j] = 0;
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
-            const int q = lane + 64 * c;
-            if (q < nchunk) {
-                nv = __builtin_amdgcn_sdot4((int)cv[c].x, (int)cv[c].x, nv, false);
-                nv = __builtin_amdgcn_sdot4((int)cv[c].y, (int)cv[c].y, nv, false);
+            nv = __builtin_amdgcn_sdot4((int)cv[c].x, (int)cv[c].x, nv, false);
+            nv = __builtin_amdgcn_sdot4((int)cv[c].y, (int)cv[c].y, nv, false);
 #pragma unroll
-                for (int j = 0; j < kMaxJ; ++j) {
-                    if (j < J) {
-                        const uint2 cc = s_cc[j * nchunk + q];
-                        dj[j] = __builtin_amdgcn_sdot4((int)cv[c].x, (int)cc.x, dj[j], false);
-                        dj[j] = __builtin_amdgcn_sdot4((int)cv[c].y, (int)cc.y, dj[j], false);
-                    }
-                }
+            for (int j = 0; j < JMAX; ++j) {
+                const uint2 cc = s_cc[j * kChunks + lane + 64 * c];
+                dj[j] = __builtin_amdgcn_sdot4((int)cv[c].x, (int)cc.x, dj[j], false);
+                dj[j] = __builtin_amdgcn_sdot4((int)cv[c].y, (int)cc.y, dj[j], false);
             }
         }
-        // slot J holds Nv (J <= 7 here); J == 8 handled with a second reduction
+        int part[8];
 #pragma unroll
-        for (int j = 0; j < kMaxJ; ++j) part[j] = (j < J) ? dj[j] : (j == J ? nv : 0);
-        const int tot = reduce8(part, lane);
-        int nv_tot;
-        if (J < kMaxJ) {
-            nv_tot = __shfl(tot, 8 * J);
-        } else {
+        for (int j = 0; j < 8; ++j) part[j] = (j < JMAX) ? dj[j] : 0;
+        if (JMAX < 8) part[JMAX < 8 ? J : 0] = nv;           // slot J holds Nv
+        const int tot = reduce8(part, lane);                 // value (lane >> 3) of this row
+        if ((lane & 7) == r) myval = tot;
+        if (JMAX == 8) {
             int p2[8] = {nv, 0, 0, 0, 0, 0, 0, 0};
-            nv_tot = __shfl(reduce8(p2, lane), 0);
+            const int nvt = reduce8(p2, lane);               // Nv in lanes 0..7
+            if ((lane & 7) == r) mynv = nvt;
         }
-        const int slot = lane >> 3;                          // value held by this lane
-        if ((lane & 7) == 0) {
-            int32_t *st = stats + ((int64_t)b * N + i) * (J + 1);
-            if (slot < J) {
-                st[slot] = tot;
-                keys[((int64_t)b * J + slot) * N + i] = exact_key(tot, nv_tot, LS);
-            } else if (slot == J) {
-                st[J] = nv_tot;
-            }
-        }
-        if (J == kMaxJ && lane == 0) stats[((int64_t)b * N + i) * (J + 1) + J] = nv_tot;
     }
+    // lane 8v + r now holds value v of row r: one stats word and one key each
+    const int r = lane & 7, vslot = lane >> 3;
+    const int nv_r = (JMAX == 8) ? __shfl(mynv, r) : __shfl(myval, 8 * J + r);
+    if (r < nrows) {
+        const int i = row0 + r;
+        int32_t *st = stats + ((int64_t)b * N + i) * (J + 1);
+        if (vslot < J) {
+            st[vslot] = myval;
+            keys[((int64_t)b * J + vslot) * N + i] = exact_key(myval, nv_r, LS);
+        } else if (vslot == J) {
+            st[J] = myval;
+        }
+        if (JMAX == 8 && vslot == 0) st[J] = nv_r;
+    }
+}
+
+// Inclusive prefix sum over the 64 lanes of a wavefront with DPP row shifts
+// and row broadcasts (no LDS round trips).
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t v) {
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, true);  // row_shr:1
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, true);  // row_shr:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, true);  // row_shr:4
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, true);  // row_shr:8
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false); // row_bcast:15
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false); // row_bcast:31
+    return v;
+}
+
+// sum of wtot[0 .. wave) read as four 16-byte words
+__device__ __forceinline__ uint32_t waves_before(const uint32_t *wtot, int wave) {
+    const uint4 *w4 = reinterpret_cast<const uint4 *>(wtot);
+    uint32_t s = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint4 v = w4[q];
+        s += (4 * q + 0 < wave ? v.x : 0u) + (4 * q + 1 < wave ? v.y : 0u) +
+             (4 * q + 2 < wave ? v.z : 0u) + (4 * q + 3 < wave ? v.w : 0u);
+    }
+    return s;
 }
 
 // ---------------------------------------------------------------------------
 // 3. top-K.  One 1024-thread workgroup per sample; thread t owns tokens
 //    t*E .. t*E+E-1 (E <= 8), so the final compaction is an ordered scan.
-//    Per concept: candidates = tokens not yet kept; the composite
-//    X = (key ^ 2^63) * 2^13 + (8191 - i) is unique, so "the quota largest X"
-//    is exactly "the quota best tokens, lower index first on equal cosine".
-//    MSD radix select with 11-bit digits, starting at the highest bit where
-//    candidates differ, stopping as soon as the boundary bucket is taken whole.
+//    Per concept: candidates = tokens not yet kept.  Each exact key k is
+//    mapped to an order-preserving 67-bit code V = [s | e | m]: s = 1 for
+//    k >= 0, e = bit length of |k| (6 bits), m = |k| without its leading one,
+//    left-aligned to 60 bits; negative keys take the bitwise complement of
+//    (e, m) with s = 0.  The composite X = V * 2^13 + (8191 - i) is unique, so
+//    "the quota largest X" is exactly "the quota best tokens, lower index first
+//    on equal cosine".  MSD radix select with 11-bit digits from the top of X:
+//    the first digit is sign + exponent + 4 mantissa bits, which spreads the
+//    typical scores (most near zero) over many buckets; the select stops as
+//    soon as the boundary bucket is taken whole.
 // ---------------------------------------------------------------------------
 constexpr int kTkThreads = 1024;
 constexpr int kTkMaxE = 8;
 constexpr int kDigit = 11;
 constexpr int kBins = 1 << kDigit;
-constexpr int kIdxBits = 13;
+constexpr int kLoBits = 16;          // low word of X: 3 mantissa bits + 13 index bits
+constexpr int kXBits = 80;           // 1 + 6 + 60 + 13
 
-__device__ __forceinline__ uint32_t comp_digit(uint64_t hk, uint32_t lo13, int lo, int w) {
+struct Composite {
+    uint64_t hi;      // X >> 16
+    uint32_t lo;      // X & 0xFFFF
+};
+
+__device__ __forceinline__ Composite make_composite(int64_t k, int i) {
+    const uint64_t u = (uint64_t)(k < 0 ? -k : k);
+    uint64_t e = 0, m = 0;                       // 6-bit exponent, 60-bit mantissa
+    if (u) {
+        const int lz = __clzll((long long)u);
+        e = (uint64_t)(64 - lz);                 // 1 .. 61
+        m = ((u << lz) << 1) >> 4;               // drop the leading one, keep 60 bits
+    }
+    uint64_t em_hi = (e << 57) | (m >> 3);       // 63 bits: e(6) m(57 top)
+    uint32_t em_lo = (uint32_t)(m & 7);          // 3 low mantissa bits
+    if (k < 0) {                                 // s = 0, complement (e, m)
+        em_hi = ~em_hi & ((1ull << 63) - 1);
+        em_lo = ~em_lo & 7u;
+    } else {
+        em_hi |= 1ull << 63;                     // s = 1
+    }
+    return Composite{em_hi, (em_lo << 13) | (uint32_t)(8191 - i)};
+}
+
+// bits [lo, lo + w) of X (w <= 11)
+__device__ __forceinline__ uint32_t comp_digit(const Composite &x, int lo, int w) {
     const uint32_t mask = (1u << w) - 1u;
-    if (lo >= kIdxBits) return (uint32_t)(hk >> (lo - kIdxBits)) & mask;
-    const uint64_t x = (hk << (kIdxBits - lo)) | (uint64_t)(lo13 >> lo);
-    return (uint32_t)x & mask;
+    if (lo >= kLoBits) return (uint32_t)(x.hi >> (lo - kLoBits)) & mask;
+    const uint64_t v = (x.hi << (kLoBits - lo)) | (uint64_t)(x.lo >> lo);
+    return (uint32_t)v & mask;
 }
 
 __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__restrict__ keys,
                                                             int N, int J, int K,
                                                             int32_t *__restrict__ idx_out) {
-    __shared__ uint32_t hist[kBins];
-    __shared__ uint32_t wtot[kTkThreads / 64];
-    __shared__ uint64_t rmin[kTkThreads / 64], rmax[kTkThreads / 64];
+    __shared__ __attribute__((aligned(16))) uint32_t hist[kBins];
+    __shared__ __attribute__((aligned(16))) uint32_t wtot[kTkThreads / 64];
     __shared__ uint32_t sh_bucket, sh_gt, sh_eq;
 
     const int b = blockIdx.x;
@@ -261,62 +344,50 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__res
     const int lane = t & 63, wave = t >> 6;
     const int E = (N + kTkThreads - 1) / kTkThreads;
     for (int q = t; q < kBins; q += kTkThreads) hist[q] = 0;
+    __syncthreads();
     uint32_t kept = 0;
 
-    for (int j = 0; j < J; ++j) {
-        const uint32_t quota = (uint32_t)(K / J + (j < K % J ? 1 : 0));
-        if (quota == 0) continue;
+    // keys of the next concept are loaded while the current one is selected
+    int64_t kn[kTkMaxE];
+    auto load_keys = [&](int j) {
         const int64_t *kj = keys + ((int64_t)b * J + j) * N;
-        uint64_t hk[kTkMaxE];
-        uint32_t cont = 0;
-        uint64_t mn = ~0ull, mx = 0;
 #pragma unroll
         for (int e = 0; e < kTkMaxE; ++e) {
             const int i = t * E + e;
-            hk[e] = 0;
-            if (e < E && i < N && !((kept >> e) & 1u)) {
-                hk[e] = (uint64_t)kj[i] ^ (1ull << 63);
-                cont |= 1u << e;
-                mn = min(mn, hk[e]);
-                mx = max(mx, hk[e]);
-            }
+            kn[e] = (e < E && i < N) ? kj[i] : 0;
         }
+    };
+    load_keys(0);
+    for (int j = 0; j < J; ++j) {
+        const uint32_t quota = (uint32_t)(K / J + (j < K % J ? 1 : 0));
+        Composite x[kTkMaxE];
+        uint32_t cont = 0;
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            mn = min(mn, (uint64_t)__shfl_xor((unsigned long long)mn, o));
-            mx = max(mx, (uint64_t)__shfl_xor((unsigned long long)mx, o));
+        for (int e = 0; e < kTkMaxE; ++e) {
+            const int i = t * E + e;
+            x[e] = make_composite(kn[e], i);
+            if (e < E && i < N && !((kept >> e) & 1u)) cont |= 1u << e;
         }
-        if (lane == 0) { rmin[wave] = mn; rmax[wave] = mx; }
-        __syncthreads();
-        mn = rmin[0];
-        mx = rmax[0];
-        for (int w = 1; w < kTkThreads / 64; ++w) { mn = min(mn, rmin[w]); mx = max(mx, rmax[w]); }
-        int pos = (mn != mx) ? kIdxBits + 64 - __clzll((long long)(mn ^ mx)) : kIdxBits;
-
+        if (j + 1 < J) load_keys(j + 1);
+        if (quota == 0) continue;                            // block-uniform
         uint32_t need = quota;
+        int pos = kXBits;
         while (true) {
             const int w = min(kDigit, pos);
             const int lo = pos - w;
 #pragma unroll
             for (int e = 0; e < kTkMaxE; ++e)
-                if ((cont >> e) & 1u)
-                    atomicAdd(&hist[comp_digit(hk[e], (uint32_t)(8191 - (t * E + e)), lo, w)], 1u);
+                if ((cont >> e) & 1u) atomicAdd(&hist[comp_digit(x[e], lo, w)], 1u);
             __syncthreads();
             // reverse-order inclusive scan: thread t covers bins kBins-1-2t, kBins-2-2t
             const int b0 = kBins - 1 - 2 * t, b1 = kBins - 2 - 2 * t;
             const uint32_t c0 = hist[b0], c1 = hist[b1];
             hist[b0] = 0;
             hist[b1] = 0;
-            uint32_t inc = c0 + c1;
-#pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const uint32_t up = (uint32_t)__shfl_up((int)inc, o);
-                if (lane >= o) inc += up;
-            }
+            const uint32_t inc = wave_inclusive_scan(c0 + c1);
             if (lane == 63) wtot[wave] = inc;
             __syncthreads();
-            uint32_t excl = inc - (c0 + c1);
-            for (int w2 = 0; w2 < wave; ++w2) excl += wtot[w2];
+            const uint32_t excl = inc - (c0 + c1) + waves_before(wtot, wave);
             if (excl < need && need <= excl + c0) { sh_bucket = b0; sh_gt = excl; sh_eq = c0; }
             const uint32_t e1 = excl + c0;
             if (e1 < need && need <= e1 + c1) { sh_bucket = b1; sh_gt = e1; sh_eq = c1; }
@@ -325,7 +396,7 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__res
 #pragma unroll
             for (int e = 0; e < kTkMaxE; ++e) {
                 if ((cont >> e) & 1u) {
-                    const uint32_t dg = comp_digit(hk[e], (uint32_t)(8191 - (t * E + e)), lo, w);
+                    const uint32_t dg = comp_digit(x[e], lo, w);
                     if (dg > bucket) { kept |= 1u << e; cont &= ~(1u << e); }
                     else if (dg < bucket) { cont &= ~(1u << e); }
                 }
@@ -338,26 +409,23 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__res
 
     // ordered compaction of the kept set
     const uint32_t cnt = __builtin_popcount(kept);
-    uint32_t inc = cnt;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t up = (uint32_t)__shfl_up((int)inc, o);
-        if (lane >= o) inc += up;
-    }
+    const uint32_t inc = wave_inclusive_scan(cnt);
     __syncthreads();
     if (lane == 63) wtot[wave] = inc;
     __syncthreads();
-    uint32_t pos = inc - cnt;
-    for (int w2 = 0; w2 < wave; ++w2) pos += wtot[w2];
+    uint32_t opos = inc - cnt + waves_before(wtot, wave);
     int32_t *out = idx_out + (int64_t)b * K;
 #pragma unroll
     for (int e = 0; e < kTkMaxE; ++e)
-        if (((kept >> e) & 1u) && pos < (uint32_t)K) out[pos++] = t * E + e;
+        if (((kept >> e) & 1u) && opos < (uint32_t)K) out[opos++] = t * E + e;
 }
 
 // ---------------------------------------------------------------------------
-// 4. gather: one wavefront per output row, 16-byte copies
+// 4. gather: one wavefront per output row; all of a row's 16-byte loads are
+//    issued before its stores (up to 8 KB in flight per wavefront)
 // ---------------------------------------------------------------------------
+constexpr int kGatherMaxCh = 16;      // chunks per lane held in registers (d <= 8192)
+
 __global__ __launch_bounds__(256) void k_select_gather(const uint4 *__restrict__ vis,
                                                        const uint4 *__restrict__ text,
                                                        const int32_t *__restrict__ idx, int B,
@@ -376,32 +444,50 @@ __global__ __launch_bounds__(256) void k_select_gather(const uint4 *__restrict__
     }
     const uint4 *src = (r < K) ? vis + ((int64_t)b * N + src_tok) * dchunks
                                : text + ((int64_t)b * T + (r - K)) * dchunks;
-    for (int q = lane; q < dchunks; q += 64) dst[q] = src[q];
+    for (int q0 = 0; q0 < dchunks; q0 += 64 * kGatherMaxCh) {
+        uint4 v[kGatherMaxCh];
+#pragma unroll
+        for (int c = 0; c < kGatherMaxCh; ++c) {
+            const int q = q0 + lane + 64 * c;
+            if (q < dchunks) v[c] = load_nt(src + q);
+        }
+#pragma unroll
+        for (int c = 0; c < kGatherMaxCh; ++c) {
+            const int q = q0 + lane + 64 * c;
+            if (q < dchunks) dst[q] = v[c];
+        }
+    }
+}
+
+template <int CH, int JMAX, bool BF16, bool CLIP1>
+hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const void *vis,
+                        const SelectWorkspace &ws, hipStream_t stream) {
+    const dim3 grid((N + 4 * kRowsPerWave - 1) / (4 * kRowsPerWave), B);
+    const size_t lds = (size_t)JMAX * 64 * CH * 8;
+    hipLaunchKernelGGL((k_select_score<CH, JMAX, BF16, CLIP1>), grid, dim3(256), lds, stream,
+                       static_cast<const uint8_t *>(vis), N, d, J, clip, LS, ws.ccodes, ws.stats,
+                       ws.keys);
+    return hipGetLastError();
 }
 
 template <int CH, bool BF16, bool CLIP1>
-hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const void *vis,
-                        const SelectWorkspace &ws, hipStream_t stream) {
-    constexpr int kRowsPerWave = 16;
-    const dim3 grid((N + 4 * kRowsPerWave - 1) / (4 * kRowsPerWave), B);
-    const size_t lds = (size_t)J * d;
-    hipLaunchKernelGGL((k_select_score<CH, BF16, CLIP1>), grid, dim3(256), lds, stream,
-                       static_cast<const uint8_t *>(vis), N, d, J, clip, kRowsPerWave, LS,
-                       ws.ccodes, ws.stats, ws.keys);
-    return hipGetLastError();
+hipError_t launch_score_j(int B, int N, int d, int J, float clip, int LS, const void *vis,
+                          const SelectWorkspace &ws, hipStream_t stream) {
+    if (J <= 4) return launch_score<CH, 4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    return launch_score<CH, 8, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
 }
 
 template <bool BF16, bool CLIP1>
 hipError_t launch_score_typed(int B, int N, int d, int J, float clip, int LS, const void *vis,
                               const SelectWorkspace &ws, hipStream_t stream) {
     const int per_lane = (d / 8 + 63) / 64;
-    if (per_lane <= 1) return launch_score<1, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 2) return launch_score<2, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 4) return launch_score<4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 8) return launch_score<8, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 10) return launch_score<10, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 16) return launch_score<16, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    return launch_score<32, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    if (per_lane <= 1) return launch_score_j<1, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    if (per_lane <= 2) return launch_score_j<2, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    if (per_lane <= 4) return launch_score_j<4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    if (per_lane <= 8) return launch_score_j<8, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    if (per_lane <= 10) return launch_score_j<10, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    if (per_lane <= 16) return launch_score_j<16, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    return launch_score<32, 4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
 }
 
 template <bool BF16, bool CLIP1>

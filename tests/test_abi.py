@@ -90,7 +90,7 @@ def select(**kw):
     (dict(ws=ALIGNED + 16), L.P4Q_ERR_INVALID_ARG),
     (dict(clip=2.0), L.P4Q_ERR_INVALID_ARG),
     (dict(dt=2), L.P4Q_ERR_UNSUPPORTED),
-    (dict(J=8, d=16384), L.P4Q_ERR_UNSUPPORTED),
+    (dict(J=5, d=8224), L.P4Q_ERR_UNSUPPORTED),
 ])
 def test_select_validation(kw, status):
     assert select(**kw) == status
