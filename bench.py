@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="next7b_b16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
 
 
@@ -127,17 +129,21 @@ class Events:
 
 def cpu_baseline(cfg):
     """The oracle on a bounded sample of the same workload, scaled to the step:
-    one image's selection and 32 rows of every quantize + linear."""
+    every image through the selector and 8192 of the pruned rows through
+    every quantize + linear (weights quantized beforehand, untimed)."""
     import oracle
     from workload import selector_inputs, weight, attn_standin, mlp_standin
 
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    si = selector_inputs(cfg, samples=[0])
+    n_img = cfg.B
+    si = selector_inputs(cfg, samples=list(range(n_img)))
+    toks = []
     t0 = time.perf_counter()
-    _, tok, _, _ = oracle.select(si.vis[0], si.concepts[0], si.text[0], cfg.K)
-    t_sel = time.perf_counter() - t0
-    rows = 32
-    xs = {"x": tok[:rows],
+    for b in range(n_img):
+        toks.append(oracle.select(si.vis[b], si.concepts[b], si.text[b], cfg.K)[1])
+    t_sel = (time.perf_counter() - t0) / n_img
+    rows = min(8192, n_img * (cfg.K + cfg.T))
+    xs = {"x": np.concatenate(toks)[:rows],
           "attn": attn_standin(cfg, rows), "mlp": mlp_standin(cfg, rows)}
     t_lin = 0.0
     for li, lin in enumerate(cfg.linears):
@@ -149,16 +155,47 @@ def cpu_baseline(cfg):
     t_full = cfg.B * t_sel + (cfg.M / rows) * t_lin
     return {"value": round(cfg.linear_ops() / t_full / 1e12, 6), "unit": "TOPS",
             "cores": threads, "kind": "oracle",
-            "sample": (f"1 of {cfg.B} images through the selector ({t_sel:.2f}s) and {rows} of "
-                       f"{cfg.M} rows through quantize + all 7 linears ({t_lin:.2f}s), "
-                       f"scaled to the full step ({t_full:.1f}s)")}
+            "sample": (f"{n_img} of {cfg.B} images through the selector ({n_img * t_sel:.1f}s) and "
+                       f"{rows} of {cfg.M} rows through quantize + all 7 linears ({t_lin:.1f}s), "
+                       f"scaled to the full step ({t_full:.0f}s)")}
+
+
+def copy_calibration(dev, nbytes=1 << 30, reps=5):
+    """A plain device-to-device copy of known size, run so that the HBM
+    counters (FETCH_SIZE, WRITE_SIZE) can be scaled to bytes: the counter
+    reading of one copy dispatch corresponds to exactly `nbytes` read and
+    `nbytes` written."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "dispatches": reps}), flush=True)
+
+
+def traffic_from_profile():
+    """HBM bytes per GEMM launch from the committed counter summary, or None
+    when the GEMM source changed after the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_w4a4_gemm_llava_next_b16.md")
+    src = os.path.join(ROOT, "paper_2609_34867_amd", "csrc", "w4a4_gemm.hip")
+    try:
+        fields = dict(l.strip("- \n").split(": ", 1) for l in open(path)
+                      if l.startswith("- ") and ": " in l)
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if fields.get("w4a4_gemm.hip sha256") != sha:
+            return None
+        return int(fields["hbm bytes per launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the multi-GPU sharding is described in DESIGN.md, not run)", file=sys.stderr)
+              "(this build shows the per-GPU kernels; sharding across GPUs is not run)", file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2609_34867_amd as p4q
@@ -166,25 +203,26 @@ def main():
 
     cfg = CONFIGS[args.config]
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        copy_calibration(dev)
+        return
     st = setup(cfg, dev)
     for i in range(args.warmup):
         step(cfg, st, i)
     torch.cuda.synchronize()
 
+    # HIP events on the launch stream (torch's current stream, which the
+    # binding passes to every call): one pair around the K steps, one pair
+    # around every call inside them
+    ev = Events()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for i in range(args.steps):
-        step(cfg, st, i)
+        step(cfg, st, i, ev)
     end.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
-
-    # per-call breakdown with HIP events on the launch stream (separate pass)
-    ev = Events()
-    for i in range(args.steps):
-        step(cfg, st, i, ev)
-    torch.cuda.synchronize()
     tot = {k: v / args.steps for k, v in ev.totals_ms().items()}
 
     ops = cfg.linear_ops()
@@ -212,8 +250,9 @@ def main():
                    "M": cfg.M, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
                      "unit": "TOPS", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
-                     "traffic": None, "kernel": "k_w4a4_gemm_t256",
-                     "per_launch": "2*M*n_out*k_in int ops; 7 launches per step"},
+                     "traffic": traffic_from_profile(), "kernel": "k_w4a4_gemm_t256",
+                     "per_launch": "2*M*n_out*k_in int ops, averaged over the 7 launches of a step; "
+                                   "traffic in HBM bytes per launch"},
         "gemm_tops": round(gemm_tops, 2),
         "selector_tokens_per_s": round(sel_tokens / (tot["select"] * 1e-3), 1),
         "selector_gbs": round(sel_gbs, 1),
