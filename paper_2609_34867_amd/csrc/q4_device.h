@@ -10,7 +10,7 @@
 // low mantissa bits, and fma(x, r, -q) gives the exact residual x*r - q up to
 // one rounding.  For |x/s| < 8, |x*r - x/s| <= 8*2^-24 and
 // |fl32(x/s) - x/s| <= 2^-22, so when x*r is farther than 2^-19 from every
-// half-integer, rne(x*r) == rne(fl32(x/s)).  Otherwise the row is flagged and
+// half-integer, rne(x*r) == rne(fl32(x/s)).  Otherwise the values are
 // recomputed with the correctly rounded division (HIP's default fp32 '/').
 // Past |x/s| >= 8 only clamped codes are produced, which both paths agree on.
 #pragma once
@@ -106,12 +106,12 @@ __device__ __forceinline__ uint32_t bytes4(uint32_t w0, uint32_t w1, uint32_t w2
     return lo | hi;
 }
 
-// low nibbles of eight words -> packed int4 word (nibble i from w_i)
-__device__ __forceinline__ uint32_t nibbles8(const uint32_t *w) {
-    uint32_t p = 0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) p |= (w[i] & 0xFu) << (4 * i);
-    return p;
+// low nibbles of eight words -> packed int4 word (nibble i from w_i), with
+// two byte gathers and one bit-field insert
+__device__ __forceinline__ uint32_t pack_nibbles(const uint32_t *w) {
+    const uint32_t e = bytes4(w[0], w[2], w[4], w[6]);   // even values, one per byte
+    const uint32_t o = bytes4(w[1], w[3], w[5], w[7]);   // odd values
+    return (e & 0x0F0F0F0Fu) | ((o << 4) & 0xF0F0F0F0u);
 }
 
 // Quantize the 8 values of one 16-byte chunk.  out[i] low byte = code of
