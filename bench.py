@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="next7b_b16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode GEMV measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -160,6 +161,84 @@ def cpu_baseline(cfg):
                        f"scaled to the full step ({t_full:.0f}s)")}
 
 
+def decode_gemv(dev, steps=20):
+    """Decode-step W4A4 linears of the 13B-shape layer (h = 5120, f = 13824)
+    at M in {1, 4, 16}: HBM-bound, reported against the 8 TB/s peak.  The
+    linears that share an input run as one launch on row-concatenated weights
+    (q|k|v and gate|up, as serving stacks store them), so a layer is 4
+    launches: qkv, o, gate_up, down.  Four weight copies (634 MB) rotate so
+    the 158.8 MB of packed weights of a layer come from HBM, not from the
+    256 MB MALL."""
+    import torch
+    import paper_2609_34867_amd as p4q
+    from workload import CONFIGS, weight, gemv_activations
+
+    cfg = CONFIGS["stress13b_b8"]
+    names = [lin.name for lin in cfg.linears]
+    q = {}
+    for li, lin in enumerate(cfg.linears):
+        q[lin.name] = p4q.quant_act(torch.from_numpy(weight(cfg, li)).to(dev))
+    groups = [("qkv", ["q_proj", "k_proj", "v_proj"]), ("o", ["o_proj"]),
+              ("gate_up", ["gate_proj", "up_proj"]), ("down", ["down_proj"])]
+    fused = []
+    for gname, members in groups:
+        wc = torch.cat([q[m][0] for m in members])
+        ws = torch.cat([q[m][1] for m in members])
+        fused.append((gname, wc, ws, cfg.linears[names.index(members[0])].k_in))
+    del q
+    torch.cuda.synchronize()
+    copies = [[(wc.clone(), ws.clone()) for (_, wc, ws, _) in fused] for _ in range(N_WEIGHT_SETS)]
+    wbytes = sum(wc.numel() + 4 * ws.numel() for (_, wc, ws, _) in fused)
+    del fused
+    kins = [cfg.linears[names.index(members[0])].k_in for _, members in groups]
+    out = {}
+    for M in cfg.gemv_M:
+        acts = {}
+        for k_in in set(kins):
+            x = torch.from_numpy(gemv_activations(cfg, M, k_in)).to(dev)
+            acts[k_in] = p4q.quant_act(x)
+        ys = [torch.empty((M, wc.shape[0]), dtype=torch.bfloat16, device=dev)
+              for (wc, _) in copies[0]]
+
+        def layer(i):
+            W = copies[i % N_WEIGHT_SETS]
+            for gi, k_in in enumerate(kins):
+                a = acts[k_in]
+                p4q.w4a4_linear(a[0], a[1], W[gi][0], W[gi][1], y=ys[gi])
+
+        def timed(run):
+            for i in range(5):
+                run(i)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(steps):
+                run(i)
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) * 1e3 / steps
+
+        us_eager = timed(layer)
+        # the decode loop of a server replays captured graphs: one per weight copy
+        graphs = []
+        for i in range(N_WEIGHT_SETS):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                layer(i)
+            graphs.append(g)
+        us = timed(lambda i: graphs[i % N_WEIGHT_SETS].replay())
+        del graphs
+        nbytes = wbytes + sum(M * (k // 2 + 4) for k in kins) + sum(y.numel() * 2 for y in ys)
+        out[str(M)] = {"us_per_layer": round(us, 2), "gbs": round(nbytes / us / 1e3, 1),
+                       "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
+                       "us_per_layer_eager": round(us_eager, 2)}
+    return {"workload": "13b-shape decode step: 7 W4A4 linears (h=5120, f=13824) as 4 launches "
+                        "(qkv, o, gate_up, down on row-concatenated weights), bf16 out, "
+                        f"{wbytes / 1e6:.1f} MB of packed weights per layer; us_per_layer is a "
+                        "HIP-graph replay, us_per_layer_eager the same launches from Python",
+            "M": out}
+
+
 def copy_calibration(dev, nbytes=1 << 30, reps=5):
     """A plain device-to-device copy of known size, run so that the HBM
     counters (FETCH_SIZE, WRITE_SIZE) can be scaled to bytes: the counter
@@ -260,6 +339,10 @@ def main():
         "breakdown_ms": {k: round(v, 4) for k, v in tot.items()},
         "lib": p4q.version(),
     }
+    if not args.no_decode:
+        del st
+        torch.cuda.empty_cache()
+        res["decode_gemv"] = decode_gemv(dev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(res), flush=True)

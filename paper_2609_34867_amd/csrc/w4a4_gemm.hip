@@ -420,6 +420,138 @@ __global__ __launch_bounds__(256, 1) void k_w4a4_gemm_t256(const uint8_t *__rest
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Decode-shaped kernel (M <= 16): the weights are streamed from HBM once, so
+// the kernel is bound by HBM bandwidth and by how many bytes are in flight.
+// A 512-thread work-group computes 16 output rows (one MFMA fragment) at a
+// time; its 8 wavefronts split K into contiguous ranges of at most G_BATCH
+// 128-value k-tiles.  Work-groups are persistent: each walks row groups
+// blockIdx.x, blockIdx.x + gridDim.x, ... and loads the next group's
+// fragments before computing on the current ones, so HBM latency overlaps
+// with the MFMAs, the reduction and the epilogue.  Every weight byte is used
+// exactly once, so fragments go straight from HBM to registers.  The M
+// activation rows (zero-filled to 16 by the buffer range check) are the
+// MFMA's second operand.  Per k-tile, lane (r, c) loads the 16 bytes at
+// [64 kt + 16 c, +16) of weight row r and of activation row r; both operands
+// use the same k placement, so the MFMA sums every k exactly once.  The 8
+// partial accumulators are summed through LDS (integer sums: exact and
+// order-independent) before the epilogue.
+// ---------------------------------------------------------------------------
+constexpr int G_ROWS = 16;
+constexpr int G_WAVES = 8;
+constexpr int G_MAX_BATCH = 14;             // k-tiles per wavefront: K_in <= 14336
+
+// range-checked 16-byte load: offsets at or past the range read as zeros
+__device__ __forceinline__ uint4 gbuf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
+}
+
+template <int G_BATCH, bool BF16OUT>
+__global__ __launch_bounds__(64 * G_WAVES) void k_w4a4_gemv(const uint8_t *__restrict__ A,
+                                                            const float *__restrict__ sa,
+                                                            const uint8_t *__restrict__ W,
+                                                            const float *__restrict__ sw, int M,
+                                                            int N, int Kb, void *__restrict__ y,
+                                                            int64_t ldy,
+                                                            int32_t *__restrict__ acc_out) {
+    __shared__ v4i red[2][G_WAVES][64];                     // 16 KB, double-buffered
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int r = lane & 15, c = lane >> 4;
+    const int ktiles = (Kb + 63) / 64;
+    const int kt0 = (int)((int64_t)ktiles * wave / G_WAVES);
+    const int nk = (int)((int64_t)ktiles * (wave + 1) / G_WAVES) - kt0;   // <= G_BATCH
+    const int groups = (N + G_ROWS - 1) / G_ROWS;
+
+    // whole-matrix descriptors: rows past N or M fall outside the ranges and
+    // read as zero
+    const __amdgpu_buffer_rsrc_t dW =
+        __builtin_amdgcn_make_buffer_rsrc((void *)W, 0, (int)min((int64_t)N * Kb, (int64_t)0x7FFFFFFF), 0x00020000);
+    const __amdgpu_buffer_rsrc_t dA =
+        __builtin_amdgcn_make_buffer_rsrc((void *)A, 0, M * Kb, 0x00020000);
+    const uint32_t off = (uint32_t)(r * Kb + 16 * c + 64 * kt0);
+    uint32_t kin = 0;                                       // bit u: k-tile kt0+u in range
+#pragma unroll
+    for (int u = 0; u < G_BATCH; ++u)
+        if (u < nk && 64 * (kt0 + u) + 16 * c < Kb) kin |= 1u << u;
+
+    auto load_w = [&](int g, uint4 *w) {
+        const uint32_t base = (uint32_t)(g * G_ROWS) * (uint32_t)Kb + off;
+#pragma unroll
+        for (int u = 0; u < G_BATCH; ++u)
+            w[u] = gbuf_load16(dW, ((kin >> u) & 1) ? base + 64 * u : 0x80000000u);
+    };
+    auto unpack = [](uint32_t w0, uint32_t w1) {
+        return v4i{(int)nib_lo(w0), (int)nib_hi(w0), (int)nib_lo(w1), (int)nib_hi(w1)};
+    };
+
+    // this wavefront's activation fragments (packed), loaded once for all groups
+    uint4 a[G_BATCH];
+#pragma unroll
+    for (int u = 0; u < G_BATCH; ++u)
+        a[u] = gbuf_load16(dA, ((kin >> u) & 1) ? off + 64 * u : 0x80000000u);
+
+    // epilogue operands: lane l serves m = l & 15 and n = 16 g + 4 (l >> 4) + e
+    const int m = lane & 15;
+    const float sam = (m < M) ? sa[m] : 0.0f;
+    const __amdgpu_buffer_rsrc_t dS = __builtin_amdgcn_make_buffer_rsrc((void *)sw, 0, N * 4, 0x00020000);
+    auto load_sw = [&](int g) {
+        return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              dS, (uint32_t)(g * G_ROWS + 4 * (lane >> 4)) * 4u, 0, 0));
+    };
+
+    int g = blockIdx.x;
+    uint4 wc[G_BATCH];
+    float4 swc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (g < groups) {
+        load_w(g, wc);
+        swc = load_sw(g);
+    }
+    for (int it = 0; g < groups; g += gridDim.x, ++it) {
+        uint4 wn[G_BATCH];
+        float4 swn = make_float4(0.f, 0.f, 0.f, 0.f);
+        const int gn = g + gridDim.x;
+        if (gn < groups) {                                   // prefetch the next group
+            load_w(gn, wn);
+            swn = load_sw(gn);
+        }
+        v4i acc = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int u = 0; u < G_BATCH; ++u) {
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack(wc[u].x, wc[u].y),
+                                                        unpack(a[u].x, a[u].y), acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack(wc[u].z, wc[u].w),
+                                                        unpack(a[u].z, a[u].w), acc, 0, 0, 0);
+        }
+        const int buf = it & 1;
+        red[buf][wave][lane] = acc;
+        __syncthreads();
+        if (wave == 0) {
+            v4i s = red[buf][0][lane];
+#pragma unroll
+            for (int w = 1; w < G_WAVES; ++w) s += red[buf][w][lane];
+            const int nb = g * G_ROWS + 4 * (lane >> 4);
+            const float swv[4] = {swc.x, swc.y, swc.z, swc.w};
+            if (m < M) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int n = nb + e;
+                    if (n < N) {
+                        const int v = s[e] >> 8;
+                        store_out<BF16OUT>(y, (int64_t)m * ldy + n,
+                                           __fmul_rn(__fmul_rn((float)v, sam), swv[e]));
+                        if (acc_out) acc_out[(int64_t)m * N + n] = v;
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < G_BATCH; ++u) wc[u] = wn[u];
+        swc = swn;
+    }
+}
+
 }  // namespace
 
 size_t gemm_workspace_bytes(int, int, int) { return 0; }
@@ -428,6 +560,34 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
                             const uint8_t *w, const float *sw, p4q_dtype out_dt, void *y,
                             int64_t ldy, int32_t *acc_out, void *, size_t, hipStream_t stream) {
     const bool bf16 = (out_dt == P4Q_BF16);
+    // decode kernel: 32-bit buffer offsets need N * K_in / 2 < 2^31
+    if (M <= 16 && K <= 128 * G_WAVES * G_MAX_BATCH && (int64_t)N * (K / 2) < 0x7FFF0000LL) {
+        static int cus = 0;
+        if (cus == 0) {
+            int dev = 0;
+            if (hipGetDevice(&dev) != hipSuccess ||
+                hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+                cus <= 0)
+                cus = 256;
+        }
+        const int groups = (N + G_ROWS - 1) / G_ROWS;
+        const int per_wave = ((K + 127) / 128 + G_WAVES - 1) / G_WAVES;   // k-tiles per wavefront
+        auto go = [&](auto kern, int blocks_per_cu) {
+            hipLaunchKernelGGL(kern, dim3(min(groups, blocks_per_cu * cus)), dim3(64 * G_WAVES), 0,
+                               stream, a, sa, w, sw, M, N, K / 2, y, ldy, acc_out);
+            return hipGetLastError();
+        };
+#define P4Q_GEMV(NB, BPC)                                                                   \
+    if (per_wave <= NB)                                                                    \
+        return bf16 ? go(k_w4a4_gemv<NB, true>, BPC) : go(k_w4a4_gemv<NB, false>, BPC);
+        P4Q_GEMV(2, 2)
+        P4Q_GEMV(4, 2)
+        P4Q_GEMV(6, 2)
+        P4Q_GEMV(8, 1)
+        P4Q_GEMV(11, 1)
+        P4Q_GEMV(14, 1)
+#undef P4Q_GEMV
+    }
     if (M >= 1024 && N >= 1024) {
         const int tiles_m = (M + L_BM - 1) / L_BM, tiles_n = (N + L_BN - 1) / L_BN;
         const dim3 grid(tiles_m * tiles_n);

@@ -1,6 +1,8 @@
 """GPU parity of p4q_w4a4_linear against the oracle: int32 accumulators and
 fp16/bf16 outputs must match bit for bit (the epilogue's operation order is
 fixed, so 'within 1e-3 relative' is met with zero error)."""
+import functools
+
 import numpy as np
 import pytest
 import torch
@@ -114,3 +116,84 @@ def test_llava_next_b16_linears_sampled(li):
         m, n = int(rng.integers(cfg.M)), int(rng.integers(lin.n_out))
         racc, ry = oracle.w4a4_linear_entry(ap, sa, wp, sw, m, n, "bf16")
         assert acc[m, n] == racc and bits(y)[m, n] == ry
+
+
+@pytest.mark.parametrize("M", [1, 2, 4, 7, 16])
+@pytest.mark.parametrize("NK", [(5120, 5120), (5120, 13824), (1000, 4128), (33, 32), (47, 224)])
+def test_decode_gemv_shapes(M, NK):
+    """M <= 16 runs the HBM-streaming decode kernel: ragged N (not a multiple
+    of its 32-row groups), K not a multiple of its 128-value k-tiles, K split
+    unevenly over its 8 wavefronts, every M in the padded 16-row operand."""
+    N, K = NK
+    check_full(*codes_for(M, N, K, 31 * M + N + K), "bf16" if M % 2 else "fp16")
+
+
+@pytest.mark.parametrize("extreme", [-8, 7])
+def test_decode_gemv_extreme_codes(extreme):
+    check_full(*codes_for(16, 40, 65536, 5, extreme), "bf16")
+
+
+def test_decode_gemv_strided_output():
+    ap, sa, wp, sw = codes_for(3, 70, 512, 13)
+    y = torch.full((3, 80), -1.0, dtype=torch.bfloat16, device="cuda")
+    p4q.w4a4_linear(to_gpu(ap), to_gpu(sa), to_gpu(wp), to_gpu(sw), y=y)
+    torch.cuda.synchronize()
+    _, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
+    got = to_np(y)
+    assert np.array_equal(bits(got[:, :70]), bits(ry))
+    assert np.all(bits(got[:, 70:]) == 0xBF80)
+
+
+@functools.lru_cache(maxsize=None)
+def _weights_13b(li):
+    cfg = CONFIGS["stress13b_b8"]
+    w = weight(cfg, li)
+    return (w,) + tuple(oracle.quant_act(w))
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("M", [1, 4, 16])
+def test_decode_13b_layer(M):
+    """Decode step of the 13B-shape stress config: quantized decode-step
+    activations against all seven quantized linears (weights from the
+    config's recipe), bit-exact."""
+    from workload import gemv_activations
+    cfg = CONFIGS["stress13b_b8"]
+    for li, lin in enumerate(cfg.linears):
+        w, wp, sw = _weights_13b(li)
+        x = gemv_activations(cfg, M, lin.k_in)
+        xq = p4q.quant_act(to_gpu(x))
+        wq = p4q.quant_act(to_gpu(w))
+        y, acc = p4q.w4a4_linear(*xq, *wq, torch.bfloat16, return_acc=True)
+        torch.cuda.synchronize()
+        ap, sa = oracle.quant_act(x)
+        racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
+        assert (m := first_mismatch(to_np(acc), racc.astype(np.int32))) is None, (lin.name, m)
+        assert (m := first_mismatch(bits(to_np(y)), bits(ry))) is None, (lin.name, m)
+
+
+def test_decode_graph_replay_matches_eager():
+    """The decode linears captured in a HIP graph (as a serving loop runs
+    them): every replay, with eager work and synchronizations in between,
+    reproduces the eager outputs bit for bit."""
+    shapes = [(5120, 5120), (13824, 5120), (5120, 13824)]
+    M = 4
+    ops = [codes_for(M, N, K, 100 + i) for i, (N, K) in enumerate(shapes)]
+    ins = [tuple(to_gpu(x) for x in op) for op in ops]
+    ref = [p4q.w4a4_linear(*args, torch.bfloat16) for args in ins]
+    ys = [torch.empty_like(r) for r in ref]
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for args, yv in zip(ins, ys):
+            p4q.w4a4_linear(*args, y=yv)
+    for rep in range(3):
+        for yv in ys:
+            yv.fill_(float(rep + 1))                      # eager work between replays
+        junk = p4q.w4a4_linear(*ins[rep % 3], torch.bfloat16)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for r, yv in zip(ref, ys):
+            assert torch.equal(r.view(torch.int16), yv.view(torch.int16)), rep
+        del junk
