@@ -2,7 +2,7 @@
 // with the whole budget), four kernels on one stream:
 //
 //  1. k_concept_codes: fake-quantize the J concept rows of each sample to
-//     int8 codes (Q4, clip c).
+//     int8 codes (Q4, clip c), one work-group per row.
 //  2. k_select_score: one pass over the visual features.  Each wavefront
 //     holds one token row in registers, takes its absmax, quantizes it
 //     on-chip (the fake-quantized copy is never written), and forms the exact
@@ -46,31 +46,40 @@ __device__ __forceinline__ int64_t exact_key(int32_t D, int32_t Nv, int LS) {
 }
 
 // ---------------------------------------------------------------------------
-// 1. concept codes: one wavefront per concept row, int8 codes out
+// 1. concept codes: one 256-thread work-group per concept row (all of the
+//    row's loads issued at once), int8 codes out
 // ---------------------------------------------------------------------------
-template <bool BF16, bool CLIP1>
-__global__ __launch_bounds__(256) void k_concept_codes(const uint8_t *__restrict__ con, int rows,
-                                                       int d, float clip,
-                                                       int8_t *__restrict__ ccodes) {
-    const int lane = threadIdx.x & 63;
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= rows) return;
+template <int CH, bool BF16, bool CLIP1>
+__global__ __launch_bounds__(256) void k_concept_codes(const uint8_t *__restrict__ con, int d,
+                                                       float clip, int8_t *__restrict__ ccodes) {
+    __shared__ uint32_t s_max[4];
+    const int row = blockIdx.x, t = threadIdx.x;
     const int nchunk = d / 8;
     const uint4 *src = reinterpret_cast<const uint4 *>(con + (int64_t)row * d * 2);
     uint2 *dst = reinterpret_cast<uint2 *>(ccodes + (int64_t)row * d);
+    uint4 v[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const int q = t + 256 * c;
+        v[c] = (q < nchunk) ? src[q] : make_uint4(0, 0, 0, 0);
+    }
     uint32_t m2 = 0;
-    for (int q = lane; q < nchunk; q += 64) m2 = absmax_chunk(m2, src[q]);
-    const uint32_t mbits = wave_max_u32(max(m2 & 0xFFFFu, m2 >> 16));
+#pragma unroll
+    for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
+    const uint32_t mw = wave_max_u32(max(m2 & 0xFFFFu, m2 >> 16));
+    if ((t & 63) == 0) s_max[t >> 6] = mw;
+    __syncthreads();
+    const uint32_t mbits = max(max(s_max[0], s_max[1]), max(s_max[2], s_max[3]));
     const float s = row_scale<CLIP1>(mag_to_f32<BF16>(mbits), clip);
     const bool tiny = !(s >= kTinyScale);
     const float r = tiny ? 0.0f : 1.0f / s;
-    for (int q0 = 0; q0 < nchunk; q0 += 64) {
-        const int q = q0 + lane;
-        const uint4 v = (q < nchunk) ? src[q] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const int q = t + 256 * c;
         uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         uint32_t near = 0;
-        if (s != 0.0f && !tiny) q4_chunk_fast<BF16, CLIP1>(v, r, w, near);
-        if (s != 0.0f && (tiny || __any((int)near))) q4_chunk_exact<BF16>(v, s, w);
+        if (s != 0.0f && !tiny) q4_chunk_fast<BF16, CLIP1>(v[c], r, w, near);
+        if (s != 0.0f && (tiny || near)) q4_chunk_exact<BF16>(v[c], s, w);   // rare
         if (q < nchunk) dst[q] = make_uint2(bytes4(w[0], w[1], w[2], w[3]),
                                             bytes4(w[4], w[5], w[6], w[7]));
     }
@@ -291,10 +300,11 @@ __device__ __forceinline__ uint32_t waves_before(const uint32_t *wtot, int wave)
 //    on equal cosine".  MSD radix select with 11-bit digits from the top of X:
 //    the first digit is sign + exponent + 4 mantissa bits, which spreads the
 //    typical scores (most near zero) over many buckets; the select stops as
-//    soon as the boundary bucket is taken whole.
+//    soon as the boundary bucket is taken whole, or, when every candidate left
+//    in it carries the same key (a tie), by one ordered scan that keeps the
+//    lowest indices.
 // ---------------------------------------------------------------------------
 constexpr int kTkThreads = 1024;
-constexpr int kTkMaxE = 8;
 constexpr int kDigit = 11;
 constexpr int kBins = 1 << kDigit;
 constexpr int kLoBits = 16;          // low word of X: 3 mantissa bits + 13 index bits
@@ -332,43 +342,50 @@ __device__ __forceinline__ uint32_t comp_digit(const Composite &x, int lo, int w
     return (uint32_t)v & mask;
 }
 
+template <int E>
 __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__restrict__ keys,
                                                             int N, int J, int K,
                                                             int32_t *__restrict__ idx_out) {
     __shared__ __attribute__((aligned(16))) uint32_t hist[kBins];
     __shared__ __attribute__((aligned(16))) uint32_t wtot[kTkThreads / 64];
     __shared__ uint32_t sh_bucket, sh_gt, sh_eq;
+    __shared__ unsigned long long sh_hmin, sh_hmax;      // key bits of X above the index
+    __shared__ uint32_t sh_lmin, sh_lmax;
 
     const int b = blockIdx.x;
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
-    const int E = (N + kTkThreads - 1) / kTkThreads;
     for (int q = t; q < kBins; q += kTkThreads) hist[q] = 0;
+    if (t == 0) { sh_hmin = ~0ull; sh_hmax = 0; sh_lmin = ~0u; sh_lmax = 0; }
     __syncthreads();
     uint32_t kept = 0;
 
-    // keys of the next concept are loaded while the current one is selected
-    int64_t kn[kTkMaxE];
+    // thread t owns tokens t*E .. t*E+E-1; keys of the next concept are loaded
+    // while the current one is selected
+    int64_t kn[E];
     auto load_keys = [&](int j) {
         const int64_t *kj = keys + ((int64_t)b * J + j) * N;
 #pragma unroll
-        for (int e = 0; e < kTkMaxE; ++e) {
+        for (int e = 0; e < E; ++e) {
             const int i = t * E + e;
-            kn[e] = (e < E && i < N) ? kj[i] : 0;
+            kn[e] = (i < N) ? kj[i] : 0;
         }
     };
+    // prefetch of the next concept's keys only while registers allow it
+    constexpr bool kPrefetch = E <= 6;
     load_keys(0);
     for (int j = 0; j < J; ++j) {
         const uint32_t quota = (uint32_t)(K / J + (j < K % J ? 1 : 0));
-        Composite x[kTkMaxE];
+        if (!kPrefetch && j > 0) load_keys(j);
+        Composite x[E];
         uint32_t cont = 0;
 #pragma unroll
-        for (int e = 0; e < kTkMaxE; ++e) {
+        for (int e = 0; e < E; ++e) {
             const int i = t * E + e;
             x[e] = make_composite(kn[e], i);
-            if (e < E && i < N && !((kept >> e) & 1u)) cont |= 1u << e;
+            if (i < N && !((kept >> e) & 1u)) cont |= 1u << e;
         }
-        if (j + 1 < J) load_keys(j + 1);
+        if (kPrefetch && j + 1 < J) load_keys(j + 1);
         if (quota == 0) continue;                            // block-uniform
         uint32_t need = quota;
         int pos = kXBits;
@@ -376,7 +393,7 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__res
             const int w = min(kDigit, pos);
             const int lo = pos - w;
 #pragma unroll
-            for (int e = 0; e < kTkMaxE; ++e)
+            for (int e = 0; e < E; ++e)
                 if ((cont >> e) & 1u) atomicAdd(&hist[comp_digit(x[e], lo, w)], 1u);
             __syncthreads();
             // reverse-order inclusive scan: thread t covers bins kBins-1-2t, kBins-2-2t
@@ -393,16 +410,54 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__res
             if (e1 < need && need <= e1 + c1) { sh_bucket = b1; sh_gt = e1; sh_eq = c1; }
             __syncthreads();
             const uint32_t bucket = sh_bucket, gt = sh_gt, eq = sh_eq;
+            // key part of X: hi (67 - 3 bits) and the 3 key bits of lo
+            unsigned long long hmin = ~0ull, hmax = 0;
+            uint32_t lmin = ~0u, lmax = 0;
 #pragma unroll
-            for (int e = 0; e < kTkMaxE; ++e) {
+            for (int e = 0; e < E; ++e) {
                 if ((cont >> e) & 1u) {
                     const uint32_t dg = comp_digit(x[e], lo, w);
                     if (dg > bucket) { kept |= 1u << e; cont &= ~(1u << e); }
                     else if (dg < bucket) { cont &= ~(1u << e); }
+                    else {
+                        hmin = min(hmin, (unsigned long long)x[e].hi);
+                        hmax = max(hmax, (unsigned long long)x[e].hi);
+                        lmin = min(lmin, x[e].lo >> 13);
+                        lmax = max(lmax, x[e].lo >> 13);
+                    }
                 }
             }
             need -= gt;
             if (eq == need || lo == 0) { kept |= cont; break; }   // block-uniform
+            // Still ambiguous.  If every remaining candidate has the same key
+            // (a tie in cosine), the lower indices win: take the `need` first
+            // candidates in token order with one ordered scan instead of
+            // walking the remaining digits down to the index bits.
+            if (cont) {
+                atomicMin(&sh_hmin, hmin);
+                atomicMax(&sh_hmax, hmax);
+                atomicMin(&sh_lmin, lmin);
+                atomicMax(&sh_lmax, lmax);
+            }
+            __syncthreads();
+            const bool tied = (sh_hmin == sh_hmax) && (sh_lmin == sh_lmax);
+            __syncthreads();
+            if (t == 0) { sh_hmin = ~0ull; sh_hmax = 0; sh_lmin = ~0u; sh_lmax = 0; }
+            if (tied) {                                          // block-uniform
+                const uint32_t c = __builtin_popcount(cont);
+                const uint32_t ic = wave_inclusive_scan(c);
+                if (lane == 63) wtot[wave] = ic;
+                __syncthreads();
+                uint32_t rank = ic - c + waves_before(wtot, wave);
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    if ((cont >> e) & 1u) {
+                        if (rank < need) kept |= 1u << e;
+                        ++rank;
+                    }
+                __syncthreads();                                 // wtot reused below
+                break;
+            }
             pos = lo;
         }
     }
@@ -416,7 +471,7 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__res
     uint32_t opos = inc - cnt + waves_before(wtot, wave);
     int32_t *out = idx_out + (int64_t)b * K;
 #pragma unroll
-    for (int e = 0; e < kTkMaxE; ++e)
+    for (int e = 0; e < E; ++e)
         if (((kept >> e) & 1u) && opos < (uint32_t)K) out[opos++] = t * E + e;
 }
 
@@ -493,8 +548,16 @@ hipError_t launch_score_typed(int B, int N, int d, int J, float clip, int LS, co
 template <bool BF16, bool CLIP1>
 hipError_t launch_concepts(int rows, int d, float clip, const void *con, int8_t *cc,
                            hipStream_t stream) {
-    hipLaunchKernelGGL((k_concept_codes<BF16, CLIP1>), dim3((rows + 3) / 4), dim3(256), 0,
-                       stream, static_cast<const uint8_t *>(con), rows, d, clip, cc);
+    const int per = (d / 8 + 255) / 256;            // d <= 16384: at most 8 chunks per thread
+    const uint8_t *src = static_cast<const uint8_t *>(con);
+    if (per <= 1)
+        hipLaunchKernelGGL((k_concept_codes<1, BF16, CLIP1>), dim3(rows), dim3(256), 0, stream, src, d, clip, cc);
+    else if (per <= 2)
+        hipLaunchKernelGGL((k_concept_codes<2, BF16, CLIP1>), dim3(rows), dim3(256), 0, stream, src, d, clip, cc);
+    else if (per <= 4)
+        hipLaunchKernelGGL((k_concept_codes<4, BF16, CLIP1>), dim3(rows), dim3(256), 0, stream, src, d, clip, cc);
+    else
+        hipLaunchKernelGGL((k_concept_codes<8, BF16, CLIP1>), dim3(rows), dim3(256), 0, stream, src, d, clip, cc);
     return hipGetLastError();
 }
 
@@ -538,8 +601,16 @@ hipError_t launch_select(p4q_dtype dt, int B, int N, int d, const void *vis, con
     else e = clip1 ? launch_score_typed<false, true>(B, N, d, J, clip, LS, vis, ws, stream)
                    : launch_score_typed<false, false>(B, N, d, J, clip, LS, vis, ws, stream);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_select_topk, dim3(B), dim3(kTkThreads), 0, stream, ws.keys, N, J, K,
-                       idx_out);
+    switch ((N + kTkThreads - 1) / kTkThreads) {    // tokens per thread, N <= 8192
+#define P4Q_TK(E)                                                                            \
+    case E:                                                                                 \
+        hipLaunchKernelGGL(k_select_topk<E>, dim3(B), dim3(kTkThreads), 0, stream, ws.keys, N, \
+                           J, K, idx_out);                                                  \
+        break;
+        P4Q_TK(1) P4Q_TK(2) P4Q_TK(3) P4Q_TK(4) P4Q_TK(5) P4Q_TK(6) P4Q_TK(7) P4Q_TK(8)
+#undef P4Q_TK
+        default: return hipErrorInvalidValue;
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t rows = (int64_t)B * (K + T);
     hipLaunchKernelGGL(k_select_gather, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream,
