@@ -329,7 +329,7 @@ def main():
                    "M": cfg.M, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
                      "unit": "TOPS", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
-                     "traffic": traffic_from_profile(), "kernel": "k_w4a4_gemm_t256",
+                     "traffic": traffic_from_profile(), "kernel": "k_w4a4_gemm_2cu",
                      "per_launch": "2*M*n_out*k_in int ops, averaged over the 7 launches of a step; "
                                    "traffic in HBM bytes per launch"},
         "gemm_tops": round(gemm_tops, 2),

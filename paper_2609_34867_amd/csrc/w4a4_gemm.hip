@@ -157,23 +157,31 @@ __global__ __launch_bounds__(kThreads) void k_w4a4_gemm(const uint8_t *__restric
 
 
 // ---------------------------------------------------------------------------
-// Large-M kernel: 256 x 256 block tile, 4 wavefronts of 128 x 128 (8 x 8 MFMA
-// tiles, 256 accumulator registers per lane).
+// Large-M kernel: 256 (m) x 128 (n) block tile, 4 wavefronts of 128 x 64
+// (4 x 8 tiles of v_mfma_i32_16x16x64_i8, 128 accumulator registers), and
+// at most 256 registers per lane, so TWO blocks are resident per CU: one
+// wavefront of each block on every SIMD.  While one block waits on its
+// operand DMA, its LDS reads or its epilogue, the other block's wavefront
+// keeps the SIMD's matrix unit busy.
 //  * Packed int4 tiles go straight from HBM to LDS (buffer_load ... lds): no
 //    staging registers and no LDS store instructions.  Out-of-range rows and
-//    k-chunks are zero-filled by the buffer's range check.  A ring of 4 LDS
-//    stages (32 KB each) keeps 3 k-tiles in flight; waits are explicit
+//    k-chunks are zero-filled by the buffer's range check.  A ring of 3 LDS
+//    stages (24 KB each) keeps 2 k-tiles in flight; waits are explicit
 //    (vmcnt + a bare s_barrier).
 //  * After the LDS read each wave unpacks its fragments to int8 in registers.
 //  * The weight fragment is the MFMA's first operand: lane l then owns four
-//    consecutive output columns n of one row m, stored as one 8-byte write.
+//    consecutive output columns n of one row m.
+//  * Epilogue: the dequantized tile is assembled in LDS and leaves as full
+//    256-byte row segments, one 16-byte store per lane, with no waits between
+//    stores.  The block's scales were fetched into LDS with the first stage.
 //  * Work-group ids are remapped so that each XCD (ids are dealt round-robin
 //    over 8 XCDs) walks a contiguous, M-grouped range of tiles, sharing A and
 //    W panels in its own L2.
 // ---------------------------------------------------------------------------
-constexpr int L_BM = 256, L_BN = 256;
-constexpr int L_STAGES = 4;
-constexpr int L_STAGE = (L_BM + L_BN) * BKB;     // 32 KB of packed codes
+constexpr int L_BM = 256, L_BN = 128;
+constexpr int L_STAGES = 3;
+constexpr int L_STAGE = (L_BM + L_BN) * BKB;       // 24 KB of packed codes
+constexpr int L_SCALE_OFF = L_STAGES * L_STAGE;    // sa[256], sw[128] (fp32)
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 
@@ -186,14 +194,20 @@ __device__ __forceinline__ v4i buffer_desc(const void *base, uint32_t bytes) {
     return v4i{(int)(uint32_t)b, (int)((b >> 32) & 0xFFFFu), (int)bytes, 0x00020000};
 }
 
-// 16 bytes per lane from a buffer straight into LDS at lds + 16 * lane.  Issued
-// as inline asm so the compiler does not add its conservative vmcnt(0) before
-// every LDS read (it cannot tell the ring slots apart); the kernel waits with
-// explicit vmcnt counts instead.
+// 16 (or 4) bytes per lane from a buffer straight into LDS at lds + 16 *
+// lane (4 * lane).  Issued as inline asm so the compiler does not add its
+// conservative vmcnt(0) before every LDS read (it cannot tell the ring slots
+// apart); the kernel waits with explicit vmcnt counts instead.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(v4i desc, uint32_t voffset, uint32_t lds_addr) {
     asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voffset), "s"(desc), "s"(lds_addr)
+                 : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(v4i desc, uint32_t voffset, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dword %0, %1, 0 offen lds"
                  :
                  : "v"(voffset), "s"(desc), "s"(lds_addr)
                  : "memory", "m0");
@@ -218,16 +232,20 @@ __device__ __forceinline__ void tile_coords(int wg, int tiles_m, int tiles_n, in
     tn = in_g / gsize;
 }
 
-template <bool BF16OUT>
-__global__ __launch_bounds__(256, 1) void k_w4a4_gemm_t256(const uint8_t *__restrict__ A,
-                                                           const float *__restrict__ sa,
-                                                           const uint8_t *__restrict__ W,
-                                                           const float *__restrict__ sw, int M,
-                                                           int N, int Kb, void *__restrict__ y,
-                                                           int64_t ldy,
-                                                           int32_t *__restrict__ acc_out,
-                                                           int tiles_m, int tiles_n) {
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[L_STAGES * L_STAGE];
+__device__ __forceinline__ v4i unpack2(uint32_t w0, uint32_t w1) {
+    return v4i{(int)nib_lo(w0), (int)nib_hi(w0), (int)nib_lo(w1), (int)nib_hi(w1)};
+}
+
+template <bool BF16OUT, bool ACC>
+__global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restrict__ A,
+                                                          const float *__restrict__ sa,
+                                                          const uint8_t *__restrict__ W,
+                                                          const float *__restrict__ sw, int M,
+                                                          int N, int Kb, void *__restrict__ y,
+                                                          int64_t ldy,
+                                                          int32_t *__restrict__ acc_out,
+                                                          int tiles_m, int tiles_n) {
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[L_STAGES * L_STAGE + 1536];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     int tm, tn;
@@ -235,186 +253,184 @@ __global__ __launch_bounds__(256, 1) void k_w4a4_gemm_t256(const uint8_t *__rest
     const int m0 = tm * L_BM, n0 = tn * L_BN;
     const int ktiles = (Kb + BKB - 1) / BKB;
 
-    // buffer views of this block's 256 A rows and 256 W rows
     const v4i dA = buffer_desc(A + (int64_t)m0 * Kb, (uint32_t)(min(M - m0, L_BM) * Kb));
     const v4i dW = buffer_desc(W + (int64_t)n0 * Kb, (uint32_t)(min(N - n0, L_BN) * Kb));
 
-    // DMA mapping: instruction i of wave w fills LDS bytes [(4w+i)*1024, +1024)
-    // = rows 16(4w+i) .. +16; lane L -> row 16(4w+i) + L/4, slot L%4, which
-    // holds k-chunk c = slot ^ ((row >> 1) & 3) of that row.
+    // DMA: one 1 KB instruction fills 16 rows of 64 bytes; lane L -> row
+    // +L/4, slot L%4, which holds k-chunk (L%4) ^ ((row >> 1) & 3).  Wave w
+    // copies A rows [64w, 64w+64) (4 instructions) and W rows [32w, 32w+32)
+    // (2 instructions).
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    uint32_t voff[4];
-    int kc[4];
+    uint32_t voffA[4], voffW[2];
+    int kcA[4], kcW[2];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int row = 16 * (4 * wave + i) + (lane >> 2);
-        kc[i] = ((lane & 3) ^ ((row >> 1) & 3)) * 16;
-        voff[i] = (uint32_t)(row * Kb + kc[i]);
+        const int row = 64 * wave + 16 * i + (lane >> 2);
+        kcA[i] = ((lane & 3) ^ ((row >> 1) & 3)) * 16;
+        voffA[i] = (uint32_t)(row * Kb + kcA[i]);
     }
-    const uint32_t lds0 = lds_addr(smem) + wave_u * 4096;
-    auto issue = [&](int slot, int kt) {
-        const uint32_t base = lds0 + slot * L_STAGE;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int row = 32 * wave + 16 * i + (lane >> 2);
+        kcW[i] = ((lane & 3) ^ ((row >> 1) & 3)) * 16;
+        voffW[i] = (uint32_t)(row * Kb + kcW[i]);
+    }
+    const uint32_t ldsA = lds_addr(smem) + wave_u * 4096;
+    const uint32_t ldsW = lds_addr(smem) + L_BM * BKB + wave_u * 2048;
+    auto issue = [&](int slot, int kt) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const bool kin = kt * BKB + kc[i] < Kb;
-            const uint32_t o = kin ? voff[i] + (uint32_t)(kt * BKB) : 0x80000000u;
-            dma16(dA, o, base + i * 1024);
-            dma16(dW, o, base + L_BM * BKB + i * 1024);
+            const uint32_t o = (kt * BKB + kcA[i] < Kb) ? voffA[i] + (uint32_t)(kt * BKB) : 0x80000000u;
+            dma16(dA, o, ldsA + slot * L_STAGE + i * 1024);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const uint32_t o = (kt * BKB + kcW[i] < Kb) ? voffW[i] + (uint32_t)(kt * BKB) : 0x80000000u;
+            dma16(dW, o, ldsW + slot * L_STAGE + i * 1024);
         }
     };
 
-    v4i acc[8][8];
-#pragma unroll
-    for (int f = 0; f < 8; ++f)
-#pragma unroll
-        for (int g = 0; g < 8; ++g) acc[f][g] = v4i{0, 0, 0, 0};
-
-    // fragment addresses inside a stage: frags 0..7 = W rows, 8..15 = A rows
-    const int c = lane >> 4;
-    uint32_t foff[16];
-#pragma unroll
-    for (int f = 0; f < 8; ++f) {
-        const int wr = wn * 128 + f * 16 + (lane & 15);
-        foff[f] = L_BM * BKB + wr * BKB + ((c ^ ((wr >> 1) & 3)) << 4);
-        const int ar = wm * 128 + f * 16 + (lane & 15);
-        foff[8 + f] = ar * BKB + ((c ^ ((ar >> 1) & 3)) << 4);
+    {   // the block's scales -> LDS (zeros past M / N), ahead of the stages
+        const v4i dSa = buffer_desc(sa + m0, (uint32_t)(min(M - m0, L_BM) * 4));
+        const v4i dSw = buffer_desc(sw + n0, (uint32_t)(min(N - n0, L_BN) * 4));
+        const uint32_t sbase = lds_addr(smem) + L_SCALE_OFF;
+        dma4(dSa, (uint32_t)(64 * wave + lane) * 4u, sbase + wave_u * 256);
+        if (wave_u < 2) dma4(dSw, (uint32_t)(64 * wave + lane) * 4u, sbase + 1024 + wave_u * 256);
     }
-    auto read_frags = [&](int slot, uint4 *p) {
-        const uint8_t *base = smem + slot * L_STAGE;
+    issue(0, 0);
+    if (ktiles > 1) issue(1, 1);
+
+    v4i acc[4][8];
 #pragma unroll
-        for (int f = 0; f < 16; ++f) p[f] = *reinterpret_cast<const uint4 *>(base + foff[f]);
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+
+    // Fragments: W f = 0..3 (rows wn*64 + 16f), A f = 4..11 (rows
+    // wm*128 + 16(f-4)).  Lane l reads row l%16, chunk l/16 (32 k values;
+    // words x,y feed k-step 0 and z,w k-step 1 -- the same placement for A
+    // and W, so every k meets its partner exactly once).
+    const int r16 = lane & 15, cq = lane >> 4;
+    const uint32_t cofs = (uint32_t)((cq ^ ((r16 >> 1) & 3)) << 4);
+    const uint32_t fW = L_BM * BKB + (wn * 64 + r16) * BKB + cofs;
+    const uint32_t fA = (wm * 128 + r16) * BKB + cofs;
+    uint4 P[12];
+    auto read_tile = [&](int slot) __attribute__((always_inline)) {
+        const uint8_t *b = smem + slot * L_STAGE;
+#pragma unroll
+        for (int f = 0; f < 12; ++f) {
+            const uint32_t o = (f < 4) ? fW + f * 1024 : fA + (f - 4) * 1024;
+            P[f] = *reinterpret_cast<const uint4 *>(b + o);
+        }
     };
-    auto unpack = [&](uint32_t w0, uint32_t w1) {
-        return v4i{(int)nib_lo(w0), (int)nib_hi(w0), (int)nib_lo(w1), (int)nib_hi(w1)};
+    auto operands = [&](int s, v4i *u) __attribute__((always_inline)) {
+#pragma unroll
+        for (int f = 0; f < 12; ++f) u[f] = s ? unpack2(P[f].z, P[f].w) : unpack2(P[f].x, P[f].y);
     };
-    auto mfma_step = [&](const v4i *u) {
+    auto mfma_step = [&](const v4i *u) __attribute__((always_inline)) {
 #pragma unroll
-        for (int f = 0; f < 8; ++f)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int g = 0; g < 8; ++g)
-                acc[f][g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(u[f], u[8 + g], acc[f][g], 0,
-                                                                  0, 0);
+            for (int j = 0; j < 8; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(u[i], u[4 + j], acc[i][j], 0, 0, 0);
     };
 
-#pragma unroll
-    for (int s = 0; s < L_STAGES - 1; ++s)
-        if (s < ktiles) issue(s, s);
-
-    // Software pipeline.  Entering iteration kt, u0 holds the unpacked step-0
-    // operands of tile kt and pc the packed step-1 words.  Phase A runs the
-    // step-0 MFMAs while the next tile's fragments are read from LDS and the
-    // step-1 operands are unpacked; phase B runs the step-1 MFMAs while the
-    // next tile's step-0 operands are unpacked.
-    v4i u0[16], u1[16];
-    uint2 pc[16];
-    uint4 pn[16];
-    if (ktiles > 2) asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
-    else if (ktiles == 2) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-    read_frags(0, pn);
-#pragma unroll
-    for (int f = 0; f < 16; ++f) {
-        u0[f] = unpack(pn[f].x, pn[f].y);
-        pc[f] = make_uint2(pn[f].z, pn[f].w);
-    }
-    for (int kt = 0; kt + 1 < ktiles; ++kt) {
-        // tile kt+1 must have landed (from every wave) before phase A reads it
-        if (kt + 2 < ktiles) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+    v4i u0[12], u1[12];
+    for (int kt = 0; kt < ktiles; ++kt) {
+        // tile kt has landed (from every wave) and every wave is done with
+        // tile kt-1, whose slot the DMA of tile kt+2 now overwrites
+        if (kt + 1 < ktiles) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
         else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-        if (kt + L_STAGES - 1 < ktiles) issue((kt + L_STAGES - 1) % L_STAGES, kt + L_STAGES - 1);
-        // phase A
-        read_frags((kt + 1) % L_STAGES, pn);
-#pragma unroll
-        for (int f = 0; f < 16; ++f) u1[f] = unpack(pc[f].x, pc[f].y);
+        if (kt + 2 < ktiles) issue((kt + 2) % L_STAGES, kt + 2);
+        read_tile(kt % L_STAGES);
+        operands(0, u0);
+        __builtin_amdgcn_sched_barrier(0);
+        operands(1, u1);
         mfma_step(u0);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // 1 LDS read
+        for (int i = 0; i < 24; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // 1 MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // 2 VALU
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);   // 3 VALU
         }
-        // phase B
-#pragma unroll
-        for (int f = 0; f < 16; ++f) {
-            u0[f] = unpack(pn[f].x, pn[f].y);
-            pc[f] = make_uint2(pn[f].z, pn[f].w);
-        }
+        __builtin_amdgcn_sched_barrier(0);
         mfma_step(u1);
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        }
+        __builtin_amdgcn_sched_barrier(0);
     }
-    // last tile
-#pragma unroll
-    for (int f = 0; f < 16; ++f) u1[f] = unpack(pc[f].x, pc[f].y);
-    mfma_step(u0);
-    mfma_step(u1);
 
-    // epilogue: acc[f][g] lane l, reg e -> n = n0 + wn*128 + f*16 + 4*(l>>4) + e,
-    //                                       m = m0 + wm*128 + g*16 + (l&15)
+    // Epilogue.  acc[i][j] lane l, register e holds
+    //   n = n0 + wn*64 + 16 i + 4 (l/16) + e,  m = m0 + wm*128 + 16 j + l%16.
+    // The 256 x 128 tile is assembled in LDS: row m of 256 bytes, 8-byte unit
+    // u (4 columns) stored at unit u ^ 2 (m & 15), which keeps both the
+    // 8-byte writes and the 16-byte row reads free of bank conflicts.
+    __syncthreads();
+    const float *s_sa = reinterpret_cast<const float *>(smem + L_SCALE_OFF);
+    const float *s_sw = s_sa + L_BM;
     float sam[8];
 #pragma unroll
-    for (int g = 0; g < 8; ++g) {
-        const int m = m0 + wm * 128 + g * 16 + (lane & 15);
-        sam[g] = (m < M) ? sa[m] : 0.0f;
-    }
-    const bool vec_ok = ((ldy & 3) == 0) && ((reinterpret_cast<uintptr_t>(y) & 7) == 0);
+    for (int j = 0; j < 8; ++j) sam[j] = s_sa[wm * 128 + 16 * j + r16];
 #pragma unroll
-    for (int f = 0; f < 8; ++f) {
-        const int nb = n0 + wn * 128 + f * 16 + 4 * (lane >> 4);
-        float swn[4];
+    for (int i = 0; i < 4; ++i) {
+        const int nl = wn * 64 + 16 * i + 4 * cq;
+        const float4 swv = *reinterpret_cast<const float4 *>(s_sw + nl);
+        const float swe[4] = {swv.x, swv.y, swv.z, swv.w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) swn[e] = (nb + e < N) ? sw[nb + e] : 0.0f;
-#pragma unroll
-        for (int g = 0; g < 8; ++g) {
-            const int m = m0 + wm * 128 + g * 16 + (lane & 15);
-            if (m >= M) continue;
+        for (int j = 0; j < 8; ++j) {
             int v[4];
             float o[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                v[e] = acc[f][g][e] >> 8;
-                o[e] = __fmul_rn(__fmul_rn((float)v[e], sam[g]), swn[e]);
+                v[e] = acc[i][j][e] >> 8;
+                o[e] = __fmul_rn(__fmul_rn((float)v[e], sam[j]), swe[e]);
             }
-            const int64_t off = (int64_t)m * ldy + nb;
-            if (vec_ok && nb + 3 < N) {
-                uint2 packed;
-                if constexpr (BF16OUT) {
-                    // v_cvt_pk_bf16_f32: two fp32 -> bf16, round to nearest even
-                    packed.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{o[0], o[1]}, bf2));
-                    packed.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{o[2], o[3]}, bf2));
-                } else {
-                    uint32_t h[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        float ov = o[e];
-                        asm volatile("" : "+v"(ov));
-                        h[e] = __builtin_bit_cast(uint16_t, (_Float16)ov);
-                    }
-                    packed = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
-                }
-                *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(y) + off) = packed;
+            uint2 packed;
+            if constexpr (BF16OUT) {
+                // v_cvt_pk_bf16_f32: two fp32 -> bf16, round to nearest even
+                packed.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{o[0], o[1]}, bf2));
+                packed.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{o[2], o[3]}, bf2));
             } else {
+                uint32_t h[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (nb + e < N) store_out<BF16OUT>(y, off + e, o[e]);
+                for (int e = 0; e < 4; ++e) {
+                    float ov = o[e];
+                    asm volatile("" : "+v"(ov));
+                    h[e] = __builtin_bit_cast(uint16_t, (_Float16)ov);
+                }
+                packed = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
             }
-            if (acc_out) {
+            const int r = wm * 128 + 16 * j + r16;
+            const int u = (nl >> 2) ^ (r16 << 1);
+            *reinterpret_cast<uint2 *>(smem + r * 256 + u * 8) = packed;
+            if constexpr (ACC) {
+                const int m = m0 + r, nb = n0 + nl;
+                if (m < M) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (nb + e < N) acc_out[(int64_t)m * N + nb + e] = v[e];
+                    for (int e = 0; e < 4; ++e)
+                        if (nb + e < N) acc_out[(int64_t)m * N + nb + e] = v[e];
+                }
+            }
+        }
+    }
+    __syncthreads();
+    const int rows_left = M - m0, cols_left = N - n0;
+    const bool vec16 = ((ldy & 7) == 0) && ((reinterpret_cast<uintptr_t>(y) & 15) == 0);
+    const bool full = vec16 && rows_left >= L_BM && cols_left >= L_BN;
+    const int cch = lane & 15;
+    uint16_t *yb = static_cast<uint16_t *>(y) + (int64_t)m0 * ldy + n0 + 8 * cch;
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+        const int r = 64 * wave + 4 * i + (lane >> 4);
+        const uint4 val = *reinterpret_cast<const uint4 *>(smem + r * 256 + ((cch ^ (r & 15)) << 4));
+        uint16_t *dst = yb + (int64_t)r * ldy;
+        if (full) {
+            *reinterpret_cast<uint4 *>(dst) = val;
+        } else if (r < rows_left) {
+            if (vec16 && 8 * cch + 8 <= cols_left) {
+                *reinterpret_cast<uint4 *>(dst) = val;
+            } else {
+                const uint32_t w4[4] = {val.x, val.y, val.z, val.w};
+#pragma unroll
+                for (int jj = 0; jj < 8; ++jj)
+                    if (8 * cch + jj < cols_left) dst[jj] = (uint16_t)(w4[jj >> 1] >> (16 * (jj & 1)));
             }
         }
     }
@@ -591,13 +607,13 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
     if (M >= 1024 && N >= 1024) {
         const int tiles_m = (M + L_BM - 1) / L_BM, tiles_n = (N + L_BN - 1) / L_BN;
         const dim3 grid(tiles_m * tiles_n);
-        if (bf16)
-            hipLaunchKernelGGL(k_w4a4_gemm_t256<true>, grid, dim3(256), 0, stream, a, sa, w, sw,
-                               M, N, K / 2, y, ldy, acc_out, tiles_m, tiles_n);
-        else
-            hipLaunchKernelGGL(k_w4a4_gemm_t256<false>, grid, dim3(256), 0, stream, a, sa, w, sw,
-                               M, N, K / 2, y, ldy, acc_out, tiles_m, tiles_n);
-        return hipGetLastError();
+        auto go = [&](auto kern) {
+            hipLaunchKernelGGL(kern, grid, dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy,
+                               acc_out, tiles_m, tiles_n);
+            return hipGetLastError();
+        };
+        if (bf16) return acc_out ? go(k_w4a4_gemm_2cu<true, true>) : go(k_w4a4_gemm_2cu<true, false>);
+        return acc_out ? go(k_w4a4_gemm_2cu<false, true>) : go(k_w4a4_gemm_2cu<false, false>);
     }
     const dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
     if (bf16)
