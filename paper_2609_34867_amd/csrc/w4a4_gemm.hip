@@ -345,6 +345,10 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         read_tile(kt % L_STAGES);
         operands(0, u0);
         __builtin_amdgcn_sched_barrier(0);
+        // raised issue priority while this wave streams MFMAs, so the SIMD's
+        // arbiter keeps the matrix unit fed and the other block's wave fills
+        // the gaps with its DMA, LDS and unpack work
+        __builtin_amdgcn_s_setprio(1);
         operands(1, u1);
         mfma_step(u0);
 #pragma unroll
@@ -355,6 +359,7 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         __builtin_amdgcn_sched_barrier(0);
         mfma_step(u1);
         __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(0);
     }
 
     // Epilogue.  acc[i][j] lane l, register e holds
