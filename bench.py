@@ -6,7 +6,9 @@ One step = one pass of the whole hot path over one batch:
   2. per-token int4 quantization of X, of the attention-output stand-in and
      of the MLP-activation stand-in (p4q_quant_act);
   3. the seven W4A4 linears of one decoder layer on those codes
-     (p4q_w4a4_linear): q/k/v/gate/up on X, o_proj, down_proj.
+     (p4q_w4a4_linear): q/k/v/gate/up on X, o_proj, down_proj, as four
+     launches: q|k|v and gate|up run as one GEMM each on row-concatenated
+     weights (fused projections, as serving stacks store them).
 Weights are quantized once, before timing (offline RTN, as in the paper).
 Four copies of the layer's weights rotate across steps so that successive
 steps read weights like successive decoder layers would (101 MB per layer at
@@ -70,17 +72,42 @@ def setup(cfg, dev):
     st["mq"] = (torch.empty((M, f // 2), dtype=torch.uint8, device=dev),
                 torch.empty((M,), dtype=torch.float32, device=dev))
     out_dt = torch.bfloat16 if cfg.out_dtype == "bf16" else torch.float16
-    weights = []
+    q = {}
     for li, lin in enumerate(cfg.linears):
-        wc, ws = p4q.quant_act(t(weight(cfg, li)))          # offline weight RTN
-        weights.append((wc, ws))
+        q[lin.name] = p4q.quant_act(t(weight(cfg, li)))     # offline weight RTN
+    weights = []
+    for gname, members, src in launch_groups(cfg):
+        weights.append((torch.cat([q[m][0] for m in members]),
+                        torch.cat([q[m][1] for m in members])))
+    del q
     torch.cuda.synchronize()
     st["weights"] = [[(wc.clone(), ws.clone()) for (wc, ws) in weights]
                      for _ in range(N_WEIGHT_SETS)]
-    st["y"] = [torch.empty((M, lin.n_out), dtype=out_dt, device=dev) for lin in cfg.linears]
+    st["y"] = [torch.empty((M, wc.shape[0]), dtype=out_dt, device=dev) for (wc, _) in weights]
     del weights
     torch.cuda.synchronize()
     return st
+
+
+def launch_groups(cfg):
+    """The layer's linears as launches: linears that read the same input run as
+    one GEMM on row-concatenated weights (q|k|v and gate|up), the layout serving
+    stacks keep their fused projections in.  Returns (name, members, source)."""
+    groups, seen = [], set()
+    for lin in cfg.linears:
+        if lin.name in seen:
+            continue
+        if lin.name == "q_proj":
+            members = ["q_proj", "k_proj", "v_proj"]
+            name = "qkv"
+        elif lin.name == "gate_proj":
+            members = ["gate_proj", "up_proj"]
+            name = "gate_up"
+        else:
+            members, name = [lin.name], lin.name
+        seen.update(members)
+        groups.append((name, members, lin.source))
+    return groups
 
 
 def step(cfg, st, layer, ev=None):
@@ -105,10 +132,10 @@ def step(cfg, st, layer, ev=None):
     rec("quant_act", lambda: p4q.quant_act(st["mlp"], codes=st["mq"][0], scales=st["mq"][1]))
     W = st["weights"][layer % N_WEIGHT_SETS]
     src = {"x": st["xq"], "attn": st["aq"], "mlp": st["mq"]}
-    for li, lin in enumerate(cfg.linears):
-        a = src[lin.source]
-        rec("gemm", lambda: p4q.w4a4_linear(a[0], a[1], W[li][0], W[li][1],
-                                            y=st["y"][li]))
+    for gi, (gname, members, source) in enumerate(launch_groups(cfg)):
+        a = src[source]
+        rec("gemm", lambda: p4q.w4a4_linear(a[0], a[1], W[gi][0], W[gi][1],
+                                            y=st["y"][gi]))
 
 
 class Events:
@@ -323,14 +350,14 @@ def main():
         "dtype": "int4 (int8 MFMA, int32 acc)", "data": "synthetic",
         "config": {"workload": f"{cfg.name}: select K={cfg.K} of N={cfg.N} tokens x d={cfg.d} "
                                f"fp16 for B={cfg.B} images + T={cfg.T} text, then 7 W4A4 "
-                               f"linears (h={cfg.d}, f={cfg.linears[4].n_out}) at M={cfg.M}, "
-                               f"{cfg.out_dtype} out",
+                               f"linears (h={cfg.d}, f={cfg.linears[4].n_out}) at M={cfg.M} as 4 "
+                               f"launches (q|k|v, o, gate|up, down), {cfg.out_dtype} out",
                    "B": cfg.B, "N": cfg.N, "d": cfg.d, "K": cfg.K, "T": cfg.T, "J": cfg.J,
                    "M": cfg.M, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
                      "unit": "TOPS", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
                      "traffic": traffic_from_profile(), "kernel": "k_w4a4_gemm_2cu",
-                     "per_launch": "2*M*n_out*k_in int ops, averaged over the 7 launches of a step; "
+                     "per_launch": "2*M*n_out*k_in int ops, averaged over the 4 launches of a step; "
                                    "traffic in HBM bytes per launch"},
         "gemm_tops": round(gemm_tops, 2),
         "selector_tokens_per_s": round(sel_tokens / (tot["select"] * 1e-3), 1),

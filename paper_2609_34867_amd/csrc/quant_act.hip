@@ -80,17 +80,19 @@ __global__ __launch_bounds__(kThreads) void k_quant_act(const uint8_t *__restric
         for (int c = 0; c < CH; ++c) packed[c] = 0u;
     } else {
         const bool tiny = !(s >= kTinyScale);
-        float fm = 0.0f;
-        if (!tiny) {
-            const float r = 1.0f / s;
+        const float r = tiny ? 0.0f : 1.0f / s;
 #pragma unroll
-            for (int c = 0; c < CH; ++c) packed[c] = chunk_fast<BF16, CLIP1>(v[c], r, fm);
-        }
-        // rare: this lane holds a value within 2^-19 of a rounding boundary
-        // (or the scale is tiny): recompute its chunks by exact division
-        if (tiny || fm > kNearHalf) {
-#pragma unroll
-            for (int c = 0; c < CH; ++c) packed[c] = chunk_exact<BF16>(v[c], s);
+        for (int c = 0; c < CH; ++c) {
+            float fm = 0.0f;
+            if (!tiny) packed[c] = chunk_fast<BF16, CLIP1>(v[c], r, fm);
+            // rare: a value of this chunk lies within 2^-19 of a rounding
+            // boundary in some lane (or the scale is tiny): recompute this
+            // chunk by exact division (wave-uniform branch)
+            if (tiny || __any(fm > kNearHalf)) {
+                uint4 vc = v[c];
+                asm volatile("" : "+v"(vc.x), "+v"(vc.y), "+v"(vc.z), "+v"(vc.w));
+                packed[c] = chunk_exact<BF16>(vc, s);
+            }
         }
     }
 #pragma unroll

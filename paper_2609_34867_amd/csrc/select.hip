@@ -15,6 +15,8 @@
 //  4. k_select_gather: copies the ORIGINAL rows of the kept tokens, then the
 //     text rows, into the pruned sequence with 16-byte vector copies.
 #include "p4q_internal.h"
+
+#include <algorithm>
 #include "q4_device.h"
 
 namespace p4q {
@@ -123,11 +125,11 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t o
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
 }
 
-constexpr int kRowsPerWave = 4;   // rows per wavefront (sums gathered for one key per lane)
+constexpr int kRowsPerWave = 8;   // rows per batch (sums gathered for one key per lane)
 
 template <int CH, int JMAX, bool BF16, bool CLIP1>
 __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uint8_t *__restrict__ vis, int N, int d,
-                                                      int J, float clip, int LS,
+                                                      int J, float clip, int LS, int rpw,
                                                       const int8_t *__restrict__ ccodes,
                                                       int32_t *__restrict__ stats,
                                                       int64_t *__restrict__ keys) {
@@ -150,18 +152,21 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
     }
     __syncthreads();
 
-    const int row0 = (blockIdx.x * 4 + wave) * kRowsPerWave;
-    if (row0 >= N) return;                                   // wave-uniform
-    const int nrows = min(kRowsPerWave, N - row0);
-    const uint8_t *vb = vis + ((int64_t)b * N + row0) * d * 2;
-    const __amdgpu_buffer_rsrc_t rv =
-        __builtin_amdgcn_make_buffer_rsrc((void *)vb, 0, nrows * d * 2, 0x00020000);
+    // this wavefront's rows [first, last), in batches of up to 8 (one stats
+    // word and one key per lane and batch)
+    const int first = (blockIdx.x * 4 + wave) * rpw;
+    const int last = min(first + rpw, N);
     uint32_t coff[CH];
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
         const int q = lane + 64 * c;
         coff[c] = (q < nchunk) ? (uint32_t)q * 16u : 0x80000000u;
     }
+    for (int row0 = first; row0 < last; row0 += kRowsPerWave) {   // wave-uniform
+    const int nrows = min(kRowsPerWave, last - row0);
+    const uint8_t *vb = vis + ((int64_t)b * N + row0) * d * 2;
+    const __amdgpu_buffer_rsrc_t rv =
+        __builtin_amdgcn_make_buffer_rsrc((void *)vb, 0, nrows * d * 2, 0x00020000);
     auto load_row = [&](int r, uint4 *v) {
 #pragma unroll
         for (int c = 0; c < CH; ++c) v[c] = buf_load16(rv, coff[c] + (uint32_t)(r * d * 2));
@@ -195,21 +200,21 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
 #pragma unroll
         for (int c = 0; c < CH; ++c) cv[c] = make_uint2(0, 0);
         if (s != 0.0f) {
-            uint32_t near = 0;
             const bool tiny = !(s >= kTinyScale);
-            if (!tiny) {
-                const float rc = 1.0f / s;
+            const float rc = tiny ? 0.0f : 1.0f / s;
 #pragma unroll
-                for (int c = 0; c < CH; ++c) {
-                    uint32_t w[8];
+            for (int c = 0; c < CH; ++c) {
+                uint32_t w[8];
+                uint32_t near = 0;
+                if (!tiny) {
                     q4_chunk_fast<BF16, CLIP1>(v[c], rc, w, near);
                     cv[c] = make_uint2(bytes4(w[0], w[1], w[2], w[3]), bytes4(w[4], w[5], w[6], w[7]));
                 }
-            }
-            if (tiny || __any((int)near)) {                  // wave-uniform, rare
-#pragma unroll
-                for (int c = 0; c < CH; ++c) {
-                    uint32_t w[8];
+                // wave-uniform and rare: some lane holds a value of this chunk
+                // within 2^-19 of a rounding boundary (exact fp16 ratios such as
+                // x = a/2 land on ties), or the scale is tiny.  Only this chunk
+                // is recomputed by exact division.
+                if (tiny || __any((int)near)) {
                     uint4 vc = v[c];
                     // opaque copy: keeps the exact path's fp16 -> fp32 conversions
                     // from being hoisted into (and paid on) the fast path
@@ -260,6 +265,7 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
             st[J] = myval;
         }
         if (JMAX == 8 && vslot == 0) st[J] = nv_r;
+    }
     }
 }
 
@@ -517,10 +523,25 @@ __global__ __launch_bounds__(256) void k_select_gather(const uint4 *__restrict__
 template <int CH, int JMAX, bool BF16, bool CLIP1>
 hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const void *vis,
                         const SelectWorkspace &ws, hipStream_t stream) {
-    const dim3 grid((N + 4 * kRowsPerWave - 1) / (4 * kRowsPerWave), B);
     const size_t lds = (size_t)JMAX * 64 * CH * 8;
+    // Rows per wavefront: enough that the whole grid is resident at once
+    // (one wave of blocks, no partly filled last wave).
+    static int resident = 0;                      // blocks per CU x CUs, per instantiation
+    if (resident == 0) {
+        int dev = 0, cus = 0, per_cu = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_select_score<CH, JMAX, BF16, CLIP1>, 256,
+                                                         lds) != hipSuccess ||
+            cus <= 0 || per_cu <= 0)
+            per_cu = 1, cus = 256;
+        resident = per_cu * cus;
+    }
+    const int64_t waves = 4LL * resident;
+    const int rpw = (int)std::max<int64_t>(1, ((int64_t)B * N + waves - 1) / waves);
+    const dim3 grid((N + 4 * rpw - 1) / (4 * rpw), B);
     hipLaunchKernelGGL((k_select_score<CH, JMAX, BF16, CLIP1>), grid, dim3(256), lds, stream,
-                       static_cast<const uint8_t *>(vis), N, d, J, clip, LS, ws.ccodes, ws.stats,
+                       static_cast<const uint8_t *>(vis), N, d, J, clip, LS, rpw, ws.ccodes, ws.stats,
                        ws.keys);
     return hipGetLastError();
 }

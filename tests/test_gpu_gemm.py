@@ -118,6 +118,31 @@ def test_llava_next_b16_linears_sampled(li):
         assert acc[m, n] == racc and bits(y)[m, n] == ry
 
 
+@pytest.mark.slow
+@pytest.mark.parametrize("members", [(0, 1, 2), (4, 5)])
+def test_llava_next_b16_fused_projections_sampled(members):
+    """The fused launches the benchmark runs: q|k|v (12288 x 4096) and
+    gate|up (22016 x 4096) on row-concatenated weights at M = 11264; the first
+    and last 32 rows and 1024 random entries are checked against the oracle."""
+    cfg = CONFIGS["next7b_b16"]
+    k_in = cfg.linears[members[0]].k_in
+    rng = np.random.default_rng(sum(members))
+    ap = rng.integers(0, 256, size=(cfg.M, k_in // 2), dtype=np.uint8)
+    sa = rng.uniform(1e-3, 4, size=cfg.M).astype(np.float32)
+    parts = [oracle.quant_act(weight(cfg, li)) for li in members]
+    wp = np.concatenate([p[0] for p in parts])
+    sw = np.concatenate([p[1] for p in parts])
+    y, acc = run_gpu(ap, sa, wp, sw, "bf16")
+    for rows in (slice(0, 32), slice(cfg.M - 32, cfg.M)):
+        racc, ry = oracle.w4a4_linear(ap[rows], sa[rows], wp, sw, "bf16")
+        assert (m := first_mismatch(acc[rows], racc.astype(np.int32))) is None, m
+        assert (m := first_mismatch(bits(y[rows]), bits(ry))) is None, m
+    for _ in range(1024):
+        m, n = int(rng.integers(cfg.M)), int(rng.integers(wp.shape[0]))
+        racc, ry = oracle.w4a4_linear_entry(ap, sa, wp, sw, m, n, "bf16")
+        assert acc[m, n] == racc and bits(y)[m, n] == ry
+
+
 @pytest.mark.parametrize("M", [1, 2, 4, 7, 16])
 @pytest.mark.parametrize("NK", [(5120, 5120), (5120, 13824), (1000, 4128), (33, 32), (47, 224)])
 def test_decode_gemv_shapes(M, NK):
