@@ -26,6 +26,10 @@ Acceleration"):
   weights, per-token 4-bit activations, group size -1, activation clip 1.0.
 * Appendix B.3: after calibration the weights are quantized with RTN for W4A4
   inference -- an integer GEMM on codes followed by dequantization.
+* Sec. 3.2 (Visual Saliency and Visual Diversity paragraphs, budget ratios
+  alpha = 0.3, beta = 0.2, gamma = 0.5): the full selector -- CLS-attention
+  top-k over the tokens left after Query Relevance, then max-min completion
+  on the cosines of the fake-quantized copies.
 
 Readings where the paper is silent (each is listed in the design doc):
 * code range [-8, 7], scale = fl32(fl32(c*absmax)/7); ties round half to even;
@@ -37,6 +41,10 @@ Readings where the paper is silent (each is listed in the design doc):
 * the Query-Relevance budget is split evenly across concepts (remainder to the
   earliest), concepts are processed in order, already-kept tokens are skipped;
 * retained rows are emitted in ascending index order, text rows after them;
+* stage budgets are floor(alpha K), floor(beta K) and the rest, in exact
+  integer arithmetic; equal CLS weights and equal max-cosines go to the lower
+  index; a zero code vector has cosine 0 with everything; with an empty
+  retained set the diversity stage starts from the most salient token;
 * epilogue y = out_rne(fl32(fl32(float(acc) * s_a[m]) * s_w[n])).
 """
 from __future__ import annotations
@@ -246,6 +254,93 @@ def select_batch(vis: np.ndarray, concepts: np.ndarray, text: np.ndarray, K: int
     D = np.stack([o[2] for o in outs])
     Nv = np.stack([o[3] for o in outs])
     return idx, tok, D, Nv
+
+
+# --------------------------------------------------------------------------
+# O3': the full progressive selector (Sec. 3.2, Eq. p4q_progressive_selection):
+#      Query Relevance, then Visual Saliency over the tokens left, then Visual
+#      Diversity completion, with budget ratios alpha, beta, gamma.
+# --------------------------------------------------------------------------
+def stage_budgets(K: int, alpha: Tuple[int, int] = (3, 10),
+                  beta: Tuple[int, int] = (2, 10)) -> Tuple[int, int, int]:
+    """Token budgets of the three stages: floor(alpha K), floor(beta K) and the
+    rest, in exact integer arithmetic (the paper's defaults alpha = 0.3,
+    beta = 0.2, gamma = 0.5 give (192, 128, 320) at K = 640)."""
+    kq = K * alpha[0] // alpha[1]
+    ks = K * beta[0] // beta[1]
+    return kq, ks, K - kq - ks
+
+
+def saliency_topk(a_cls: np.ndarray, kept: Sequence[int], k: int) -> List[int]:
+    """Visual Saliency: among the tokens not kept by the earlier stage, the k
+    with the largest head-averaged CLS-to-patch attention weight A_i^cls
+    (equal weights: lower index first).  Returns them best first."""
+    taken = set(int(i) for i in kept)
+    remaining = [i for i in range(len(a_cls)) if i not in taken]
+    order = sorted(remaining, key=lambda i: (-float(a_cls[i]), i))
+    return order[:k]
+
+
+def diversity_greedy(cv: np.ndarray, kept: Sequence[int], k: int,
+                     a_cls: np.ndarray) -> List[int]:
+    """Visual Diversity completion, k picks.  For every candidate left, the
+    maximum cosine similarity to the retained set is computed; the candidate
+    whose maximum is lowest is retained (equal maxima: lower index); the
+    retained set grows by it and the maxima are recomputed.
+
+    Cosines are those of the fake-quantized copies: cos(i, t) =
+    D_it / sqrt(Nv_i Nv_t) with D = cv cv^T, exactly (scales cancel), and 0
+    when either code vector is all zero.  They are compared through the exact
+    rational sgn(cos) cos^2.  With an empty retained set the first pick is the
+    most salient token (the paper leaves this case open)."""
+    cv64 = cv.astype(np.int64)
+    G = cv64 @ cv64.T                      # exact: every entry < 2^53
+    Nv = np.diag(G)
+    S = [int(i) for i in kept]
+    in_s = set(S)
+    picks: List[int] = []
+    if k > 0 and not S:
+        seed = saliency_topk(a_cls, [], 1)[0]
+        S.append(seed)
+        in_s.add(seed)
+        picks.append(seed)
+        k -= 1
+    cand = [i for i in range(cv.shape[0]) if i not in in_s]
+    m = {i: max(signed_cos2(G[i, t], Nv[i], Nv[t]) for t in S) for i in cand}
+    for _ in range(k):
+        best = min(cand, key=lambda i: (m[i], i))
+        picks.append(best)
+        S.append(best)
+        cand.remove(best)
+        del m[best]
+        for i in cand:
+            c = signed_cos2(G[i, best], Nv[i], Nv[best])
+            if c > m[i]:
+                m[i] = c
+    return picks
+
+
+def select_full(vis: np.ndarray, concepts: np.ndarray, a_cls: np.ndarray,
+                text: np.ndarray, K: int, kq: int, ks: int,
+                dtype: str = "fp16", clip: float = 1.0):
+    """The three-stage selector for one sample: kq tokens by Query Relevance,
+    ks by Visual Saliency over the rest, K - kq - ks by Visual Diversity.
+
+    vis [N, d], concepts [J, d], a_cls [N] (fp32 head-averaged CLS-to-patch
+    attention), text [T, d].  Returns (idx int32 [K] ascending, tokens
+    [K+T, d] storage dtype, (query picks sorted, saliency picks best first,
+    diversity picks in pick order))."""
+    N = vis.shape[0]
+    if not (1 <= K <= N) or kq < 0 or ks < 0 or kq + ks > K:
+        raise ValueError("need 1 <= K <= N and 0 <= kq, ks with kq + ks <= K")
+    cv, _ = quantize_rows(vis, dtype, clip)
+    cq, _ = quantize_rows(concepts, dtype, clip)
+    q_picks = [int(i) for i in select_query_relevance(cv, cq, kq)] if kq else []
+    s_picks = saliency_topk(a_cls, q_picks, ks)
+    d_picks = diversity_greedy(cv, q_picks + s_picks, K - kq - ks, a_cls)
+    idx = np.array(sorted(q_picks + s_picks + d_picks), dtype=np.int32)
+    tokens = np.concatenate([np.asarray(vis)[idx], np.asarray(text)], axis=0)
+    return idx, tokens, (q_picks, s_picks, d_picks)
 
 
 # --------------------------------------------------------------------------

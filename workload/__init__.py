@@ -19,7 +19,12 @@ Value recipe (identical for every config):
   * weights: N(0, 0.02^2), one independent stream per linear;
   * inputs of o_proj / down_proj (stand-ins for the attention output and the
     gated MLP activation): drawn like the visual features, each with its own
-    outlier channels.
+    outlier channels;
+  * CLS-to-patch attention (stand-in for the vision tower's final-layer
+    attention that the Visual Saliency stage reads, Sec. 3.2): per image
+    tile of 576 patches and per head (16 heads), a softmax of N(0, 3^2)
+    logits over the tile's patches, averaged over the heads; the tiles'
+    weights are concatenated (one global ranking over all tiles).
 All values are drawn in float32 with numpy's PCG64 and cast to fp16 with
 round-to-nearest-even.  The seed of every tensor is
 SeedSequence([42, config_id, tensor_id, sample]); 42 echoes the paper's seed.
@@ -36,6 +41,7 @@ SEED = 42
 # tensor ids of the seed tree
 _T_VIS, _T_TEXT, _T_OUTLIER, _T_OPROJ_IN, _T_DOWN_IN = 0, 1, 2, 3, 4
 _T_OPROJ_OUTLIER, _T_DOWN_OUTLIER = 5, 6
+_T_CLS = 7               # CLS-to-patch attention stand-in
 _T_WEIGHT0 = 16          # weights use tensor ids 16 + linear index
 _T_GEMV_IN = 32          # decode-step activations
 
@@ -168,6 +174,27 @@ def to_f32(a: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "fp16":
         return a.astype(np.float32)
     return (a.astype(np.uint32) << 16).view(np.float32)
+
+
+CLS_HEADS = 16
+CLS_LOGIT_STD = 3.0
+PATCHES_PER_TILE = 576
+
+
+def cls_attention(cfg_id: int, N: int, sample: int = 0) -> np.ndarray:
+    """[N] fp32 head-averaged CLS-to-patch attention weights of one image.
+
+    Input synthesis only: softmax over each tile's patches of seeded logits,
+    computed in float64 and rounded to fp32."""
+    g = _rng(cfg_id, _T_CLS, sample)
+    out = np.empty(N, dtype=np.float64)
+    for t0 in range(0, N, PATCHES_PER_TILE):
+        n = min(PATCHES_PER_TILE, N - t0)
+        z = g.standard_normal((CLS_HEADS, n)) * CLS_LOGIT_STD
+        z -= z.max(axis=1, keepdims=True)
+        e = np.exp(z)
+        out[t0:t0 + n] = (e / e.sum(axis=1, keepdims=True)).mean(axis=0)
+    return out.astype(np.float32)
 
 
 @dataclass
