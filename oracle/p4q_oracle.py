@@ -293,8 +293,11 @@ def diversity_greedy(cv: np.ndarray, kept: Sequence[int], k: int,
     when either code vector is all zero.  They are compared through the exact
     rational sgn(cos) cos^2.  With an empty retained set the first pick is the
     most salient token (the paper leaves this case open)."""
-    cv64 = cv.astype(np.int64)
-    G = cv64 @ cv64.T                      # exact: every entry < 2^53
+    # Gram matrix of the codes as a float64 matmul: every product is an
+    # integer of magnitude <= 64 and every partial sum an integer of magnitude
+    # <= 64 d < 2^53, so the result is exact whatever the summation order
+    cvf = cv.astype(np.float64)
+    G = (cvf @ cvf.T).astype(np.int64)
     Nv = np.diag(G)
     S = [int(i) for i in kept]
     in_s = set(S)
