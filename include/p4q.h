@@ -101,6 +101,50 @@ int p4q_select(p4q_dtype dt, int B, int N, int d,
                void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * The three-stage quantization-aware selector (Sec. 3.2, Eq.
+ * p4q_progressive_selection: Query Relevance, Visual Saliency, Visual
+ * Diversity, with budgets kq + ks + kd = K).
+ *
+ * For each sample b < B, with the fake-quantized codes cv_i, cq_j of
+ * p4q_select:
+ *   1. Query Relevance keeps kq tokens, exactly as p4q_select with K = kq;
+ *   2. Visual Saliency keeps, among the tokens not kept by stage 1, the ks
+ *      with the largest cls_attn[b][i] (the vision tower's last-layer
+ *      CLS-to-patch attention averaged over heads; equal weights: lower
+ *      index first);
+ *   3. Visual Diversity runs kd = K - kq - ks greedy steps; each keeps the
+ *      remaining token whose largest cosine similarity to the tokens kept so
+ *      far is smallest (equal values: lower index first), with
+ *      cos(i, t) = <cv_i, cv_t> / sqrt(Nv_i Nv_t) (0 when either code vector
+ *      is zero), compared exactly.  If stages 1-2 keep nothing, the first
+ *      step keeps the most salient token (largest cls_attn, lower index
+ *      first).
+ *   idx_out[b][0..K) = all kept tokens, ascending; tokens_out as p4q_select.
+ *   stages_out (may be NULL), int32 [B, K]: stage 1's tokens ascending, then
+ *   stage 2's ascending, then stage 3's in the order they were kept.
+ *
+ * Layouts: as p4q_select; cls_attn fp32 [B, N], finite values.
+ * Workspace: at least p4q_select_full_workspace_bytes(B, N, d, J, K) bytes,
+ *   256-byte aligned; it holds the B code Gram matrices (B * N^2 int32).  Its
+ *   first B*N*(J+1) int32 hold D and Nv as for p4q_select.
+ * Limits: as p4q_select, plus d <= 8192 and 0 <= kq, 0 <= ks, kq + ks <= K;
+ *   cls_attn 4-byte aligned, stages_out 4-byte aligned when given.
+ * ---------------------------------------------------------------------- */
+size_t p4q_select_full_workspace_bytes(int B, int N, int d, int J, int K);
+
+/* The default budget split of Sec. 3.2 (alpha, beta, gamma) = (0.3, 0.2,
+ * 0.5): kq = floor(3K/10), ks = floor(2K/10), kd = K - kq - ks.  Host-only;
+ * P4Q_ERR_INVALID_ARG for K < 0 or a NULL output. */
+int p4q_select_budgets(int K, int *kq, int *ks, int *kd);
+
+int p4q_select_full(p4q_dtype dt, int B, int N, int d,
+                    const void *vis, const void *concepts, int J,
+                    const float *cls_attn, const void *text, int T,
+                    int K, int kq, int ks, float clip,
+                    int32_t *idx_out, int32_t *stages_out, void *tokens_out,
+                    void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Per-row activation quantization + packing (Appendix A / B.3: per-token
  * int4 activations; the same call quantizes weight rows per output channel).
  *

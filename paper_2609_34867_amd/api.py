@@ -79,6 +79,69 @@ def select(vis: torch.Tensor, concepts: torch.Tensor, text: Optional[torch.Tenso
     return idx_out, tokens_out
 
 
+def select_budgets(K: int) -> Tuple[int, int, int]:
+    """The default (Query Relevance, Visual Saliency, Visual Diversity) token
+    budgets for K kept tokens (p4q_select_budgets)."""
+    kq, ks, kd = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    check(lib().p4q_select_budgets(K, ctypes.byref(kq), ctypes.byref(ks), ctypes.byref(kd)))
+    return kq.value, ks.value, kd.value
+
+
+def select_full_workspace(B: int, N: int, d: int, J: int, K: int, device) -> torch.Tensor:
+    """Workspace for select_full() (holds the B N x N code Gram matrices)."""
+    n = lib().p4q_select_full_workspace_bytes(B, N, d, J, K)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def select_full(vis: torch.Tensor, concepts: torch.Tensor, cls_attn: torch.Tensor,
+                text: Optional[torch.Tensor], K: int, kq: Optional[int] = None,
+                ks: Optional[int] = None, clip: float = 1.0,
+                idx_out: Optional[torch.Tensor] = None,
+                stages_out: Optional[torch.Tensor] = None,
+                tokens_out: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None, return_stages: bool = False):
+    """The three-stage selector (p4q_select_full): kq tokens by Query Relevance,
+    ks by Visual Saliency (cls_attn fp32 [B, N]) over the rest, K - kq - ks by
+    Visual Diversity.  kq / ks default to the paper's split of K.
+
+    Returns (idx int32 [B, K] ascending, tokens [B, K+T, d]) and, when
+    return_stages, also stages int32 [B, K] (query picks ascending, saliency
+    picks ascending, diversity picks in pick order)."""
+    _need_gpu(vis, concepts, cls_attn, text)
+    B, N, d = vis.shape
+    J = concepts.shape[1]
+    T = 0 if text is None else text.shape[1]
+    if concepts.shape != (B, J, d) or (text is not None and text.shape != (B, T, d)):
+        raise ValueError("shape mismatch between vis, concepts and text")
+    if cls_attn.shape != (B, N) or cls_attn.dtype != torch.float32 or not cls_attn.is_contiguous():
+        raise ValueError("cls_attn must be contiguous fp32 [B, N]")
+    for t in (vis, concepts, text):
+        if t is not None and (t.dtype != vis.dtype or not t.is_contiguous()):
+            raise ValueError("vis/concepts/text must be contiguous and share a dtype")
+    if kq is None or ks is None:
+        dq, ds, _ = select_budgets(K)
+        kq = dq if kq is None else kq
+        ks = ds if ks is None else ks
+    dev = vis.device
+    if idx_out is None:
+        idx_out = torch.empty((B, K), dtype=torch.int32, device=dev)
+    if stages_out is None and return_stages:
+        stages_out = torch.empty((B, K), dtype=torch.int32, device=dev)
+    if tokens_out is None:
+        tokens_out = torch.empty((B, K + T, d), dtype=vis.dtype, device=dev)
+    if workspace is None:
+        workspace = select_full_workspace(B, N, d, J, K, dev)
+    st = lib().p4q_select_full(_dtype_code(vis.dtype), B, N, d, _ptr(vis), _ptr(concepts), J,
+                               _ptr(cls_attn), _ptr(text) if T > 0 else None, T, K, kq, ks,
+                               ctypes.c_float(clip), _ptr(idx_out), _ptr(stages_out),
+                               _ptr(tokens_out), _ptr(workspace),
+                               workspace.numel() * workspace.element_size(), _stream(dev))
+    check(st)
+    if return_stages:
+        return idx_out, tokens_out, stages_out
+    return idx_out, tokens_out
+
+
 # --------------------------------------------------------------------------- quantizer
 def quant_act(x: torch.Tensor, clip: float = 1.0, codes: Optional[torch.Tensor] = None,
               scales: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:

@@ -92,6 +92,55 @@ int p4q_select(p4q_dtype dt, int B, int N, int d, const void *vis, const void *c
                       "p4q_select");
 }
 
+size_t p4q_select_full_workspace_bytes(int B, int N, int d, int J, int K) {
+    if (B <= 0 || N <= 0 || d <= 0 || J <= 0 || K <= 0) return 0;
+    return p4q::select_full_workspace_bytes(B, N, d, J, K);
+}
+
+int p4q_select_budgets(int K, int *kq, int *ks, int *kd) {
+    if (K < 0 || !kq || !ks || !kd) return fail(P4Q_ERR_INVALID_ARG, "p4q_select_budgets: K=%d or null output", K);
+    *kq = (int)((int64_t)K * 3 / 10);
+    *ks = (int)((int64_t)K * 2 / 10);
+    *kd = K - *kq - *ks;
+    return ok();
+}
+
+int p4q_select_full(p4q_dtype dt, int B, int N, int d, const void *vis, const void *concepts, int J,
+                    const float *cls_attn, const void *text, int T, int K, int kq, int ks, float clip,
+                    int32_t *idx_out, int32_t *stages_out, void *tokens_out, void *ws, size_t ws_bytes,
+                    hipStream_t stream) {
+    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select_full: dtype %d", (int)dt);
+    if (B <= 0 || N <= 0 || d <= 0 || J <= 0 || K <= 0 || T < 0)
+        return fail(P4Q_ERR_INVALID_ARG,
+                    "p4q_select_full: sizes must be positive (B=%d N=%d d=%d J=%d K=%d T=%d)", B, N, d, J, K, T);
+    if (K > N) return fail(P4Q_ERR_INVALID_ARG, "p4q_select_full: K=%d > N=%d", K, N);
+    if (kq < 0 || ks < 0 || (int64_t)kq + ks > K)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select_full: budgets kq=%d ks=%d do not fit K=%d", kq, ks, K);
+    if (!vis || !concepts || !cls_attn || !idx_out || !tokens_out)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select_full: null pointer");
+    if ((T > 0) != (text != nullptr))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select_full: text must be given iff T > 0");
+    if (!valid_clip(clip))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select_full: clip %g outside [2^-16, 1]", clip);
+    if (d % 32 != 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_select_full: d=%d not a multiple of 32", d);
+    if (!aligned(vis, 16) || !aligned(concepts, 16) || !aligned(tokens_out, 16) ||
+        (text && !aligned(text, 16)) || !aligned(idx_out, 4) || !aligned(cls_attn, 4) ||
+        (stages_out && !aligned(stages_out, 4)))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_select_full: misaligned pointer");
+    if (N > 8192) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select_full: N=%d > 8192", N);
+    if (J > 8) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select_full: J=%d > 8", J);
+    if (d > 8192) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select_full: d=%d > 8192", d);
+    if (B > 65535) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select_full: B=%d > 65535", B);
+    const size_t need = p4q::select_full_workspace_bytes(B, N, d, J, K);
+    if (!ws || ws_bytes < need)
+        return fail(P4Q_ERR_WORKSPACE, "p4q_select_full: workspace %zu < %zu bytes", ws_bytes, need);
+    if (!aligned(ws, 256)) return fail(P4Q_ERR_INVALID_ARG, "p4q_select_full: workspace not 256-byte aligned");
+    const p4q::SelectFullWorkspace w = p4q::select_full_workspace_carve(ws, B, N, d, J, K);
+    return hip_status(p4q::launch_select_full(dt, B, N, d, vis, concepts, J, cls_attn, text, T, K, kq, ks,
+                                              clip, idx_out, stages_out, tokens_out, w, stream),
+                      "p4q_select_full");
+}
+
 int p4q_quant_act(p4q_dtype dt, int M, int K_in, const void *x, int64_t ldx, float clip,
                   uint8_t *codes, float *scales, hipStream_t stream) {
     if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_quant_act: dtype %d", (int)dt);

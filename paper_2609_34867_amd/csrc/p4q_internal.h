@@ -20,7 +20,19 @@ struct SelectWorkspace {
     int32_t *stats;      // [B][N][J+1]: D_0..D_{J-1}, Nv   (documented)
     int64_t *keys;       // [B][J][N]: exact order keys (internal)
     int8_t *ccodes;      // [B][J][d]: concept codes (internal)
+    uint32_t *vcodes = nullptr;   // [B][N][d/8] packed visual codes, or none
 };
+
+// the three-stage selector's workspace: the above, then
+struct SelectFullWorkspace {
+    SelectWorkspace sel;    // vcodes set
+    int32_t *gram;          // [B][N][N] code Gram matrices (exact int32)
+    int64_t *mp;            // [B][N] diversity state: max over the kept set,
+    int32_t *mq;            //        as the pair (p, q) (see diversity.hip)
+    int32_t *stages;        // [B][K] stage picks when the caller gives none
+};
+size_t select_full_workspace_bytes(int B, int N, int d, int J, int K);
+SelectFullWorkspace select_full_workspace_carve(void *ws, int B, int N, int d, int J, int K);
 size_t select_workspace_bytes(int B, int N, int d, int J);
 SelectWorkspace select_workspace_carve(void *ws, int B, int N, int d, int J);
 
@@ -29,7 +41,24 @@ hipError_t launch_select(p4q_dtype dt, int B, int N, int d, const void *vis,
                          float clip, int32_t *idx_out, void *tokens_out,
                          const SelectWorkspace &ws, hipStream_t stream);
 
+hipError_t launch_select_full(p4q_dtype dt, int B, int N, int d, const void *vis,
+                              const void *concepts, int J, const float *cls_attn,
+                              const void *text, int T, int K, int kq, int ks, float clip,
+                              int32_t *idx_out, int32_t *stages_out, void *tokens_out,
+                              const SelectFullWorkspace &ws, hipStream_t stream);
+
+// Visual Diversity completion (diversity.hip): n0 = kq + ks tokens already
+// in stages[b][0, n0); kd greedy picks appended there in pick order;
+// idx_out[b][0, K) = all K kept tokens, ascending.
+hipError_t launch_diversity(int B, int N, int K, int n0, int kd, const int32_t *gram,
+                            const float *cls_attn, int64_t *mp, int32_t *mq, int32_t *stages,
+                            int32_t *idx_out, hipStream_t stream);
+
 // ---- W4A4 GEMM ---------------------------------------------------------------
+// G_b = C_b C_b^T for b < B, C_b = codes + b * n * (k/2) packed [n, k/2];
+// G int32 [B][n][n].
+hipError_t launch_code_gram(int B, int n, int k, const uint8_t *codes, int32_t *G,
+                            hipStream_t stream);
 size_t gemm_workspace_bytes(int M, int N, int K);
 hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *sa,
                             const uint8_t *w, const float *sw, p4q_dtype out_dt, void *y,

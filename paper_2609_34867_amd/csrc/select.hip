@@ -18,6 +18,7 @@
 
 #include <algorithm>
 #include "q4_device.h"
+#include "wave_ops.h"
 
 namespace p4q {
 namespace {
@@ -132,7 +133,8 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
                                                       int J, float clip, int LS, int rpw,
                                                       const int8_t *__restrict__ ccodes,
                                                       int32_t *__restrict__ stats,
-                                                      int64_t *__restrict__ keys) {
+                                                      int64_t *__restrict__ keys,
+                                                      uint32_t *__restrict__ vcodes) {
     extern __shared__ uint2 s_cc[];          // [JMAX][64*CH] uint2, zero-padded
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63;
@@ -199,6 +201,14 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
         uint2 cv[CH];                                        // int8 codes, 8 per chunk
 #pragma unroll
         for (int c = 0; c < CH; ++c) cv[c] = make_uint2(0, 0);
+        // packed int4 copy of the codes, when asked for (the Gram matrix of
+        // the diversity stage is computed from it)
+        uint32_t *vrow = vcodes ? vcodes + ((int64_t)b * N + row0 + r) * (d / 8) : nullptr;
+        if (s == 0.0f && vrow) {
+#pragma unroll
+            for (int c = 0; c < CH; ++c)
+                if (lane + 64 * c < nchunk) vrow[lane + 64 * c] = 0u;
+        }
         if (s != 0.0f) {
             const bool tiny = !(s >= kTinyScale);
             const float rc = tiny ? 0.0f : 1.0f / s;
@@ -222,6 +232,7 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
                     q4_chunk_exact<BF16>(vc, s, w);
                     cv[c] = make_uint2(bytes4(w[0], w[1], w[2], w[3]), bytes4(w[4], w[5], w[6], w[7]));
                 }
+                if (vrow && lane + 64 * c < nchunk) vrow[lane + 64 * c] = pack_nibbles(w);
             }
         }
 
@@ -267,31 +278,6 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
         if (JMAX == 8 && vslot == 0) st[J] = nv_r;
     }
     }
-}
-
-// Inclusive prefix sum over the 64 lanes of a wavefront with DPP row shifts
-// and row broadcasts (no LDS round trips).
-__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t v) {
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, true);  // row_shr:1
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, true);  // row_shr:2
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, true);  // row_shr:4
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, true);  // row_shr:8
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false); // row_bcast:15
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false); // row_bcast:31
-    return v;
-}
-
-// sum of wtot[0 .. wave) read as four 16-byte words
-__device__ __forceinline__ uint32_t waves_before(const uint32_t *wtot, int wave) {
-    const uint4 *w4 = reinterpret_cast<const uint4 *>(wtot);
-    uint32_t s = 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const uint4 v = w4[q];
-        s += (4 * q + 0 < wave ? v.x : 0u) + (4 * q + 1 < wave ? v.y : 0u) +
-             (4 * q + 2 < wave ? v.z : 0u) + (4 * q + 3 < wave ? v.w : 0u);
-    }
-    return s;
 }
 
 // ---------------------------------------------------------------------------
@@ -348,10 +334,24 @@ __device__ __forceinline__ uint32_t comp_digit(const Composite &x, int lo, int w
     return (uint32_t)v & mask;
 }
 
-template <int E>
-__global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__restrict__ keys,
+// Order-preserving integer key of an fp32 value (finite inputs): larger
+// values give larger keys, -0 and +0 the same key.
+__device__ __forceinline__ int64_t f32_order_key(float a) {
+    const uint32_t u = __float_as_uint(a);
+    return (u >> 31) ? -(int64_t)(u & 0x7FFFFFFFu) : (int64_t)u;
+}
+
+// FKEYS: `keys` holds one fp32 score per token ([B][N], J == 1) instead of
+// exact int64 keys ([B][J][N]).  Tokens listed in pre[b * pre_stride + 0 ..
+// npre) are kept beforehand: they are never candidates and are not written.
+// idx_out[b * out_stride + 0 .. K) = the K newly kept tokens, ascending.
+template <int E, bool FKEYS>
+__global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restrict__ keys_,
                                                             int N, int J, int K,
-                                                            int32_t *__restrict__ idx_out) {
+                                                            const int32_t *__restrict__ pre,
+                                                            int npre, int pre_stride,
+                                                            int32_t *__restrict__ idx_out,
+                                                            int out_stride) {
     __shared__ __attribute__((aligned(16))) uint32_t hist[kBins];
     __shared__ __attribute__((aligned(16))) uint32_t wtot[kTkThreads / 64];
     __shared__ uint32_t sh_bucket, sh_gt, sh_eq;
@@ -364,17 +364,40 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__res
     for (int q = t; q < kBins; q += kTkThreads) hist[q] = 0;
     if (t == 0) { sh_hmin = ~0ull; sh_hmax = 0; sh_lmin = ~0u; sh_lmax = 0; }
     __syncthreads();
-    uint32_t kept = 0;
+    // tokens kept beforehand: bitmap in the (still unused) histogram
+    uint32_t prekept = 0;
+    if (npre > 0) {                                          // block-uniform
+        const int32_t *pb = pre + (int64_t)b * pre_stride;
+        for (int q = t; q < npre; q += kTkThreads) {
+            const int i = pb[q];
+            if ((unsigned)i < (unsigned)N) atomicOr(&hist[i >> 5], 1u << (i & 31));
+        }
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int i = t * E + e;
+            if (i < N && ((hist[i >> 5] >> (i & 31)) & 1u)) prekept |= 1u << e;
+        }
+        __syncthreads();
+        for (int q = t; q < (N + 31) / 32; q += kTkThreads) hist[q] = 0;
+        __syncthreads();
+    }
+    uint32_t kept = prekept;
 
     // thread t owns tokens t*E .. t*E+E-1; keys of the next concept are loaded
     // while the current one is selected
     int64_t kn[E];
     auto load_keys = [&](int j) {
-        const int64_t *kj = keys + ((int64_t)b * J + j) * N;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const int i = t * E + e;
-            kn[e] = (i < N) ? kj[i] : 0;
+            if constexpr (FKEYS) {
+                const float *kf = static_cast<const float *>(keys_) + (int64_t)b * N;
+                kn[e] = (i < N) ? f32_order_key(kf[i]) : 0;
+            } else {
+                const int64_t *kj = static_cast<const int64_t *>(keys_) + ((int64_t)b * J + j) * N;
+                kn[e] = (i < N) ? kj[i] : 0;
+            }
         }
     };
     // prefetch of the next concept's keys only while registers allow it
@@ -468,14 +491,15 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const int64_t *__res
         }
     }
 
-    // ordered compaction of the kept set
+    // ordered compaction of the newly kept set
+    kept &= ~prekept;
     const uint32_t cnt = __builtin_popcount(kept);
     const uint32_t inc = wave_inclusive_scan(cnt);
     __syncthreads();
     if (lane == 63) wtot[wave] = inc;
     __syncthreads();
     uint32_t opos = inc - cnt + waves_before(wtot, wave);
-    int32_t *out = idx_out + (int64_t)b * K;
+    int32_t *out = idx_out + (int64_t)b * out_stride;
 #pragma unroll
     for (int e = 0; e < E; ++e)
         if (((kept >> e) & 1u) && opos < (uint32_t)K) out[opos++] = t * E + e;
@@ -542,7 +566,7 @@ hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const vo
     const dim3 grid((N + 4 * rpw - 1) / (4 * rpw), B);
     hipLaunchKernelGGL((k_select_score<CH, JMAX, BF16, CLIP1>), grid, dim3(256), lds, stream,
                        static_cast<const uint8_t *>(vis), N, d, J, clip, LS, rpw, ws.ccodes, ws.stats,
-                       ws.keys);
+                       ws.keys, ws.vcodes);
     return hipGetLastError();
 }
 
@@ -582,6 +606,44 @@ hipError_t launch_concepts(int rows, int d, float clip, const void *con, int8_t 
     return hipGetLastError();
 }
 
+template <bool FKEYS>
+hipError_t launch_topk(int B, int N, int J, int K, const void *keys, const int32_t *pre, int npre,
+                       int pre_stride, int32_t *idx_out, int out_stride, hipStream_t stream) {
+    switch ((N + kTkThreads - 1) / kTkThreads) {    // tokens per thread, N <= 8192
+#define P4Q_TK(E)                                                                                  \
+    case E:                                                                                       \
+        hipLaunchKernelGGL((k_select_topk<E, FKEYS>), dim3(B), dim3(kTkThreads), 0, stream, keys, N, \
+                           J, K, pre, npre, pre_stride, idx_out, out_stride);                     \
+        break;
+        P4Q_TK(1) P4Q_TK(2) P4Q_TK(3) P4Q_TK(4) P4Q_TK(5) P4Q_TK(6) P4Q_TK(7) P4Q_TK(8)
+#undef P4Q_TK
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <bool BF16, bool CLIP1>
+hipError_t launch_codes_and_scores(int B, int N, int d, int J, float clip, const void *vis,
+                                   const void *concepts, const SelectWorkspace &ws,
+                                   hipStream_t stream) {
+    // 2^LS >= (64 d)^2: LS = 2 * ceil(log2(64 d))
+    int lg = 0;
+    while ((1ll << lg) < 64ll * d) ++lg;
+    const int LS = 2 * lg;
+    hipError_t e = launch_concepts<BF16, CLIP1>(B * J, d, clip, concepts, ws.ccodes, stream);
+    if (e != hipSuccess) return e;
+    return launch_score_typed<BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+}
+
+hipError_t launch_gather(int B, int N, int d, const void *vis, const void *text, int T, int K,
+                         const int32_t *idx, void *tokens_out, hipStream_t stream) {
+    const int64_t rows = (int64_t)B * (K + T);
+    hipLaunchKernelGGL(k_select_gather, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream,
+                       static_cast<const uint4 *>(vis), static_cast<const uint4 *>(text), idx,
+                       B, N, K, T, d / 8, static_cast<uint4 *>(tokens_out));
+    return hipGetLastError();
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
@@ -607,37 +669,70 @@ hipError_t launch_select(p4q_dtype dt, int B, int N, int d, const void *vis, con
                          void *tokens_out, const SelectWorkspace &ws, hipStream_t stream) {
     const bool bf16 = (dt == P4Q_BF16);
     const bool clip1 = (clip == 1.0f);
-    // 2^LS >= (64 d)^2: LS = 2 * ceil(log2(64 d))
-    int lg = 0;
-    while ((1ll << lg) < 64ll * d) ++lg;
-    const int LS = 2 * lg;
     hipError_t e;
-    if (bf16) e = clip1 ? launch_concepts<true, true>(B * J, d, clip, concepts, ws.ccodes, stream)
-                        : launch_concepts<true, false>(B * J, d, clip, concepts, ws.ccodes, stream);
-    else e = clip1 ? launch_concepts<false, true>(B * J, d, clip, concepts, ws.ccodes, stream)
-                   : launch_concepts<false, false>(B * J, d, clip, concepts, ws.ccodes, stream);
+    if (bf16) e = clip1 ? launch_codes_and_scores<true, true>(B, N, d, J, clip, vis, concepts, ws, stream)
+                        : launch_codes_and_scores<true, false>(B, N, d, J, clip, vis, concepts, ws, stream);
+    else e = clip1 ? launch_codes_and_scores<false, true>(B, N, d, J, clip, vis, concepts, ws, stream)
+                   : launch_codes_and_scores<false, false>(B, N, d, J, clip, vis, concepts, ws, stream);
     if (e != hipSuccess) return e;
-    if (bf16) e = clip1 ? launch_score_typed<true, true>(B, N, d, J, clip, LS, vis, ws, stream)
-                        : launch_score_typed<true, false>(B, N, d, J, clip, LS, vis, ws, stream);
-    else e = clip1 ? launch_score_typed<false, true>(B, N, d, J, clip, LS, vis, ws, stream)
-                   : launch_score_typed<false, false>(B, N, d, J, clip, LS, vis, ws, stream);
+    if ((e = launch_topk<false>(B, N, J, K, ws.keys, nullptr, 0, 0, idx_out, K, stream)) != hipSuccess)
+        return e;
+    return launch_gather(B, N, d, vis, text, T, K, idx_out, tokens_out, stream);
+}
+
+size_t select_full_workspace_bytes(int B, int N, int d, int J, int K) {
+    return select_workspace_bytes(B, N, d, J) + align256((size_t)B * N * (d / 2)) +
+           align256((size_t)B * N * N * 4) + align256((size_t)B * N * 8) +
+           align256((size_t)B * N * 4) + align256((size_t)B * K * 4);
+}
+
+SelectFullWorkspace select_full_workspace_carve(void *ws, int B, int N, int d, int J, int K) {
+    SelectFullWorkspace w;
+    w.sel = select_workspace_carve(ws, B, N, d, J);
+    uint8_t *p = static_cast<uint8_t *>(ws) + select_workspace_bytes(B, N, d, J);
+    w.sel.vcodes = reinterpret_cast<uint32_t *>(p);
+    p += align256((size_t)B * N * (d / 2));
+    w.gram = reinterpret_cast<int32_t *>(p);
+    p += align256((size_t)B * N * N * 4);
+    w.mp = reinterpret_cast<int64_t *>(p);
+    p += align256((size_t)B * N * 8);
+    w.mq = reinterpret_cast<int32_t *>(p);
+    p += align256((size_t)B * N * 4);
+    w.stages = reinterpret_cast<int32_t *>(p);
+    return w;
+}
+
+hipError_t launch_select_full(p4q_dtype dt, int B, int N, int d, const void *vis,
+                              const void *concepts, int J, const float *cls_attn,
+                              const void *text, int T, int K, int kq, int ks, float clip,
+                              int32_t *idx_out, int32_t *stages_out, void *tokens_out,
+                              const SelectFullWorkspace &ws, hipStream_t stream) {
+    const bool bf16 = (dt == P4Q_BF16);
+    const bool clip1 = (clip == 1.0f);
+    const int kd = K - kq - ks;
+    int32_t *stages = stages_out ? stages_out : ws.stages;
+    hipError_t e;
+    // codes of the fake-quantized copies (packed, for the Gram matrix) and the
+    // exact Query-Relevance keys, in one pass over the features
+    if (bf16) e = clip1 ? launch_codes_and_scores<true, true>(B, N, d, J, clip, vis, concepts, ws.sel, stream)
+                        : launch_codes_and_scores<true, false>(B, N, d, J, clip, vis, concepts, ws.sel, stream);
+    else e = clip1 ? launch_codes_and_scores<false, true>(B, N, d, J, clip, vis, concepts, ws.sel, stream)
+                   : launch_codes_and_scores<false, false>(B, N, d, J, clip, vis, concepts, ws.sel, stream);
     if (e != hipSuccess) return e;
-    switch ((N + kTkThreads - 1) / kTkThreads) {    // tokens per thread, N <= 8192
-#define P4Q_TK(E)                                                                            \
-    case E:                                                                                 \
-        hipLaunchKernelGGL(k_select_topk<E>, dim3(B), dim3(kTkThreads), 0, stream, ws.keys, N, \
-                           J, K, idx_out);                                                  \
-        break;
-        P4Q_TK(1) P4Q_TK(2) P4Q_TK(3) P4Q_TK(4) P4Q_TK(5) P4Q_TK(6) P4Q_TK(7) P4Q_TK(8)
-#undef P4Q_TK
-        default: return hipErrorInvalidValue;
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t rows = (int64_t)B * (K + T);
-    hipLaunchKernelGGL(k_select_gather, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream,
-                       static_cast<const uint4 *>(vis), static_cast<const uint4 *>(text), idx_out,
-                       B, N, K, T, d / 8, static_cast<uint4 *>(tokens_out));
-    return hipGetLastError();
+    // Query Relevance: kq tokens -> stages[b][0, kq)
+    if (kq > 0 && (e = launch_topk<false>(B, N, J, kq, ws.sel.keys, nullptr, 0, 0, stages, K, stream)) != hipSuccess)
+        return e;
+    // Visual Saliency over the tokens left: ks tokens -> stages[b][kq, kq + ks)
+    if (ks > 0 && (e = launch_topk<true>(B, N, 1, ks, cls_attn, stages, kq, K, stages + kq, K, stream)) != hipSuccess)
+        return e;
+    // Visual Diversity: kd greedy picks -> stages[b][kq + ks, K); idx_out = all K, ascending
+    if (kd > 0 && (e = launch_code_gram(B, N, d, reinterpret_cast<const uint8_t *>(ws.sel.vcodes), ws.gram,
+                                        stream)) != hipSuccess)
+        return e;
+    if ((e = launch_diversity(B, N, K, kq + ks, kd, ws.gram, cls_attn, ws.mp, ws.mq, stages, idx_out,
+                              stream)) != hipSuccess)
+        return e;
+    return launch_gather(B, N, d, vis, text, T, K, idx_out, tokens_out, stream);
 }
 
 }  // namespace p4q

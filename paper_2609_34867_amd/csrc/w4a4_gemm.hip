@@ -138,7 +138,8 @@ __global__ __launch_bounds__(kThreads) void k_w4a4_gemm(const uint8_t *__restric
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
         const int n = n0 + wn * 64 + g * 16 + (lane & 15);
-        const float swn = (n < N) ? sw[n] : 0.0f;
+        // y == nullptr: accumulators only (Gram matrices), no scales read
+        const float swn = (y && n < N) ? sw[n] : 0.0f;
 #pragma unroll
         for (int f = 0; f < 4; ++f) {
 #pragma unroll
@@ -146,8 +147,10 @@ __global__ __launch_bounds__(kThreads) void k_w4a4_gemm(const uint8_t *__restric
                 const int m = m0 + wm * 64 + f * 16 + 4 * (lane >> 4) + e;
                 if (m < M && n < N) {
                     const int v = acc[f][g][e] >> 8;
-                    const float t1 = __fmul_rn((float)v, sa[m]);
-                    store_out<BF16OUT>(y, (int64_t)m * ldy + n, __fmul_rn(t1, swn));
+                    if (y) {
+                        const float t1 = __fmul_rn((float)v, sa[m]);
+                        store_out<BF16OUT>(y, (int64_t)m * ldy + n, __fmul_rn(t1, swn));
+                    }
                     if (acc_out) acc_out[(int64_t)m * N + n] = v;
                 }
             }
@@ -236,7 +239,10 @@ __device__ __forceinline__ v4i unpack2(uint32_t w0, uint32_t w1) {
     return v4i{(int)nib_lo(w0), (int)nib_hi(w0), (int)nib_lo(w1), (int)nib_hi(w1)};
 }
 
-template <bool BF16OUT, bool ACC>
+// YOUT = false is the Gram mode: only the int32 accumulators are stored
+// (acc_out, row stride N), no scales are read and no y is written; blockIdx.y
+// selects one problem of a batch (A, W, acc_out advanced by their strides).
+template <bool BF16OUT, bool ACC, bool YOUT>
 __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restrict__ A,
                                                           const float *__restrict__ sa,
                                                           const uint8_t *__restrict__ W,
@@ -244,9 +250,14 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
                                                           int N, int Kb, void *__restrict__ y,
                                                           int64_t ldy,
                                                           int32_t *__restrict__ acc_out,
-                                                          int tiles_m, int tiles_n) {
+                                                          int tiles_m, int tiles_n,
+                                                          int64_t a_bstride, int64_t w_bstride,
+                                                          int64_t acc_bstride) {
     __shared__ __attribute__((aligned(1024))) uint8_t smem[L_STAGES * L_STAGE + 1536];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    A += blockIdx.y * a_bstride;
+    W += blockIdx.y * w_bstride;
+    if constexpr (ACC) acc_out += blockIdx.y * acc_bstride;
     const int wm = wave >> 1, wn = wave & 1;
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
@@ -290,7 +301,7 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         }
     };
 
-    {   // the block's scales -> LDS (zeros past M / N), ahead of the stages
+    if constexpr (YOUT) {   // the block's scales -> LDS (zeros past M / N), ahead of the stages
         const v4i dSa = buffer_desc(sa + m0, (uint32_t)(min(M - m0, L_BM) * 4));
         const v4i dSw = buffer_desc(sw + n0, (uint32_t)(min(N - n0, L_BN) * 4));
         const uint32_t sbase = lds_addr(smem) + L_SCALE_OFF;
@@ -360,6 +371,31 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         mfma_step(u1);
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(0);
+    }
+
+    if constexpr (!YOUT) {      // Gram mode: int32 accumulators only
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int nb = n0 + wn * 64 + 16 * i + 4 * cq;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int m = m0 + wm * 128 + 16 * j + r16;
+                if (m < M) {
+                    int v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e] >> 8;
+                    int32_t *dst = acc_out + (int64_t)m * N + nb;
+                    if (nb + 3 < N && (N & 3) == 0) {
+                        *reinterpret_cast<int4 *>(dst) = make_int4(v[0], v[1], v[2], v[3]);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (nb + e < N) dst[e] = v[e];
+                    }
+                }
+            }
+        }
+        return;
     }
 
     // Epilogue.  acc[i][j] lane l, register e holds
@@ -614,11 +650,12 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
         const dim3 grid(tiles_m * tiles_n);
         auto go = [&](auto kern) {
             hipLaunchKernelGGL(kern, grid, dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy,
-                               acc_out, tiles_m, tiles_n);
+                               acc_out, tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0);
             return hipGetLastError();
         };
-        if (bf16) return acc_out ? go(k_w4a4_gemm_2cu<true, true>) : go(k_w4a4_gemm_2cu<true, false>);
-        return acc_out ? go(k_w4a4_gemm_2cu<false, true>) : go(k_w4a4_gemm_2cu<false, false>);
+        if (bf16)
+            return acc_out ? go(k_w4a4_gemm_2cu<true, true, true>) : go(k_w4a4_gemm_2cu<true, false, true>);
+        return acc_out ? go(k_w4a4_gemm_2cu<false, true, true>) : go(k_w4a4_gemm_2cu<false, false, true>);
     }
     const dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
     if (bf16)
@@ -628,6 +665,29 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
         hipLaunchKernelGGL(k_w4a4_gemm<false>, grid, dim3(kThreads), 0, stream, a, sa, w, sw, M,
                            N, K / 2, y, ldy, acc_out);
     return hipGetLastError();
+}
+
+// Gram matrices of a batch of packed code blocks: G_b = C_b C_b^T (int32,
+// [n, n] each, row-major), C_b = codes + b * n * (k/2).  Exact integer sums.
+hipError_t launch_code_gram(int B, int n, int k, const uint8_t *codes, int32_t *G,
+                            hipStream_t stream) {
+    const int kb = k / 2;
+    if (n >= 1024) {
+        const int tiles_m = (n + L_BM - 1) / L_BM, tiles_n = (n + L_BN - 1) / L_BN;
+        hipLaunchKernelGGL((k_w4a4_gemm_2cu<true, true, false>), dim3(tiles_m * tiles_n, B), dim3(256), 0,
+                           stream, codes, nullptr, codes, nullptr, n, n, kb, nullptr, (int64_t)n, G,
+                           tiles_m, tiles_n, (int64_t)n * kb, (int64_t)n * kb, (int64_t)n * n);
+        return hipGetLastError();
+    }
+    const dim3 grid((n + BN - 1) / BN, (n + BM - 1) / BM);
+    for (int b = 0; b < B; ++b) {
+        const uint8_t *cb = codes + (int64_t)b * n * kb;
+        hipLaunchKernelGGL(k_w4a4_gemm<true>, grid, dim3(kThreads), 0, stream, cb, nullptr, cb, nullptr, n,
+                           n, kb, nullptr, (int64_t)n, G + (int64_t)b * n * n);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace p4q

@@ -102,6 +102,58 @@ def test_select_workspace_size_covers_documented_stats():
     assert L.lib().p4q_select_workspace_bytes(0, 1, 1, 1) == 0
 
 
+def select_full(**kw):
+    a = dict(dt=0, B=1, N=64, d=64, vis=ALIGNED, con=ALIGNED, J=2, cls=ALIGNED, text=ALIGNED,
+             T=4, K=10, kq=3, ks=2, clip=1.0, idx=ALIGNED, stages=None, tok=ALIGNED,
+             ws=ALIGNED, ws_bytes=1 << 30)
+    a.update(kw)
+    return L.lib().p4q_select_full(a["dt"], a["B"], a["N"], a["d"], a["vis"], a["con"], a["J"],
+                                   a["cls"], a["text"], a["T"], a["K"], a["kq"], a["ks"],
+                                   F(a["clip"]), a["idx"], a["stages"], a["tok"], a["ws"],
+                                   a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(K=65), L.P4Q_ERR_INVALID_ARG),
+    (dict(kq=-1), L.P4Q_ERR_INVALID_ARG),
+    (dict(ks=-1), L.P4Q_ERR_INVALID_ARG),
+    (dict(kq=6, ks=5), L.P4Q_ERR_INVALID_ARG),
+    (dict(cls=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(cls=ALIGNED + 2), L.P4Q_ERR_INVALID_ARG),
+    (dict(stages=ALIGNED + 1), L.P4Q_ERR_INVALID_ARG),
+    (dict(d=8224), L.P4Q_ERR_UNSUPPORTED),
+    (dict(N=9000), L.P4Q_ERR_UNSUPPORTED),
+    (dict(J=9), L.P4Q_ERR_UNSUPPORTED),
+    (dict(ws_bytes=1000), L.P4Q_ERR_WORKSPACE),
+    (dict(ws=ALIGNED + 64), L.P4Q_ERR_INVALID_ARG),
+    (dict(text=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(dt=3), L.P4Q_ERR_UNSUPPORTED),
+])
+def test_select_full_validation(kw, status):
+    assert select_full(**kw) == status
+    assert L.lib().p4q_last_error() != b""
+
+
+def test_select_full_workspace_holds_gram_matrices():
+    n = L.lib().p4q_select_full_workspace_bytes(16, 2880, 4096, 4, 640)
+    assert n >= 16 * 2880 * 2880 * 4 + L.lib().p4q_select_workspace_bytes(16, 2880, 4096, 4)
+    assert L.lib().p4q_select_full_workspace_bytes(1, 1, 32, 1, 0) == 0
+
+
+def test_select_budgets_match_the_oracle():
+    import ctypes
+    import oracle
+    for K in (0, 1, 2, 64, 192, 320, 640, 2879):
+        kq, ks, kd = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+        assert L.lib().p4q_select_budgets(K, ctypes.byref(kq), ctypes.byref(ks),
+                                          ctypes.byref(kd)) == L.P4Q_OK
+        assert (kq.value, ks.value, kd.value) == oracle.stage_budgets(K)
+    assert L.lib().p4q_select_budgets(-1, ctypes.byref(kq), ctypes.byref(ks),
+                                      ctypes.byref(kd)) == L.P4Q_ERR_INVALID_ARG
+    assert L.lib().p4q_select_budgets(5, None, ctypes.byref(ks),
+                                      ctypes.byref(kd)) == L.P4Q_ERR_INVALID_ARG
+
+
 def linear(**kw):
     a = dict(M=4, N=8, K=64, a=ALIGNED, sa=ALIGNED, w=ALIGNED, sw=ALIGNED, dt=1, y=ALIGNED,
              ldy=8, acc=None, ws=None, ws_bytes=0)
