@@ -16,23 +16,21 @@
 // candidate, (p', q') > (p, q) <=> p' q > p q': with d <= 8192, |p| <= 2^38 and
 // q <= 2^19, so both products are exact in int64.
 //
-// Across candidates the step compares a 64-bit key: the fp64 quotient
-// p / (Nv_i q) (exact operands, correctly rounded, hence monotone in the exact
-// value), mapped to order-preserving bits, its low 13 bits replaced by the
-// token index.  When the two smallest keys differ above the index bits, the
-// smallest key's token is the exact minimum; otherwise (ties and near-ties,
-// rare) the candidates sharing that truncated value are compared exactly with
-// 128-bit cross products.
+// Across candidates the step compares fp32 approximations of the values
+// (each within a few ulps of the exact rational); when the two smallest lie
+// within a small ulp window, every candidate in that window is compared
+// exactly with 128-bit cross products, so the pick is always the exact
+// minimum (equal values: lower index).
 #include "p4q_internal.h"
 
 #include "wave_ops.h"
+
+#include <algorithm>
 
 namespace p4q {
 namespace {
 
 constexpr int64_t kNoneP = -(1LL << 40);      // below every cosine: "S empty"
-constexpr int kDvThreads = 1024;
-constexpr int kDvWaves = kDvThreads / 64;
 constexpr uint64_t kIdxMask = 0x1FFFull;      // 13 index bits (N <= 8192)
 constexpr uint64_t kNoKey = ~0ull;
 
@@ -46,13 +44,6 @@ __device__ __forceinline__ void cos_pair(int32_t D, int32_t nvt, int64_t &p, int
 // (p1, q1) above (p0, q0) for one candidate
 __device__ __forceinline__ bool pair_gt(int64_t p1, int32_t q1, int64_t p0, int32_t q0) {
     return p1 * (int64_t)q0 > p0 * (int64_t)q1;
-}
-
-__device__ __forceinline__ uint64_t cand_key(int64_t p, int32_t q, int32_t nvi, int i) {
-    const double v = (p == 0) ? 0.0 : (double)p / ((double)nvi * (double)q);
-    const uint64_t u = (uint64_t)__double_as_longlong(v);
-    const uint64_t o = (u >> 63) ? ~u : (u | 0x8000000000000000ull);
-    return (o & ~kIdxMask) | (uint64_t)i;
 }
 
 // exact p_a / den_a < p_b / den_b (den > 0), by 128-bit cross products
@@ -83,17 +74,20 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
 
 // ---------------------------------------------------------------------------
 // Initial state: for every token i, the maximum over the n0 tokens already
-// kept of the pair of cos(i, t).  Grid (ceil(N / 256), B).
+// kept of the pair of cos(i, t).  Grid (ceil(N / 256), B, C): block z takes
+// the kept tokens [z n0 / C, (z + 1) n0 / C) and writes its partial maximum
+// to plane z of mp / mq ([C][B][N]); the greedy kernel merges the planes.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_div_init(const int32_t *__restrict__ G, int N,
                                                   const int32_t *__restrict__ stages, int K, int n0,
                                                   int64_t *__restrict__ mp, int32_t *__restrict__ mq) {
-    extern __shared__ int32_t s_list[];            // [n0] tokens, then [n0] Nv
-    int32_t *s_nv = s_list + n0;
-    const int b = blockIdx.y;
+    extern __shared__ int32_t s_list[];            // [cnt] tokens, then [cnt] Nv
+    const int b = blockIdx.y, z = blockIdx.z, C = gridDim.z;
+    const int q0 = (int)((int64_t)z * n0 / C), cnt = (int)((int64_t)(z + 1) * n0 / C) - q0;
+    int32_t *s_nv = s_list + cnt;
     const int32_t *Gb = G + (int64_t)b * N * N;
-    for (int q = threadIdx.x; q < n0; q += 256) {
-        int tk = stages[(int64_t)b * K + q];
+    for (int q = threadIdx.x; q < cnt; q += 256) {
+        int tk = stages[(int64_t)b * K + q0 + q];
         if ((unsigned)tk >= (unsigned)N) tk = 0;   // never taken: the stages hold valid tokens
         s_list[q] = tk;
         s_nv[q] = Gb[(int64_t)tk * N + tk];
@@ -104,14 +98,14 @@ __global__ __launch_bounds__(256) void k_div_init(const int32_t *__restrict__ G,
     int64_t p = kNoneP;
     int32_t q = 1;
     constexpr int U = 16;                          // loads in flight per thread
-    for (int u0 = 0; u0 < n0; u0 += U) {
+    for (int u0 = 0; u0 < cnt; u0 += U) {
         int32_t D[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            D[u] = (u0 + u < n0) ? Gb[(int64_t)s_list[u0 + u] * N + i] : 0;
+            D[u] = (u0 + u < cnt) ? Gb[(int64_t)s_list[u0 + u] * N + i] : 0;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (u0 + u < n0) {
+            if (u0 + u < cnt) {
                 int64_t pp;
                 int32_t qq;
                 cos_pair(D[u], s_nv[u0 + u], pp, qq);
@@ -119,38 +113,103 @@ __global__ __launch_bounds__(256) void k_div_init(const int32_t *__restrict__ G,
             }
         }
     }
-    mp[(int64_t)b * N + i] = p;
-    mq[(int64_t)b * N + i] = q;
+    const int64_t o = ((int64_t)z * gridDim.y + b) * N + i;
+    mp[o] = p;
+    mq[o] = q;
 }
 
 // ---------------------------------------------------------------------------
-// The greedy scan: one 1024-thread work-group per sample.  Thread t owns
-// candidates i = e * 1024 + t (e < E), so each row of G is read with
-// coalesced loads.  Per step: local (smallest, second smallest) key, a
-// wavefront reduction, one LDS exchange between the 16 wavefronts (each
-// wavefront then reduces the 16 partials itself, so one barrier per step),
-// the exact tie-break when needed, and the update from the new token's row.
+// Cross-lane pieces of the greedy step: DPP moves inside rows of 16 lanes,
+// readlane across the 4 rows.
 // ---------------------------------------------------------------------------
-template <int E>
-__global__ __launch_bounds__(kDvThreads) void k_div_greedy(const int32_t *__restrict__ G, int N,
-                                                           const int64_t *__restrict__ mp,
-                                                           const int32_t *__restrict__ mq,
-                                                           const float *__restrict__ cls, int K, int n0,
-                                                           int kd, int32_t *__restrict__ stages,
-                                                           int32_t *__restrict__ idx_out) {
-    __shared__ uint32_t bm[256];                                   // kept bitmap (N <= 8192)
-    __shared__ unsigned long long r1[2][kDvWaves], r2[2][kDvWaves];
-    __shared__ long long xp[kDvWaves];
-    __shared__ unsigned long long xd[kDvWaves];
-    __shared__ int xi[kDvWaves];
-    __shared__ __attribute__((aligned(16))) uint32_t wtot[kDvWaves];
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+    const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)v, CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(v >> 32), CTRL, 0xF, 0xF, false);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
 
-    const int b = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+template <int CTRL>
+__device__ __forceinline__ void merge_dpp(uint64_t &k1, uint64_t &k2) {
+    const uint64_t o1 = dpp64<CTRL>(k1), o2 = dpp64<CTRL>(k2);
+    merge2(k1, k2, o1, o2);
+}
+
+// (smallest, second smallest) of each row of 16 lanes, in every lane of it
+__device__ __forceinline__ void row_min2(uint64_t &k1, uint64_t &k2) {
+    merge_dpp<0xB1>(k1, k2);     // quad_perm [1,0,3,2]: lane ^ 1
+    merge_dpp<0x4E>(k1, k2);     // quad_perm [2,3,0,1]: lane ^ 2
+    merge_dpp<0x141>(k1, k2);    // row_half_mirror: the other quad of the 8
+    merge_dpp<0x140>(k1, k2);    // row_mirror: the other 8 of the row
+}
+
+// ... of the whole wavefront, wave-uniform
+__device__ __forceinline__ void wave_min2(uint64_t &k1, uint64_t &k2) {
+    row_min2(k1, k2);
+    uint64_t a1 = readlane64(k1, 0), a2 = readlane64(k2, 0);
+#pragma unroll
+    for (int r = 1; r < 4; ++r) merge2(a1, a2, readlane64(k1, 16 * r), readlane64(k2, 16 * r));
+    k1 = a1;
+    k2 = a2;
+}
+
+// order-preserving bits of an fp32 value (-0 below +0)
+__device__ __forceinline__ uint32_t ord32(float v) {
+    const uint32_t u = __float_as_uint(v);
+    return (u >> 31) ? ~u : (u | 0x80000000u);
+}
+
+// Candidates whose approximate values lie within this many fp32 ulps of each
+// other are compared exactly (the approximations err by at most ~10 ulps).
+constexpr uint32_t kUlpTol = 32;
+
+// ---------------------------------------------------------------------------
+// The greedy scan: one NT-thread work-group per sample; thread t owns
+// candidates i = e * NT + t (e < E), so a row of G is read with coalesced
+// loads.  Per candidate the exact pair (p, q) is kept with vf ~ p / (Nv_i q)
+// in fp32 (relative error <= 5 * 2^-24: three roundings and two correctly
+// rounded reciprocals).  A step:
+//   1. key = (ord32(vf) << 32) | i; the block's smallest two keys (DPP
+//      inside wavefronts, one LDS exchange, one barrier);
+//   2. if the two smallest values are more than kUlpTol ulps apart, the
+//      smallest key's token is the exact minimum; otherwise every candidate
+//      within kUlpTol ulps of the smallest is compared exactly (128-bit
+//      cross products; equal values: lower index);
+//   3. the new token's row D = G[best][.] updates each candidate from
+//      c = D |D| / (Nv_i Nv_best) in fp32: clearly below vf -> unchanged,
+//      clearly above -> replaced, within kUlpTol ulps -> exact comparison of
+//      the pairs.
+// ---------------------------------------------------------------------------
+template <int E, int NT>
+__global__ __launch_bounds__(NT) void k_div_greedy(const int32_t *__restrict__ G, int N,
+                                                   const int64_t *__restrict__ mp,
+                                                   const int32_t *__restrict__ mq,
+                                                   const float *__restrict__ cls, int K, int n0,
+                                                   int kd, int nplanes, int32_t *__restrict__ stages,
+                                                   int32_t *__restrict__ idx_out) {
+    constexpr int NW = NT / 64;
+    static_assert(NT >= 256 && NT <= 1024 && NT % 64 == 0, "one bitmap word per thread");
+    __shared__ uint32_t bm[256];                                   // kept bitmap (N <= 8192)
+    __shared__ unsigned long long r1[2][NW], r2[2][NW];
+    __shared__ long long xp[NW];
+    __shared__ unsigned long long xd[NW];
+    __shared__ int xi[NW];
+    __shared__ __attribute__((aligned(16))) uint32_t wtot[16];
+    __shared__ int32_t nvs[8192];                                  // Nv of the candidates
+
+    const int b = blockIdx.x, t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
     const int32_t *Gb = G + (int64_t)b * N * N;
     int32_t *st = stages + (int64_t)b * K;
-    for (int q = t; q < 256; q += kDvThreads) bm[q] = 0;
+    for (int q = t; q < 256; q += NT) bm[q] = 0;
     __syncthreads();
-    for (int q = t; q < n0; q += kDvThreads) {
+    for (int q = t; q < n0; q += NT) {
         const int tk = st[q];
         if ((unsigned)tk < (unsigned)N) atomicOr(&bm[tk >> 5], 1u << (tk & 31));
     }
@@ -158,60 +217,62 @@ __global__ __launch_bounds__(kDvThreads) void k_div_greedy(const int32_t *__rest
 
     int64_t p[E];
     int32_t q[E], nv[E];
-    uint64_t key[E];
+    float vf[E], inv[E];
     uint32_t live = 0;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const int i = e * kDvThreads + t;
+        const int i = e * NT + t;
         p[e] = kNoneP;
         q[e] = 1;
         nv[e] = 0;
-        key[e] = kNoKey;
+        inv[e] = 0.0f;
+        vf[e] = -__builtin_huge_valf();
         if (kd > 0 && i < N && !((bm[i >> 5] >> (i & 31)) & 1u)) {
             live |= 1u << e;
             nv[e] = Gb[(int64_t)i * N + i];
+            nvs[i] = nv[e];
+            inv[e] = nv[e] > 0 ? 1.0f / (float)nv[e] : 0.0f;
             if (n0 > 0) {
-                p[e] = mp[(int64_t)b * N + i];
-                q[e] = mq[(int64_t)b * N + i];
-                key[e] = cand_key(p[e], q[e], nv[e], i);
+                for (int z = 0; z < nplanes; ++z) {
+                    const int64_t o = ((int64_t)z * gridDim.x + b) * N + i;
+                    const int64_t pz = mp[o];
+                    const int32_t qz = mq[o];
+                    if (pair_gt(pz, qz, p[e], q[e])) { p[e] = pz; q[e] = qz; }
+                }
+                vf[e] = p[e] == 0 ? 0.0f : ((float)p[e] * inv[e]) * (1.0f / (float)q[e]);
             }
         }
     }
 
-    // block-wide (smallest, second smallest) of per-thread pairs; `par`
-    // alternates the LDS slots between consecutive steps
+    // block-wide smallest two of the per-thread pairs; `par` alternates the
+    // LDS slots between consecutive steps (one barrier per step)
     auto block_min2 = [&](uint64_t k1, uint64_t k2, int par, uint64_t &o1, uint64_t &o2) {
-#pragma unroll
-        for (int m = 1; m < 64; m <<= 1) merge2(k1, k2, shfl_xor_u64(k1, m), shfl_xor_u64(k2, m));
+        wave_min2(k1, k2);
         if (lane == 0) { r1[par][wave] = k1; r2[par][wave] = k2; }
         __syncthreads();
-        uint64_t a1 = lane < kDvWaves ? r1[par][lane] : kNoKey;
-        uint64_t a2 = lane < kDvWaves ? r2[par][lane] : kNoKey;
-#pragma unroll
-        for (int m = 1; m < kDvWaves; m <<= 1) merge2(a1, a2, shfl_xor_u64(a1, m), shfl_xor_u64(a2, m));
-        o1 = (uint64_t)__shfl((unsigned long long)a1, 0);
-        o2 = (uint64_t)__shfl((unsigned long long)a2, 0);
+        uint64_t a1 = lane < NW ? r1[par][lane] : kNoKey;
+        uint64_t a2 = lane < NW ? r2[par][lane] : kNoKey;
+        row_min2(a1, a2);
+        o1 = readlane64(a1, 0);
+        o2 = readlane64(a2, 0);
     };
 
-    // exact minimum among the candidates whose key shares the value bits `tv`
-    auto exact_min = [&](uint64_t tv) -> int {
+    // exact minimum among the candidates whose ord32 value is <= vmax
+    auto exact_min = [&](uint32_t vmax) -> int {
         int64_t bp = 0;
         uint64_t bd = 1;
         int bi = 0x7FFFFFFF;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            if (((live >> e) & 1u) && (key[e] & ~kIdxMask) == tv) {
-                const int i = e * kDvThreads + t;
-                const uint64_t den = p[e] == 0 ? 1ull : (uint64_t)nv[e] * (uint64_t)q[e];
-                if (bi == 0x7FFFFFFF || val_lt(p[e], den, bp, bd)) { bp = p[e]; bd = den; bi = i; }
-            }
-        }
         auto take = [&](int64_t op, uint64_t od, int oi) {
             if (oi == 0x7FFFFFFF) return;
             if (bi == 0x7FFFFFFF || val_lt(op, od, bp, bd) || (!val_lt(bp, bd, op, od) && oi < bi)) {
                 bp = op; bd = od; bi = oi;
             }
         };
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            if (((live >> e) & 1u) && ord32(vf[e]) <= vmax)
+                take(p[e], p[e] == 0 ? 1ull : (uint64_t)nv[e] * (uint64_t)q[e], e * NT + t);
+        }
 #pragma unroll
         for (int m = 1; m < 64; m <<= 1) {
             const int64_t op = (int64_t)__shfl_xor((long long)bp, m);
@@ -221,10 +282,10 @@ __global__ __launch_bounds__(kDvThreads) void k_div_greedy(const int32_t *__rest
         }
         if (lane == 0) { xp[wave] = bp; xd[wave] = bd; xi[wave] = bi; }
         __syncthreads();
-        if (lane < kDvWaves) { bp = xp[lane]; bd = xd[lane]; bi = xi[lane]; }
+        if (lane < NW) { bp = xp[lane]; bd = xd[lane]; bi = xi[lane]; }
         else { bp = 0; bd = 1; bi = 0x7FFFFFFF; }
 #pragma unroll
-        for (int m = 1; m < kDvWaves; m <<= 1) {
+        for (int m = 1; m < NW; m <<= 1) {
             const int64_t op = (int64_t)__shfl_xor((long long)bp, m);
             const uint64_t od = (uint64_t)__shfl_xor((unsigned long long)bd, m);
             const int oi = __shfl_xor(bi, m);
@@ -234,31 +295,62 @@ __global__ __launch_bounds__(kDvThreads) void k_div_greedy(const int32_t *__rest
     };
 
     // keep token `best`; update the candidates from its row of G unless it
-    // was the last pick
+    // was the last pick.  The row of `next` (the runner-up, almost always the
+    // next pick: a new token rarely raises the runner-up's maximum) is loaded
+    // ahead into Dn, so the next step usually finds its row in registers.
+    const __amdgpu_buffer_rsrc_t gres =
+        __builtin_amdgcn_make_buffer_rsrc((void *)Gb, 0, (int)(N * N * 4), 0x00020000);
+    uint32_t coff[E];                     // byte offsets of this thread's columns
+#pragma unroll
+    for (int e = 0; e < E; ++e) coff[e] = (e * NT + t < N) ? (uint32_t)(e * NT + t) * 4u : 0x80000000u;
+    auto load_row = [&](int r, int32_t *dst) {
+        const uint32_t rb = (uint32_t)r * (uint32_t)N * 4u;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            dst[e] = __builtin_amdgcn_raw_buffer_load_b32(gres, coff[e] == 0x80000000u ? coff[e] : rb + coff[e], 0, 0);
+    };
     int picks = 0;
-    auto keep = [&](int best) {
+    int pre = -1;
+    int32_t Dn[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) Dn[e] = 0;
+    __syncthreads();                                               // nvs complete
+    auto keep = [&](int best, int next) {
         if (t == 0) {
             st[n0 + picks] = best;
             bm[best >> 5] |= 1u << (best & 31);
         }
-        if ((best & (kDvThreads - 1)) == t) live &= ~(1u << (best / kDvThreads));
+        if ((best % NT) == t) live &= ~(1u << (best / NT));
         ++picks;
         if (picks == kd) return;
-        const int32_t *row = Gb + (int64_t)best * N;
+        // Row loads are unconditional buffer loads (offsets past the row read
+        // as 0), so the compiler's wait before the update only covers the
+        // older loads and leaves the prefetch in flight.
         int32_t D[E];
+        if (best == pre) {
 #pragma unroll
-        for (int e = 0; e < E; ++e) D[e] = ((live >> e) & 1u) ? row[e * kDvThreads + t] : 0;
-        const int32_t nvb = row[best];
+            for (int e = 0; e < E; ++e) D[e] = Dn[e];
+        } else {
+            load_row(best, D);
+        }
+        pre = next;
+        load_row(next >= 0 ? next : best, Dn);
+        const int32_t nvb = nvs[best];
+        const float invb = nvb > 0 ? 1.0f / (float)nvb : 0.0f;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             if ((live >> e) & 1u) {
+                const float df = (float)D[e];
+                const float cf = ((df * __builtin_fabsf(df)) * inv[e]) * invb;
+                const int64_t oc = ord32(cf), ov = ord32(vf[e]);
+                if (oc + (int64_t)kUlpTol < ov) continue;          // clearly not above
                 int64_t pp;
                 int32_t qq;
                 cos_pair(D[e], nvb, pp, qq);
-                if (pair_gt(pp, qq, p[e], q[e]) || key[e] == kNoKey) {
+                if (oc > ov + (int64_t)kUlpTol || pair_gt(pp, qq, p[e], q[e])) {
                     p[e] = pp;
                     q[e] = qq;
-                    key[e] = cand_key(pp, qq, nv[e], e * kDvThreads + t);
+                    vf[e] = cf;
                 }
             }
         }
@@ -271,34 +363,37 @@ __global__ __launch_bounds__(kDvThreads) void k_div_greedy(const int32_t *__rest
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             if ((live >> e) & 1u) {
-                const int i = e * kDvThreads + t;
+                const int i = e * NT + t;
                 uint32_t u = __float_as_uint(cls[(int64_t)b * N + i]);
                 if (u == 0x80000000u) u = 0;                                 // -0 ranks as +0
-                const uint32_t o = (u >> 31) ? ~u : (u | 0x80000000u);   // larger weight -> larger o
-                const uint64_t k = ((uint64_t)(~o) << 13) | (uint64_t)i;
-                merge2(k1, k2, k, kNoKey);
+                const uint32_t o = (u >> 31) ? ~u : (u | 0x80000000u);       // larger weight -> larger o
+                merge2(k1, k2, ((uint64_t)(~o) << 32) | (uint64_t)i, kNoKey);
             }
         }
         uint64_t o1, o2;
         block_min2(k1, k2, par, o1, o2);
         par ^= 1;
-        if (o1 != kNoKey) keep((int)(o1 & kIdxMask));
+        if (o1 != kNoKey) keep((int)(o1 & kIdxMask), -1);
     }
     while (picks < kd) {
         uint64_t k1 = kNoKey, k2 = kNoKey;
 #pragma unroll
         for (int e = 0; e < E; ++e)
-            if ((live >> e) & 1u) merge2(k1, k2, key[e], kNoKey);
+            if ((live >> e) & 1u) merge2(k1, k2, ((uint64_t)ord32(vf[e]) << 32) | (uint64_t)(e * NT + t), kNoKey);
         uint64_t o1, o2;
         block_min2(k1, k2, par, o1, o2);
         par ^= 1;
         if (o1 == kNoKey) break;             // no candidate left (not reached for kd <= N - n0)
         int best = (int)(o1 & kIdxMask);
-        if (o2 != kNoKey && (o1 & ~kIdxMask) == (o2 & ~kIdxMask)) best = exact_min(o1 & ~kIdxMask);
-        keep(best);
+        const uint32_t v1 = (uint32_t)(o1 >> 32);
+        if (o2 != kNoKey && (uint32_t)(o2 >> 32) - v1 <= kUlpTol) best = exact_min(v1 + kUlpTol);
+        int next = o2 != kNoKey ? (int)(o2 & kIdxMask) : -1;
+        if (next == best) next = (int)(o1 & kIdxMask);
+        keep(best, next);
     }
 
-    // idx_out[b] = the kept set in ascending order
+    // idx_out[b] = the kept set in ascending order (one bitmap word per
+    // thread: N <= 8192 = 32 * 256 <= 32 * NT)
     __syncthreads();
     const int nwords = (N + 31) / 32;
     uint32_t w = 0;
@@ -325,22 +420,35 @@ __global__ __launch_bounds__(kDvThreads) void k_div_greedy(const int32_t *__rest
 hipError_t launch_diversity(int B, int N, int K, int n0, int kd, const int32_t *gram,
                             const float *cls_attn, int64_t *mp, int32_t *mq, int32_t *stages,
                             int32_t *idx_out, hipStream_t stream) {
+    // planes of the initial maxima: about 40 kept tokens per block
+    const int planes = n0 > 0 ? std::min(kDivInitPlanes, (n0 + 39) / 40) : 0;
     if (kd > 0 && n0 > 0) {
-        hipLaunchKernelGGL(k_div_init, dim3((N + 255) / 256, B), dim3(256), (size_t)n0 * 8, stream,
+        const int per = (n0 + planes - 1) / planes;
+        hipLaunchKernelGGL(k_div_init, dim3((N + 255) / 256, B, planes), dim3(256), (size_t)per * 8, stream,
                            gram, N, stages, K, n0, mp, mq);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    switch ((N + kDvThreads - 1) / kDvThreads) {      // candidates per thread, N <= 8192
-#define P4Q_DV(E)                                                                                 \
-    case E:                                                                                      \
-        hipLaunchKernelGGL(k_div_greedy<E>, dim3(B), dim3(kDvThreads), 0, stream, gram, N, mp, mq, \
-                           cls_attn, K, n0, kd, stages, idx_out);                                \
-        break;
-        P4Q_DV(1) P4Q_DV(2) P4Q_DV(3) P4Q_DV(4) P4Q_DV(5) P4Q_DV(6) P4Q_DV(7) P4Q_DV(8)
-#undef P4Q_DV
+    // 512 threads while every thread holds at most 8 candidates, else 1024
+#define P4Q_DV(E, NT)                                                                              \
+    hipLaunchKernelGGL((k_div_greedy<E, NT>), dim3(B), dim3(NT), 0, stream, gram, N, mp, mq, cls_attn, K, \
+                       n0, kd, planes, stages, idx_out)
+    switch ((N + 511) / 512) {
+        case 1: P4Q_DV(1, 512); break;
+        case 2: P4Q_DV(2, 512); break;
+        case 3: P4Q_DV(3, 512); break;
+        case 4: P4Q_DV(4, 512); break;
+        case 5: P4Q_DV(5, 512); break;
+        case 6: P4Q_DV(6, 512); break;
+        case 7: P4Q_DV(7, 512); break;
+        case 8: P4Q_DV(8, 512); break;
+        case 9: case 10: P4Q_DV(5, 1024); break;
+        case 11: case 12: P4Q_DV(6, 1024); break;
+        case 13: case 14: P4Q_DV(7, 1024); break;
+        case 15: case 16: P4Q_DV(8, 1024); break;
         default: return hipErrorInvalidValue;
     }
+#undef P4Q_DV
     return hipGetLastError();
 }
 

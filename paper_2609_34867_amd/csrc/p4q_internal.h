@@ -27,8 +27,8 @@ struct SelectWorkspace {
 struct SelectFullWorkspace {
     SelectWorkspace sel;    // vcodes set
     int32_t *gram;          // [B][N][N] code Gram matrices (exact int32)
-    int64_t *mp;            // [B][N] diversity state: max over the kept set,
-    int32_t *mq;            //        as the pair (p, q) (see diversity.hip)
+    int64_t *mp;            // [kDivInitPlanes][B][N] partial maxima over the kept
+    int32_t *mq;            //        set, as pairs (p, q) (see diversity.hip)
     int32_t *stages;        // [B][K] stage picks when the caller gives none
 };
 size_t select_full_workspace_bytes(int B, int N, int d, int J, int K);
@@ -46,6 +46,8 @@ hipError_t launch_select_full(p4q_dtype dt, int B, int N, int d, const void *vis
                               const void *text, int T, int K, int kq, int ks, float clip,
                               int32_t *idx_out, int32_t *stages_out, void *tokens_out,
                               const SelectFullWorkspace &ws, hipStream_t stream);
+
+constexpr int kDivInitPlanes = 8;
 
 // Visual Diversity completion (diversity.hip): n0 = kq + ks tokens already
 // in stages[b][0, n0); kd greedy picks appended there in pick order;

@@ -682,8 +682,8 @@ hipError_t launch_select(p4q_dtype dt, int B, int N, int d, const void *vis, con
 
 size_t select_full_workspace_bytes(int B, int N, int d, int J, int K) {
     return select_workspace_bytes(B, N, d, J) + align256((size_t)B * N * (d / 2)) +
-           align256((size_t)B * N * N * 4) + align256((size_t)B * N * 8) +
-           align256((size_t)B * N * 4) + align256((size_t)B * K * 4);
+           align256((size_t)B * N * N * 4) + align256((size_t)kDivInitPlanes * B * N * 8) +
+           align256((size_t)kDivInitPlanes * B * N * 4) + align256((size_t)B * K * 4);
 }
 
 SelectFullWorkspace select_full_workspace_carve(void *ws, int B, int N, int d, int J, int K) {
@@ -695,9 +695,9 @@ SelectFullWorkspace select_full_workspace_carve(void *ws, int B, int N, int d, i
     w.gram = reinterpret_cast<int32_t *>(p);
     p += align256((size_t)B * N * N * 4);
     w.mp = reinterpret_cast<int64_t *>(p);
-    p += align256((size_t)B * N * 8);
+    p += align256((size_t)kDivInitPlanes * B * N * 8);
     w.mq = reinterpret_cast<int32_t *>(p);
-    p += align256((size_t)B * N * 4);
+    p += align256((size_t)kDivInitPlanes * B * N * 4);
     w.stages = reinterpret_cast<int32_t *>(p);
     return w;
 }

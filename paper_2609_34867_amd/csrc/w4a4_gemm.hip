@@ -15,6 +15,8 @@
 // shift by 8 recovers acc.
 #include "p4q_internal.h"
 
+#include <algorithm>
+
 namespace p4q {
 namespace {
 
@@ -235,13 +237,33 @@ __device__ __forceinline__ void tile_coords(int wg, int tiles_m, int tiles_n, in
     tn = in_g / gsize;
 }
 
+// Gram mode (M == N, A == W): only tiles holding an entry on or above the
+// diagonal, i.e. tn >= 2 tm for 256 x 128 tiles; row tm of tiles holds
+// tiles_n - 2 tm of them.  Same XCD-contiguous dealing as tile_coords.
+__device__ __forceinline__ void gram_tile_coords(int wg, int total, int tiles_n, int &tm, int &tn) {
+    const int q = total / kXcds, r = total % kXcds;
+    const int x = wg % kXcds, i = wg / kXcds;
+    int logical = (x < r) ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+    tm = 0;
+    while (true) {
+        const int c = max(0, tiles_n - 2 * tm);
+        if (logical < c) break;
+        logical -= c;
+        ++tm;
+    }
+    tn = 2 * tm + logical;
+}
+
 __device__ __forceinline__ v4i unpack2(uint32_t w0, uint32_t w1) {
     return v4i{(int)nib_lo(w0), (int)nib_hi(w0), (int)nib_lo(w1), (int)nib_hi(w1)};
 }
 
-// YOUT = false is the Gram mode: only the int32 accumulators are stored
-// (acc_out, row stride N), no scales are read and no y is written; blockIdx.y
-// selects one problem of a batch (A, W, acc_out advanced by their strides).
+// YOUT = false is the Gram mode (A == W, M == N): only the int32
+// accumulators are stored (acc_out, row stride N), no scales are read and no
+// y is written; only tiles reaching the diagonal or above run (tiles_m then
+// holds their count), each entry m < n is stored at [m][n] and at [n][m];
+// blockIdx.y selects one problem of a batch (A, W, acc_out advanced by their
+// strides).
 template <bool BF16OUT, bool ACC, bool YOUT>
 __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restrict__ A,
                                                           const float *__restrict__ sa,
@@ -260,7 +282,8 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
     if constexpr (ACC) acc_out += blockIdx.y * acc_bstride;
     const int wm = wave >> 1, wn = wave & 1;
     int tm, tn;
-    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    if constexpr (YOUT) tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    else gram_tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * L_BM, n0 = tn * L_BN;
     const int ktiles = (Kb + BKB - 1) / BKB;
 
@@ -392,6 +415,11 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
                         for (int e = 0; e < 4; ++e)
                             if (nb + e < N) dst[e] = v[e];
                     }
+                    // mirror of the strictly upper entries: 16 lanes write 64
+                    // contiguous bytes of row nb + e
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (m < nb + e && nb + e < N) acc_out[(int64_t)(nb + e) * N + m] = v[e];
                 }
             }
         }
@@ -674,9 +702,11 @@ hipError_t launch_code_gram(int B, int n, int k, const uint8_t *codes, int32_t *
     const int kb = k / 2;
     if (n >= 1024) {
         const int tiles_m = (n + L_BM - 1) / L_BM, tiles_n = (n + L_BN - 1) / L_BN;
-        hipLaunchKernelGGL((k_w4a4_gemm_2cu<true, true, false>), dim3(tiles_m * tiles_n, B), dim3(256), 0,
+        int upper = 0;                              // tiles with tn >= 2 tm
+        for (int tm = 0; tm < tiles_m; ++tm) upper += std::max(0, tiles_n - 2 * tm);
+        hipLaunchKernelGGL((k_w4a4_gemm_2cu<true, true, false>), dim3(upper, B), dim3(256), 0,
                            stream, codes, nullptr, codes, nullptr, n, n, kb, nullptr, (int64_t)n, G,
-                           tiles_m, tiles_n, (int64_t)n * kb, (int64_t)n * kb, (int64_t)n * n);
+                           upper, tiles_n, (int64_t)n * kb, (int64_t)n * kb, (int64_t)n * n);
         return hipGetLastError();
     }
     const dim3 grid((n + BN - 1) / BN, (n + BM - 1) / BM);
