@@ -15,7 +15,9 @@ steps read weights like successive decoder layers would (101 MB per layer at
 7B, i.e. not resident in the 256 MB MALL across the rotation).
 
 Prints ONE JSON line.  value = W4A4 linear ops of the step / step time (TOPS);
-the selector's token rate and the GEMM-only rate are reported beside it.
+the selector's token rate and the GEMM-only rate are reported beside it, and,
+outside the timed steps, the three-stage selector (selector_full) and the
+decode-step GEMV.
 """
 from __future__ import annotations
 
@@ -44,6 +46,8 @@ def parse():
     ap.add_argument("--config", default="next7b_b16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode GEMV measurement")
+    ap.add_argument("--no-select-full", action="store_true",
+                    help="skip the three-stage selector measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -266,6 +270,46 @@ def decode_gemv(dev, steps=20):
             "M": out}
 
 
+def selector_full(cfg, dev, reps=10):
+    """The three-stage selector (Query Relevance, Visual Saliency, Visual
+    Diversity at the paper's 0.3 / 0.2 / 0.5 split of K) on the same batch of
+    features, with the CLS-attention stand-in.  Its dominant kernels are the
+    code Gram matrix on the int8 MFMA path (2 B N^2 d ops counted for the
+    full matrix; the kernel computes the upper half and mirrors it) and the
+    sequential greedy scan (K - kq - ks dependent steps per sample)."""
+    import torch
+    import paper_2609_34867_amd as p4q
+    from workload import selector_inputs, cls_attention
+
+    si = selector_inputs(cfg)
+    t = lambda a: torch.from_numpy(a).to(dev)
+    vis, con, txt = t(si.vis), t(si.concepts), t(si.text)
+    cls = t(np.stack([cls_attention(cfg.cfg_id, cfg.N, b) for b in range(cfg.B)]))
+    kq, ks, kd = p4q.select_budgets(cfg.K)
+    idx = torch.empty((cfg.B, cfg.K), dtype=torch.int32, device=dev)
+    tok = torch.empty((cfg.B, cfg.K + cfg.T, cfg.d), dtype=vis.dtype, device=dev)
+    ws = p4q.select_full_workspace(cfg.B, cfg.N, cfg.d, cfg.J, cfg.K, dev)
+    run = lambda: p4q.select_full(vis, con, cls, txt, cfg.K, kq, ks, idx_out=idx, tokens_out=tok,
+                                  workspace=ws)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del ws
+    return {"workload": f"{cfg.name}: three-stage selection of K={cfg.K} (kq={kq}, ks={ks}, "
+                        f"kd={kd}) of N={cfg.N} tokens x d={cfg.d} for B={cfg.B} images + "
+                        f"T={cfg.T} text",
+            "ms": round(ms, 4), "tokens_per_s": round(cfg.B * cfg.N / (ms * 1e-3), 1),
+            "greedy_steps_per_sample": kd,
+            "gram_ops_full_matrix": 2 * cfg.B * cfg.N * cfg.N * cfg.d}
+
+
 def copy_calibration(dev, nbytes=1 << 30, reps=5):
     """A plain device-to-device copy of known size, run so that the HBM
     counters (FETCH_SIZE, WRITE_SIZE) can be scaled to bytes: the counter
@@ -366,6 +410,8 @@ def main():
         "breakdown_ms": {k: round(v, 4) for k, v in tot.items()},
         "lib": p4q.version(),
     }
+    if not args.no_select_full:
+        res["selector_full"] = selector_full(cfg, dev)
     if not args.no_decode:
         del st
         torch.cuda.empty_cache()
