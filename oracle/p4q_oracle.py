@@ -62,7 +62,10 @@ QDIV = np.float32(7.0)      # symmetric range divisor (2^(4-1) - 1)
 # storage helpers (dtype decoding / encoding)
 # --------------------------------------------------------------------------
 def as_f32(x: np.ndarray, dtype: str) -> np.ndarray:
-    """Decode fp16 (float16 array) or bf16 (uint16 bit patterns) exactly."""
+    """Decode fp16 (float16 array) or bf16 (uint16 bit patterns) exactly;
+    "fp32" passes float32 rows through."""
+    if dtype == "fp32":
+        return np.asarray(x, dtype=np.float32)
     if dtype == "fp16":
         return np.asarray(x, dtype=np.float16).astype(np.float32)
     if dtype == "bf16":
@@ -344,6 +347,40 @@ def select_full(vis: np.ndarray, concepts: np.ndarray, a_cls: np.ndarray,
     idx = np.array(sorted(q_picks + s_picks + d_picks), dtype=np.int32)
     tokens = np.concatenate([np.asarray(vis)[idx], np.asarray(text)], axis=0)
     return idx, tokens, (q_picks, s_picks, d_picks)
+
+
+# --------------------------------------------------------------------------
+# O5: the fused decoder prologue -- RMSNorm with its per-channel weight (the
+#     slot into which calibration's diagonal scales fold, Appendix B.3), then
+#     the per-token quantizer, without materializing the normalized row
+# --------------------------------------------------------------------------
+def rmsnorm_quant(x: np.ndarray, gamma: np.ndarray, eps: float = 1e-5,
+                  dtype: str = "fp16", clip: float = 1.0
+                  ) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-token Q4 of RMSNorm(x) * gamma.
+
+    RMSNorm(x)_k = x_k / rms(x) with rms(x) = sqrt(mean_k x_k^2 + eps).  A
+    positive factor per row does not change Q4's codes in exact arithmetic
+    and multiplies its scale, so the prologue quantizes the row
+    u = x * gamma (fp32; exact, since both factors are 16-bit floats) and
+    moves 1/rms(x) into the scale:
+        codes = Q4(u; clip).codes
+        scale = fl32(Q4(u; clip).scale * (1 / rms(x)))
+    with 1/rms(x) in float64 from the float64 sum of squares.
+
+    x [M, d] and gamma [d] in storage dtype.  Returns (packed codes uint8
+    [M, d/2], scales float32 [M])."""
+    xf = as_f32(x, dtype)
+    gf = as_f32(gamma, dtype)
+    u = (xf * gf[None, :]).astype(np.float32)
+    if not np.all(np.isfinite(u)):
+        raise ValueError("non-finite x * gamma")
+    codes, su = quantize_rows(u, "fp32", clip)
+    x64 = xf.astype(np.float64)
+    inv_rms = 1.0 / np.sqrt(np.sum(x64 * x64, axis=1) / x64.shape[1] + float(eps))
+    scales = (su.astype(np.float64) * inv_rms).astype(np.float32)
+    scales[su == 0] = 0.0
+    return pack_int4(codes), scales
 
 
 # --------------------------------------------------------------------------
