@@ -16,8 +16,8 @@ steps read weights like successive decoder layers would (101 MB per layer at
 
 Prints ONE JSON line.  value = W4A4 linear ops of the step / step time (TOPS);
 the selector's token rate and the GEMM-only rate are reported beside it, and,
-outside the timed steps, the three-stage selector (selector_full) and the
-decode-step GEMV.
+outside the timed steps, the fused RMSNorm + quantize prologue, the
+three-stage selector (selector_full) and the decode-step GEMV.
 """
 from __future__ import annotations
 
@@ -310,6 +310,43 @@ def selector_full(cfg, dev, reps=10):
             "gram_ops_full_matrix": 2 * cfg.B * cfg.N * cfg.N * cfg.d}
 
 
+def prologue(cfg, st, dev, reps=20):
+    """The fused decoder prologue (p4q_rmsnorm_quant: per-token int4 of
+    RMSNorm(X) * gamma) on the step's pruned sequence X [M, d], next to the
+    plain quantize-and-pack of X.  HBM-bound: algorithmic bytes = read X
+    (2 B/element) + gamma + codes (0.5 B/element) + scales; an unfused
+    RMSNorm would also write and re-read the normalized rows."""
+    import torch
+    import paper_2609_34867_amd as p4q
+    from workload import norm_weight
+
+    x = st["tok"].view(cfg.M, cfg.d)
+    g = torch.from_numpy(norm_weight(cfg)).to(dev)
+    codes, scales = st["xq"]
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    us = timed(lambda: p4q.rmsnorm_quant(x, g, 1e-5, codes=codes, scales=scales))
+    us_plain = timed(lambda: p4q.quant_act(x, codes=codes, scales=scales))
+    nbytes = cfg.M * cfg.d * 2 + cfg.d * 2 + cfg.M * cfg.d // 2 + 4 * cfg.M
+    return {"workload": f"per-token int4 of RMSNorm(X) * gamma, X = the pruned sequence "
+                        f"[M={cfg.M}, d={cfg.d}] fp16",
+            "us": round(us, 2), "gbs": round(nbytes / us / 1e3, 1),
+            "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
+            "us_plain_quant_act": round(us_plain, 2),
+            "unfused_extra_bytes": 2 * cfg.M * cfg.d * 2}
+
+
 def copy_calibration(dev, nbytes=1 << 30, reps=5):
     """A plain device-to-device copy of known size, run so that the HBM
     counters (FETCH_SIZE, WRITE_SIZE) can be scaled to bytes: the counter
@@ -410,6 +447,7 @@ def main():
         "breakdown_ms": {k: round(v, 4) for k, v in tot.items()},
         "lib": p4q.version(),
     }
+    res["prologue_rmsnorm_quant"] = prologue(cfg, st, dev)
     if not args.no_select_full:
         res["selector_full"] = selector_full(cfg, dev)
     if not args.no_decode:

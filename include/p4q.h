@@ -160,6 +160,30 @@ int p4q_quant_act(p4q_dtype dt, int M, int K_in, const void *x, int64_t ldx,
                   float clip, uint8_t *codes, float *scales, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Fused decoder prologue: per-token int4 quantization of RMSNorm(x) * gamma
+ * without materializing the normalized rows (Appendix A / B.3: per-token
+ * symmetric RTN activations; gamma is the RMSNorm weight, the per-channel
+ * slot into which calibration's diagonal scales fold before RTN).
+ *
+ *   u[m][k]   = x[m][k] * gamma[k]                 (fp32, exact)
+ *   codes[m]  = Q4(u[m]; clip).codes               (packed as above)
+ *   scales[m] = fl32(Q4(u[m]; clip).scale / rms(x[m])),
+ *   rms(x[m]) = sqrt(sum_k x[m][k]^2 / d + eps)     (fp32; summation order
+ *               unspecified, so scales agree with an exact rms to ~1e-6)
+ * Q4 is invariant under a positive factor per row, so these are the codes
+ * and scale of RMSNorm(x[m]) * gamma; scales[m] = 0 when u[m] is all zero.
+ *
+ * Layouts: x [M, ldx] (dtype dt, first d columns read), gamma [d] (dtype
+ *   dt), codes uint8 [M, d/2], scales fp32 [M].
+ * Limits: M >= 1, d % 32 == 0, 32 <= d <= 16384, ldx >= d, ldx % 8 == 0,
+ *   eps in [0, 1], clip in [2^-16, 1]; products x * gamma finite; x, gamma
+ *   and codes 16-byte aligned, scales 4-byte aligned.
+ * ---------------------------------------------------------------------- */
+int p4q_rmsnorm_quant(p4q_dtype dt, int M, int d, const void *x, int64_t ldx,
+                      const void *gamma, float eps, float clip,
+                      uint8_t *codes, float *scales, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * W4A4 linear (Appendix B.3: RTN int4 weights and activations for W4A4
  * inference): an integer GEMM on the codes and a dequant epilogue.
  *

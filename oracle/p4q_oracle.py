@@ -377,8 +377,9 @@ def rmsnorm_quant(x: np.ndarray, gamma: np.ndarray, eps: float = 1e-5,
         raise ValueError("non-finite x * gamma")
     codes, su = quantize_rows(u, "fp32", clip)
     x64 = xf.astype(np.float64)
-    inv_rms = 1.0 / np.sqrt(np.sum(x64 * x64, axis=1) / x64.shape[1] + float(eps))
-    scales = (su.astype(np.float64) * inv_rms).astype(np.float32)
+    with np.errstate(divide="ignore", invalid="ignore"):      # zero rows at eps = 0
+        inv_rms = 1.0 / np.sqrt(np.sum(x64 * x64, axis=1) / x64.shape[1] + float(eps))
+        scales = (su.astype(np.float64) * inv_rms).astype(np.float32)
     scales[su == 0] = 0.0
     return pack_int4(codes), scales
 

@@ -162,6 +162,29 @@ def quant_act(x: torch.Tensor, clip: float = 1.0, codes: Optional[torch.Tensor] 
     return codes, scales
 
 
+def rmsnorm_quant(x: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-5, clip: float = 1.0,
+                  codes: Optional[torch.Tensor] = None,
+                  scales: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Per-token int4 quantize + pack of RMSNorm(x) * gamma (p4q_rmsnorm_quant):
+    x [M, d] (row stride may exceed d), gamma [d] of x's dtype -> (codes uint8
+    [M, d/2], scales fp32 [M]); the normalized rows are never formed."""
+    _need_gpu(x, gamma)
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be 2-D with unit column stride")
+    M, d = x.shape
+    if gamma.shape != (d,) or gamma.dtype != x.dtype or not gamma.is_contiguous():
+        raise ValueError("gamma must be a contiguous [d] tensor of x's dtype")
+    if codes is None:
+        codes = torch.empty((M, d // 2), dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty((M,), dtype=torch.float32, device=x.device)
+    st = lib().p4q_rmsnorm_quant(_dtype_code(x.dtype), M, d, _ptr(x), x.stride(0), _ptr(gamma),
+                                 ctypes.c_float(eps), ctypes.c_float(clip), _ptr(codes),
+                                 _ptr(scales), _stream(x.device))
+    check(st)
+    return codes, scales
+
+
 # --------------------------------------------------------------------------- W4A4 linear
 def w4a4_linear_workspace(M: int, N_out: int, K_in: int, device) -> Optional[torch.Tensor]:
     n = lib().p4q_w4a4_linear_workspace_bytes(M, N_out, K_in)

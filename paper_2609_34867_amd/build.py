@@ -19,7 +19,8 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 BUILD_DIR = os.path.join(REPO, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "libp4q.so")
 
-SOURCES = ["p4q_api.hip", "quant_act.hip", "select.hip", "diversity.hip", "w4a4_gemm.hip"]
+SOURCES = ["p4q_api.hip", "quant_act.hip", "prologue.hip", "select.hip", "diversity.hip",
+           "w4a4_gemm.hip"]
 
 ARCH = "gfx950"
 HIPCC_FLAGS = [

@@ -157,6 +157,23 @@ int p4q_quant_act(p4q_dtype dt, int M, int K_in, const void *x, int64_t ldx, flo
                       "p4q_quant_act");
 }
 
+int p4q_rmsnorm_quant(p4q_dtype dt, int M, int d, const void *x, int64_t ldx, const void *gamma,
+                      float eps, float clip, uint8_t *codes, float *scales, hipStream_t stream) {
+    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_rmsnorm_quant: dtype %d", (int)dt);
+    if (M <= 0 || d <= 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_rmsnorm_quant: M=%d d=%d", M, d);
+    if (d % 32 != 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_rmsnorm_quant: d=%d not a multiple of 32", d);
+    if (d > 16384) return fail(P4Q_ERR_UNSUPPORTED, "p4q_rmsnorm_quant: d=%d > 16384", d);
+    if (ldx < d || ldx % 8 != 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_rmsnorm_quant: ldx=%lld (need >= d, multiple of 8)", (long long)ldx);
+    if (!x || !gamma || !codes || !scales) return fail(P4Q_ERR_INVALID_ARG, "p4q_rmsnorm_quant: null pointer");
+    if (!aligned(x, 16) || !aligned(gamma, 16) || !aligned(codes, 16) || !aligned(scales, 4))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_rmsnorm_quant: misaligned pointer");
+    if (!(eps >= 0.0f && eps <= 1.0f)) return fail(P4Q_ERR_INVALID_ARG, "p4q_rmsnorm_quant: eps %g outside [0, 1]", eps);
+    if (!valid_clip(clip)) return fail(P4Q_ERR_INVALID_ARG, "p4q_rmsnorm_quant: clip %g outside [2^-16, 1]", clip);
+    return hip_status(p4q::launch_rmsnorm_quant(dt, M, d, x, ldx, gamma, eps, clip, codes, scales, stream),
+                      "p4q_rmsnorm_quant");
+}
+
 size_t p4q_w4a4_linear_workspace_bytes(int M, int N_out, int K_in) {
     if (M <= 0 || N_out <= 0 || K_in <= 0) return 0;
     return p4q::gemm_workspace_bytes(M, N_out, K_in);

@@ -15,6 +15,11 @@ namespace p4q {
 hipError_t launch_quant_act(p4q_dtype dt, int M, int K_in, const void *x, int64_t ldx,
                             float clip, uint8_t *codes, float *scales, hipStream_t stream);
 
+// ---- fused prologue: per-token Q4 of RMSNorm(x) * gamma ------------------------
+hipError_t launch_rmsnorm_quant(p4q_dtype dt, int M, int d, const void *x, int64_t ldx,
+                                const void *gamma, float eps, float clip, uint8_t *codes,
+                                float *scales, hipStream_t stream);
+
 // ---- selector ---------------------------------------------------------------
 struct SelectWorkspace {
     int32_t *stats;      // [B][N][J+1]: D_0..D_{J-1}, Nv   (documented)

@@ -154,6 +154,32 @@ def test_select_budgets_match_the_oracle():
                                       ctypes.byref(kd)) == L.P4Q_ERR_INVALID_ARG
 
 
+def rmsq(**kw):
+    a = dict(dt=0, M=4, d=64, x=ALIGNED, ldx=64, g=ALIGNED, eps=1e-5, clip=1.0, codes=ALIGNED,
+             scales=ALIGNED)
+    a.update(kw)
+    return L.lib().p4q_rmsnorm_quant(a["dt"], a["M"], a["d"], a["x"], a["ldx"], a["g"],
+                                     F(a["eps"]), F(a["clip"]), a["codes"], a["scales"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(M=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(d=48, ldx=48), L.P4Q_ERR_INVALID_ARG),
+    (dict(d=16416, ldx=16416), L.P4Q_ERR_UNSUPPORTED),
+    (dict(ldx=60), L.P4Q_ERR_INVALID_ARG),
+    (dict(ldx=68), L.P4Q_ERR_INVALID_ARG),
+    (dict(g=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(g=ALIGNED + 2), L.P4Q_ERR_INVALID_ARG),
+    (dict(eps=-1.0), L.P4Q_ERR_INVALID_ARG),
+    (dict(eps=float("nan")), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip=0.0), L.P4Q_ERR_INVALID_ARG),
+    (dict(dt=9), L.P4Q_ERR_UNSUPPORTED),
+])
+def test_rmsnorm_quant_validation(kw, status):
+    assert rmsq(**kw) == status
+    assert L.lib().p4q_last_error() != b""
+
+
 def linear(**kw):
     a = dict(M=4, N=8, K=64, a=ALIGNED, sa=ALIGNED, w=ALIGNED, sw=ALIGNED, dt=1, y=ALIGNED,
              ldy=8, acc=None, ws=None, ws_bytes=0)

@@ -20,6 +20,8 @@ Value recipe (identical for every config):
   * inputs of o_proj / down_proj (stand-ins for the attention output and the
     gated MLP activation): drawn like the visual features, each with its own
     outlier channels;
+  * RMSNorm weight of the fused prologue (stand-in, with calibration's
+    diagonal scales folded in): 1 + 0.1 N(0, 1);
   * CLS-to-patch attention (stand-in for the vision tower's final-layer
     attention that the Visual Saliency stage reads, Sec. 3.2): per image
     tile of 576 patches and per head (16 heads), a softmax of N(0, 3^2)
@@ -42,6 +44,7 @@ SEED = 42
 _T_VIS, _T_TEXT, _T_OUTLIER, _T_OPROJ_IN, _T_DOWN_IN = 0, 1, 2, 3, 4
 _T_OPROJ_OUTLIER, _T_DOWN_OUTLIER = 5, 6
 _T_CLS = 7               # CLS-to-patch attention stand-in
+_T_NORM = 8              # RMSNorm weight (with folded diagonal scales) stand-in
 _T_WEIGHT0 = 16          # weights use tensor ids 16 + linear index
 _T_GEMV_IN = 32          # decode-step activations
 
@@ -239,6 +242,14 @@ def mlp_standin(cfg: Config, rows: Optional[int] = None) -> np.ndarray:
     width = f[0] if f else cfg.d
     return outlier_features(cfg.cfg_id, _T_DOWN_IN, _T_DOWN_OUTLIER, rows, width, 0,
                             cfg.in_dtype)
+
+
+def norm_weight(cfg: Config, d: Optional[int] = None) -> np.ndarray:
+    """[d] RMSNorm weight stand-in (the per-channel slot into which the
+    calibration's diagonal scales fold): 1 + 0.1 N(0, 1), storage dtype."""
+    d = cfg.d if d is None else d
+    g = _rng(cfg.cfg_id, _T_NORM).standard_normal(d, dtype=np.float32)
+    return encode(np.float32(1.0) + np.float32(0.1) * g, cfg.in_dtype)
 
 
 def gemv_activations(cfg: Config, M: int, k_in: int) -> np.ndarray:
