@@ -385,6 +385,37 @@ def rmsnorm_quant(x: np.ndarray, gamma: np.ndarray, eps: float = 1e-5,
 
 
 # --------------------------------------------------------------------------
+# O6: FP16-KV attention prefill on the pruned sequence -- the decoder step
+#     after the q/k/v linears (Appendix B.3: W4A4 with the key and value
+#     caches kept in FP16)
+# --------------------------------------------------------------------------
+def attention_prefill(q: np.ndarray, k: np.ndarray, v: np.ndarray, causal: bool = True,
+                      dtype: str = "fp16") -> np.ndarray:
+    """Scaled dot-product attention of one sequence, all heads.
+
+    q, k, v [L, H, D] in storage dtype.  For token t and head h:
+        S[t, j] = <q_t, k_j> / sqrt(D)   over the allowed keys j (j <= t when
+                                          causal, every j otherwise)
+        P[t, :] = softmax(S[t, :]),  O[t] = sum_j P[t, j] v_j
+    in float64, then rounded to the storage dtype (nearest, ties to even).
+    Returns O [L, H, D] in storage dtype."""
+    qf, kf, vf = (as_f32(a, dtype).astype(np.float64) for a in (q, k, v))
+    L, H, D = qf.shape
+    out = np.empty((L, H, D), dtype=np.float64)
+    allowed = np.tril(np.ones((L, L), dtype=bool)) if causal else np.ones((L, L), dtype=bool)
+    for h in range(H):
+        S = (qf[:, h, :] @ kf[:, h, :].T) / np.sqrt(D)
+        S = np.where(allowed, S, -np.inf)
+        S = S - S.max(axis=1, keepdims=True)
+        P = np.exp(S)
+        P = P / P.sum(axis=1, keepdims=True)
+        out[:, h, :] = P @ vf[:, h, :]
+    if dtype == "fp16":
+        return out.astype(np.float16)
+    return f32_to_bf16_rne(out.astype(np.float32))
+
+
+# --------------------------------------------------------------------------
 # O4: the W4A4 linear (integer GEMM on codes + dequant epilogue)
 # --------------------------------------------------------------------------
 def int_gemm(a_codes: np.ndarray, w_codes: np.ndarray) -> np.ndarray:
