@@ -184,6 +184,30 @@ int p4q_rmsnorm_quant(p4q_dtype dt, int M, int d, const void *x, int64_t ldx,
                       uint8_t *codes, float *scales, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Attention prefill on the pruned sequence (Appendix B.3: W4A4 linears with
+ * the key and value caches kept in FP16; this is the step after the q/k/v
+ * linears of a decoder layer).
+ *
+ * For sample b < B, head h < H and token t < L:
+ *   S[t, j] = <q[b,t,h,:], k[b,j,h,:]> / sqrt(D) over j <= t (causal = 1)
+ *             or every j < L (causal = 0),
+ *   out[b,t,h,:] = sum_j softmax_j(S[t, :]) v[b,j,h,:].
+ * fp32 scores, softmax and accumulation; the softmax weights are rounded to
+ * the input dtype before they multiply v (so outputs agree with an exact
+ * evaluation to about 2^-10 (fp16) / 2^-7 (bf16) of max|v|); out is rounded
+ * to the input dtype (nearest, ties to even).
+ *
+ * Layouts: element (b, t, h, d) of q, k and v is at ptr[(b L + t) ld + h D
+ *   + d] -- so q, k, v can point into one fused q|k|v projection output
+ *   with ld = 3 H D -- and of out at out[(b L + t) ld_out + h D + d].
+ * Limits: D == 128; ld >= H D, ld % 8 == 0; ld_out >= H D, ld_out % 4 == 0;
+ *   q, k, v 16-byte aligned, out 8-byte aligned; causal is 0 or 1.
+ * ---------------------------------------------------------------------- */
+int p4q_attention_prefill(p4q_dtype dt, int B, int L, int H, int D,
+                          const void *q, const void *k, const void *v, int64_t ld,
+                          void *out, int64_t ld_out, int causal, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * W4A4 linear (Appendix B.3: RTN int4 weights and activations for W4A4
  * inference): an integer GEMM on the codes and a dequant epilogue.
  *

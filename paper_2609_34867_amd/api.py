@@ -185,6 +185,34 @@ def rmsnorm_quant(x: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-5, clip:
     return codes, scales
 
 
+# --------------------------------------------------------------------------- attention
+def attention_prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, B: int, H: int,
+                      causal: bool = True, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Attention prefill (p4q_attention_prefill) with head dimension 128.
+
+    q, k, v: 2-D [B*L, >= H*128] views with a shared row stride (e.g. column
+    slices of one fused q|k|v output); returns out [B*L, H*128] of the same
+    dtype."""
+    _need_gpu(q, k, v, out)
+    rows = q.shape[0]
+    if rows % B:
+        raise ValueError("rows must be B * L")
+    L = rows // B
+    D = 128
+    for t in (q, k, v):
+        if t.dim() != 2 or t.shape[0] != rows or t.shape[1] < H * D or t.stride(1) != 1:
+            raise ValueError("q, k, v must be 2-D [B*L, >= H*D] with unit column stride")
+        if t.stride(0) != q.stride(0) or t.dtype != q.dtype:
+            raise ValueError("q, k, v must share row stride and dtype")
+    if out is None:
+        out = torch.empty((rows, H * D), dtype=q.dtype, device=q.device)
+    st = lib().p4q_attention_prefill(_dtype_code(q.dtype), B, L, H, D, _ptr(q), _ptr(k), _ptr(v),
+                                     q.stride(0), _ptr(out), out.stride(0), int(causal),
+                                     _stream(q.device))
+    check(st)
+    return out
+
+
 # --------------------------------------------------------------------------- W4A4 linear
 def w4a4_linear_workspace(M: int, N_out: int, K_in: int, device) -> Optional[torch.Tensor]:
     n = lib().p4q_w4a4_linear_workspace_bytes(M, N_out, K_in)

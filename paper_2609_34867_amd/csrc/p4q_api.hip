@@ -174,6 +174,26 @@ int p4q_rmsnorm_quant(p4q_dtype dt, int M, int d, const void *x, int64_t ldx, co
                       "p4q_rmsnorm_quant");
 }
 
+int p4q_attention_prefill(p4q_dtype dt, int B, int L, int H, int D, const void *q, const void *k,
+                          const void *v, int64_t ld, void *out, int64_t ld_out, int causal,
+                          hipStream_t stream) {
+    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_attention_prefill: dtype %d", (int)dt);
+    if (B <= 0 || L <= 0 || H <= 0 || D <= 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_attention_prefill: B=%d L=%d H=%d D=%d", B, L, H, D);
+    if (D != 128) return fail(P4Q_ERR_UNSUPPORTED, "p4q_attention_prefill: head dimension %d (128 only)", D);
+    if (causal != 0 && causal != 1) return fail(P4Q_ERR_INVALID_ARG, "p4q_attention_prefill: causal=%d", causal);
+    if (ld < (int64_t)H * D || ld % 8 != 0 || ld_out < (int64_t)H * D || ld_out % 4 != 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_attention_prefill: ld=%lld ld_out=%lld (need >= H*D; multiples of 8 / 4)",
+                    (long long)ld, (long long)ld_out);
+    if (!q || !k || !v || !out) return fail(P4Q_ERR_INVALID_ARG, "p4q_attention_prefill: null pointer");
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 8))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_attention_prefill: misaligned pointer");
+    if (B > 65535 || H > 65535 || (int64_t)B * L > (1LL << 31) / 2)
+        return fail(P4Q_ERR_UNSUPPORTED, "p4q_attention_prefill: B=%d H=%d L=%d too large", B, H, L);
+    return hip_status(p4q::launch_attention(dt, B, L, H, q, k, v, ld, out, ld_out, causal, stream),
+                      "p4q_attention_prefill");
+}
+
 size_t p4q_w4a4_linear_workspace_bytes(int M, int N_out, int K_in) {
     if (M <= 0 || N_out <= 0 || K_in <= 0) return 0;
     return p4q::gemm_workspace_bytes(M, N_out, K_in);

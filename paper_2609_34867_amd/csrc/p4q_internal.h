@@ -20,6 +20,11 @@ hipError_t launch_rmsnorm_quant(p4q_dtype dt, int M, int d, const void *x, int64
                                 const void *gamma, float eps, float clip, uint8_t *codes,
                                 float *scales, hipStream_t stream);
 
+// ---- attention prefill (FP16 / BF16 Q, K, V; head dimension 128) -------------
+hipError_t launch_attention(p4q_dtype dt, int B, int L, int H, const void *q, const void *k,
+                            const void *v, int64_t ld, void *o, int64_t ldo, int causal,
+                            hipStream_t stream);
+
 // ---- selector ---------------------------------------------------------------
 struct SelectWorkspace {
     int32_t *stats;      // [B][N][J+1]: D_0..D_{J-1}, Nv   (documented)

@@ -180,6 +180,31 @@ def test_rmsnorm_quant_validation(kw, status):
     assert L.lib().p4q_last_error() != b""
 
 
+def attn(**kw):
+    a = dict(dt=0, B=1, L=16, H=2, D=128, q=ALIGNED, k=ALIGNED, v=ALIGNED, ld=768, o=ALIGNED,
+             ldo=256, causal=1)
+    a.update(kw)
+    return L.lib().p4q_attention_prefill(a["dt"], a["B"], a["L"], a["H"], a["D"], a["q"], a["k"],
+                                         a["v"], a["ld"], a["o"], a["ldo"], a["causal"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(L=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(D=64), L.P4Q_ERR_UNSUPPORTED),
+    (dict(causal=2), L.P4Q_ERR_INVALID_ARG),
+    (dict(ld=200), L.P4Q_ERR_INVALID_ARG),
+    (dict(ld=772), L.P4Q_ERR_INVALID_ARG),
+    (dict(ldo=255), L.P4Q_ERR_INVALID_ARG),
+    (dict(k=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(v=ALIGNED + 8), L.P4Q_ERR_INVALID_ARG),
+    (dict(o=ALIGNED + 2), L.P4Q_ERR_INVALID_ARG),
+    (dict(dt=4), L.P4Q_ERR_UNSUPPORTED),
+])
+def test_attention_validation(kw, status):
+    assert attn(**kw) == status
+    assert L.lib().p4q_last_error() != b""
+
+
 def linear(**kw):
     a = dict(M=4, N=8, K=64, a=ALIGNED, sa=ALIGNED, w=ALIGNED, sw=ALIGNED, dt=1, y=ALIGNED,
              ldy=8, acc=None, ws=None, ws_bytes=0)
