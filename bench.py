@@ -16,8 +16,8 @@ steps read weights like successive decoder layers would (101 MB per layer at
 
 Prints ONE JSON line.  value = W4A4 linear ops of the step / step time (TOPS);
 the selector's token rate and the GEMM-only rate are reported beside it, and,
-outside the timed steps, the fused RMSNorm + quantize prologue, the
-three-stage selector (selector_full) and the decode-step GEMV.
+outside the timed steps, the fused RMSNorm + quantize prologue, the attention
+prefill, the three-stage selector (selector_full) and the decode-step GEMV.
 """
 from __future__ import annotations
 
@@ -34,6 +34,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 INT8_PEAK_TOPS = 5000.0      # MI355X dense int8 MFMA
+FP16_PEAK_TFLOPS = 2500.0    # MI355X dense fp16 MFMA
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 N_WEIGHT_SETS = 4
 
@@ -347,6 +348,38 @@ def prologue(cfg, st, dev, reps=20):
             "unfused_extra_bytes": 2 * cfg.M * cfg.d * 2}
 
 
+def attention(cfg, dev, reps=20):
+    """Causal attention prefill of the decoder layer on the pruned sequence
+    (B samples x K+T tokens, 32 heads of 128) reading q, k, v out of one fused
+    q|k|v buffer, fp16.  Bound by the MFMA work: 4 B H D sum_t (t+1) flops
+    (the causal half), fp16 dense peak 2500 TFLOP/s."""
+    import torch
+    import paper_2609_34867_amd as p4q
+
+    B, L, D = cfg.B, cfg.K + cfg.T, 128
+    H = cfg.d // D
+    g = torch.Generator(device="cpu").manual_seed(7)
+    qkv = torch.randn((B * L, 3 * H * D), generator=g, dtype=torch.float32).to(torch.float16).to(dev)
+    out = torch.empty((B * L, H * D), dtype=torch.float16, device=dev)
+    run = lambda: p4q.attention_prefill(qkv[:, :H * D], qkv[:, H * D:2 * H * D], qkv[:, 2 * H * D:],
+                                        B, H, True, out=out)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    flops = 4 * B * H * D * (L * (L + 1) // 2)
+    return {"workload": f"causal attention prefill, B={B} x L={L} tokens, H={H} heads of {D}, "
+                        "fp16 q|k|v from one fused buffer",
+            "us": round(us, 2), "tflops": round(flops / us / 1e6, 1),
+            "mfma_frac": round(flops / us / 1e6 / FP16_PEAK_TFLOPS, 4)}
+
+
 def copy_calibration(dev, nbytes=1 << 30, reps=5):
     """A plain device-to-device copy of known size, run so that the HBM
     counters (FETCH_SIZE, WRITE_SIZE) can be scaled to bytes: the counter
@@ -448,6 +481,7 @@ def main():
         "lib": p4q.version(),
     }
     res["prologue_rmsnorm_quant"] = prologue(cfg, st, dev)
+    res["attention_prefill"] = attention(cfg, dev)
     if not args.no_select_full:
         res["selector_full"] = selector_full(cfg, dev)
     if not args.no_decode:

@@ -188,8 +188,9 @@ int p4q_attention_prefill(p4q_dtype dt, int B, int L, int H, int D, const void *
     if (!q || !k || !v || !out) return fail(P4Q_ERR_INVALID_ARG, "p4q_attention_prefill: null pointer");
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 8))
         return fail(P4Q_ERR_INVALID_ARG, "p4q_attention_prefill: misaligned pointer");
-    if (B > 65535 || H > 65535 || (int64_t)B * L > (1LL << 31) / 2)
-        return fail(P4Q_ERR_UNSUPPORTED, "p4q_attention_prefill: B=%d H=%d L=%d too large", B, H, L);
+    if (B > 65535 || H > 65535 || (int64_t)L * ld * 2 >= (1LL << 31))
+        return fail(P4Q_ERR_UNSUPPORTED, "p4q_attention_prefill: B=%d H=%d L=%d ld=%lld too large (L*ld*2 < 2^31)",
+                    B, H, L, (long long)ld);
     return hip_status(p4q::launch_attention(dt, B, L, H, q, k, v, ld, out, ld_out, causal, stream),
                       "p4q_attention_prefill");
 }
