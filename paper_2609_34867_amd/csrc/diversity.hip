@@ -33,6 +33,7 @@ namespace {
 constexpr int64_t kNoneP = -(1LL << 40);      // below every cosine: "S empty"
 constexpr uint64_t kIdxMask = 0x1FFFull;      // 13 index bits (N <= 8192)
 constexpr uint64_t kNoKey = ~0ull;
+constexpr uint32_t kNone32 = 0xFFFFFFFFu;
 
 // the pair of cos(i, t) from D = G[i][t] and Nv_t
 __device__ __forceinline__ void cos_pair(int32_t D, int32_t nvt, int64_t &p, int32_t &q) {
@@ -159,6 +160,43 @@ __device__ __forceinline__ void wave_min2(uint64_t &k1, uint64_t &k2) {
     k2 = a2;
 }
 
+template <int CTRL>
+__device__ __forceinline__ uint64_t min_dpp(uint64_t a) {
+    const uint64_t b = dpp64<CTRL>(a);
+    return b < a ? b : a;
+}
+
+// smallest key of the wavefront, wave-uniform
+__device__ __forceinline__ uint64_t wave_min1(uint64_t a) {
+    a = min_dpp<0xB1>(a);
+    a = min_dpp<0x4E>(a);
+    a = min_dpp<0x141>(a);
+    a = min_dpp<0x140>(a);
+    uint64_t r = readlane64(a, 0);
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+        const uint64_t x = readlane64(a, 16 * w);
+        r = x < r ? x : r;
+    }
+    return r;
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t min_dpp32(uint32_t a) {
+    return min(a, (uint32_t)__builtin_amdgcn_mov_dpp((int)a, CTRL, 0xF, 0xF, false));
+}
+
+// smallest value of the wavefront, wave-uniform
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t a) {
+    a = min_dpp32<0xB1>(a);
+    a = min_dpp32<0x4E>(a);
+    a = min_dpp32<0x141>(a);
+    a = min_dpp32<0x140>(a);
+    const uint32_t r0 = __builtin_amdgcn_readlane((int)a, 0), r1 = __builtin_amdgcn_readlane((int)a, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane((int)a, 32), r3 = __builtin_amdgcn_readlane((int)a, 48);
+    return min(min(r0, r1), min(r2, r3));
+}
+
 // order-preserving bits of an fp32 value (-0 below +0)
 __device__ __forceinline__ uint32_t ord32(float v) {
     const uint32_t u = __float_as_uint(v);
@@ -195,6 +233,9 @@ __global__ __launch_bounds__(NT) void k_div_greedy(const int32_t *__restrict__ G
                                                    int32_t *__restrict__ idx_out) {
     constexpr int NW = NT / 64;
     static_assert(NT >= 256 && NT <= 1024 && NT % 64 == 0, "one bitmap word per thread");
+    // greedy picks verified per block-wide selection (fewer at 1024 threads,
+    // where a thread has 128 registers)
+    constexpr int kBatch = NT <= 512 ? (E <= 6 ? 16 : 8) : (E <= 5 ? 4 : 2);
     __shared__ uint32_t bm[256];                                   // kept bitmap (N <= 8192)
     __shared__ unsigned long long r1[2][NW], r2[2][NW];
     __shared__ long long xp[NW];
@@ -202,6 +243,8 @@ __global__ __launch_bounds__(NT) void k_div_greedy(const int32_t *__restrict__ G
     __shared__ int xi[NW];
     __shared__ __attribute__((aligned(16))) uint32_t wtot[16];
     __shared__ int32_t nvs[8192];                                  // Nv of the candidates
+    __shared__ uint32_t wlv[NW][kBatch + 1], wli[NW][kBatch + 1];  // per-wavefront smallest values, tokens
+    __shared__ uint32_t vflag[2];                                  // verified list positions
 
     const int b = blockIdx.x, t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -356,6 +399,8 @@ __global__ __launch_bounds__(NT) void k_div_greedy(const int32_t *__restrict__ G
         }
     };
 
+    if (t == 0) { vflag[0] = 0; vflag[1] = 0; }
+    __syncthreads();
     int par = 0;
     if (n0 == 0 && kd > 0) {
         // seed: the most salient token (largest CLS weight, lower index first)
@@ -375,21 +420,179 @@ __global__ __launch_bounds__(NT) void k_div_greedy(const int32_t *__restrict__ G
         par ^= 1;
         if (o1 != kNoKey) keep((int)(o1 & kIdxMask), -1);
     }
+    // Batched steps.  The kBatch + 1 smallest approximate values c_0 <= c_1
+    // <= ... are taken in one block-wide selection and their rows loaded
+    // together.  c_0 is the exact minimum when it is more than kUlpTol ulps
+    // below c_1 (otherwise the exact comparison picks one token and the batch
+    // ends there).  c_j (j >= 1) is the exact minimum after c_0 .. c_{j-1} are
+    // kept when its value raised by their rows is still more than kUlpTol ulps
+    // below the value of c_{j+1}: every other candidate's value can only have
+    // grown from at least that.  The verified prefix is kept and every
+    // candidate is updated from its rows.
+    int nbatch = 0;
     while (picks < kd) {
-        uint64_t k1 = kNoKey, k2 = kNoKey;
+        // (1) selection on the order-preserving bits of vf (ties between
+        //     equal values are left to the verification, which never accepts
+        //     them): per wavefront the kBatch + 1 smallest, then the same
+        //     extraction over the wavefronts' lists
+        uint32_t lv[kBatch + 1], li[kBatch + 1];
+        {
+            uint32_t ov[E];
 #pragma unroll
-        for (int e = 0; e < E; ++e)
-            if ((live >> e) & 1u) merge2(k1, k2, ((uint64_t)ord32(vf[e]) << 32) | (uint64_t)(e * NT + t), kNoKey);
-        uint64_t o1, o2;
-        block_min2(k1, k2, par, o1, o2);
-        par ^= 1;
-        if (o1 == kNoKey) break;             // no candidate left (not reached for kd <= N - n0)
-        int best = (int)(o1 & kIdxMask);
-        const uint32_t v1 = (uint32_t)(o1 >> 32);
-        if (o2 != kNoKey && (uint32_t)(o2 >> 32) - v1 <= kUlpTol) best = exact_min(v1 + kUlpTol);
-        int next = o2 != kNoKey ? (int)(o2 & kIdxMask) : -1;
-        if (next == best) next = (int)(o1 & kIdxMask);
-        keep(best, next);
+            for (int e = 0; e < E; ++e) ov[e] = ((live >> e) & 1u) ? ord32(vf[e]) : kNone32;
+            uint32_t ext = 0;
+            auto local_min = [&]() {
+                uint32_t m = kNone32;
+#pragma unroll
+                for (int e = 0; e < E; ++e) m = ((ext >> e) & 1u) ? m : min(m, ov[e]);
+                return m;
+            };
+            uint32_t lm = local_min();
+#pragma unroll
+            for (int r = 0; r <= kBatch; ++r) {
+                const uint32_t v = wave_min_u32(lm);
+                uint32_t tok = kNone32;
+                if (v != kNone32) {
+                    const int src = (int)__builtin_ctzll(__ballot(lm == v));      // lowest lane holding v
+                    int slot = 0;
+                    if (lane == src) {
+#pragma unroll
+                        for (int e = E - 1; e >= 0; --e)
+                            if (!((ext >> e) & 1u) && ov[e] == v) slot = e;
+                        ext |= 1u << slot;
+                        lm = local_min();
+                    }
+                    tok = (uint32_t)__shfl(slot * NT + t, src);
+                }
+                if (lane == 0) { wlv[wave][r] = v; wli[wave][r] = tok; }
+            }
+            __syncthreads();
+            constexpr int NE = NW * (kBatch + 1);
+            constexpr int PER = (NE + 63) / 64;
+            uint32_t av[PER], ai[PER];
+#pragma unroll
+            for (int u = 0; u < PER; ++u) {
+                const int q = lane + 64 * u;
+                av[u] = q < NE ? wlv[q / (kBatch + 1)][q % (kBatch + 1)] : kNone32;
+                ai[u] = q < NE ? wli[q / (kBatch + 1)][q % (kBatch + 1)] : kNone32;
+            }
+#pragma unroll
+            for (int r = 0; r <= kBatch; ++r) {
+                uint32_t m = kNone32;
+#pragma unroll
+                for (int u = 0; u < PER; ++u) m = min(m, av[u]);
+                const uint32_t v = wave_min_u32(m);
+                uint32_t tok = kNone32;
+                if (v != kNone32) {
+                    const int src = (int)__builtin_ctzll(__ballot(m == v));
+                    uint32_t mine = kNone32;
+                    if (lane == src) {
+                        bool done = false;
+#pragma unroll
+                        for (int u = 0; u < PER; ++u)
+                            if (!done && av[u] == v) { mine = ai[u]; av[u] = kNone32; done = true; }
+                    }
+                    tok = (uint32_t)__shfl((int)mine, src);
+                }
+                lv[r] = v;
+                li[r] = tok;
+            }
+        }
+        if (lv[0] == kNone32) break;          // no candidate left (not reached for kd <= N - n0)
+        // (2) the head: exact unless it is clear of the runner-up
+        const bool head_clear = lv[1] == kNone32 || lv[1] - lv[0] > kUlpTol;
+        int nb = head_clear ? min(kBatch, kd - picks) : 1;
+        int c[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) c[j] = (int)li[j];
+        if (!head_clear) c[0] = exact_min(lv[0] + kUlpTol);
+        for (int j = 1; j < kBatch; ++j)      // the list may run out
+            if (j < nb && lv[j] == kNone32) nb = j;
+        // (3) rows of the batch, all in flight together
+        int32_t Drow[kBatch][E];
+        float invb[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            if (j < nb) {
+                load_row(c[j], Drow[j]);
+                const int32_t nvb = nvs[c[j]];
+                invb[j] = nvb > 0 ? 1.0f / (float)nvb : 0.0f;
+            }
+        }
+        // (4) verify c_1 .. c_{nb-1}: the owner of c_j raises its value by the
+        // rows of c_0 .. c_{j-1} and compares with the value of c_{j+1}
+        const int fb = nbatch & 1;            // alternating flag word: one barrier per batch
+        ++nbatch;
+        if (nb > 1) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int i = e * NT + t;
+#pragma unroll
+                for (int j = 1; j < kBatch; ++j) {
+                    if (j < nb && i == c[j] && ((live >> e) & 1u)) {
+                        float v = vf[e];
+#pragma unroll
+                        for (int k2 = 0; k2 < kBatch; ++k2) {
+                            if (k2 < j) {
+                                const float df = (float)Drow[k2][e];
+                                v = __builtin_fmaxf(v, ((df * __builtin_fabsf(df)) * inv[e]) * invb[k2]);
+                            }
+                        }
+                        if (lv[j + 1] == kNone32 || (int64_t)ord32(v) + (int64_t)kUlpTol < (int64_t)lv[j + 1])
+                            atomicOr(&vflag[fb], 1u << j);
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        const uint32_t fl = vflag[fb];
+        int a = 1;
+        while (a < nb && ((fl >> a) & 1u)) ++a;
+        // (5) keep c_0 .. c_{a-1}
+        if (t == 0) {
+            for (int j = 0; j < a; ++j) {
+                st[n0 + picks + j] = c[j];
+                bm[c[j] >> 5] |= 1u << (c[j] & 31);
+            }
+            vflag[fb ^ 1] = 0;                // the next batch's word
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+            if (j < a && (c[j] % NT) == t) live &= ~(1u << (c[j] / NT));
+        picks += a;
+        if (picks >= kd) break;
+        // (6) update every candidate from the kept rows: the largest fp32
+        // cosine of the batch against vf first (the usual case ends there)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            if (!((live >> e) & 1u)) continue;
+            float cmax = -__builtin_huge_valf();
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                if (j < a) {
+                    const float df = (float)Drow[j][e];
+                    cmax = __builtin_fmaxf(cmax, ((df * __builtin_fabsf(df)) * inv[e]) * invb[j]);
+                }
+            }
+            if ((int64_t)ord32(cmax) + (int64_t)kUlpTol < (int64_t)ord32(vf[e])) continue;   // clearly not above
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {                    // rare: row by row
+                if (j < a) {
+                    const float df = (float)Drow[j][e];
+                    const float cf = ((df * __builtin_fabsf(df)) * inv[e]) * invb[j];
+                    const int64_t oc = ord32(cf), ov = ord32(vf[e]);
+                    if (oc + (int64_t)kUlpTol < ov) continue;
+                    int64_t pp;
+                    int32_t qq;
+                    cos_pair(Drow[j][e], nvs[c[j]], pp, qq);
+                    if (oc > ov + (int64_t)kUlpTol || pair_gt(pp, qq, p[e], q[e])) {
+                        p[e] = pp;
+                        q[e] = qq;
+                        vf[e] = cf;
+                    }
+                }
+            }
+        }
     }
 
     // idx_out[b] = the kept set in ascending order (one bitmap word per
