@@ -30,6 +30,10 @@ Acceleration"):
   alpha = 0.3, beta = 0.2, gamma = 0.5): the full selector -- CLS-attention
   top-k over the tokens left after Query Relevance, then max-min completion
   on the cosines of the fake-quantized copies.
+* Sec. 3.3, Eq. (p4q_pruning_aware_calibration) and Appendix B.3: block-wise
+  calibration minimizes the per-sample mean squared error between the
+  W4A4 fake-quantized and the full-precision outputs on the pruned sequence,
+  over diagonal channel scales and weight / activation clipping factors.
 
 Readings where the paper is silent (each is listed in the design doc):
 * code range [-8, 7], scale = fl32(fl32(c*absmax)/7); ties round half to even;
@@ -46,6 +50,13 @@ Readings where the paper is silent (each is listed in the design doc):
   index; a zero code vector has cosine 0 with everything; with an empty
   retained set the diversity stage starts from the most salient token;
 * epilogue y = out_rne(fl32(fl32(float(acc) * s_a[m]) * s_w[n])).
+* calibration (O7), one linear at a time: the diagonal scales divide the
+  activation channels and multiply the weight input channels; the clipping
+  factor multiplies the row maximum before the division by 7 (one factor for
+  activations, one per output channel for weights); rounding passes
+  gradients straight through, the clamp only where the rounded quotient is
+  in [-8, 7], the row maximum to its lowest-index element; the loss is the
+  squared error summed over the M x N outputs divided by M N.
 """
 from __future__ import annotations
 
@@ -454,3 +465,144 @@ def w4a4_linear_entry(a_packed: np.ndarray, a_scales: np.ndarray, w_packed: np.n
     y = epilogue(np.array([[acc]], dtype=np.int64), a_scales[m:m + 1], w_scales[n:n + 1],
                  out_dtype)
     return acc, y[0, 0]
+
+
+# --------------------------------------------------------------------------
+# O7: pruning-aware calibration mechanics (Sec. 3.3, Eq.
+#     p4q_pruning_aware_calibration; Appendix B.3) -- the reconstruction
+#     objective of one W4A4 fake-quantized linear on a pruned sequence and its
+#     gradients with respect to the learnable diagonal channel scales and the
+#     activation / weight clipping factors
+# --------------------------------------------------------------------------
+def quant_rows_scaled(z: np.ndarray, sigma: np.ndarray, divide: bool, clip,
+                      dtype: str = "fp16"):
+    """Q4 of the channel-transformed rows z'.
+
+    z' = fl32(z / sigma_k) (divide=True: activations, whose channels the
+    diagonal scales divide) or fl32(z * sigma_k) (divide=False: weights, whose
+    input channels they multiply), each a correctly rounded fp32 operation.
+    clip is one factor for every row or one per row.  Returns (codes int8
+    [R, L], scales fp32 [R], absmax fp32 [R] = max_k |z'_k|, kstar int64 [R] =
+    the lowest k attaining it, z' fp32 [R, L])."""
+    zf = as_f32(z, dtype)
+    sig = np.asarray(sigma, dtype=np.float32)
+    zp = (zf / sig[None, :]) if divide else (zf * sig[None, :])
+    zp = zp.astype(np.float32)
+    if not np.all(np.isfinite(zp)):
+        raise ValueError("non-finite transformed row")
+    R = zp.shape[0]
+    clips = np.broadcast_to(np.asarray(clip, dtype=np.float32), (R,))
+    codes = np.zeros(zp.shape, dtype=np.int8)
+    scales = np.zeros(R, dtype=np.float32)
+    absmax = np.zeros(R, dtype=np.float32)
+    kstar = np.zeros(R, dtype=np.int64)
+    for r in range(R):
+        c, s = quantize_rows(zp[r:r + 1], "fp32", float(clips[r]))
+        codes[r], scales[r] = c[0], s[0]
+        mag = np.abs(zp[r])
+        absmax[r] = mag.max()
+        kstar[r] = int(np.flatnonzero(mag == absmax[r])[0])
+    return codes, scales, absmax, kstar, zp
+
+
+def fq_row_backward(zp: np.ndarray, s: float, clip: float, codes: np.ndarray,
+                    absmax: float, kstar: int, g: np.ndarray):
+    """Gradient of one fake-quantized row F(z') = s * clamp(rne(z'/s), -8, 7),
+    s = clip * max|z'| / 7, given the upstream gradient g = dL/dF.
+
+    Rounding passes gradients straight through; the clamp passes them only
+    where the rounded quotient rho = rne(fl32(z'/s)) lies in [-8, 7]
+    ("inside"); the maximum passes its share to the lowest index attaining it.
+    With g_s = dL/ds = sum_k g_k (code_k - inside_k z'_k / s):
+        dL/dz'_k  = inside_k g_k + [k = kstar] g_s (clip / 7) sign(z'_k)
+        dL/dclip  = g_s * absmax / 7
+    A row with s = 0 has no gradient.  Returns (dz' float64 [L], dclip)."""
+    if s == 0:
+        return np.zeros(zp.shape, dtype=np.float64), 0.0
+    rho = np.rint(zp / np.float32(s))                  # the quotient's fp32 rounding decides
+    inside = ((rho >= QMIN) & (rho <= QMAX)).astype(np.float64)
+    z64 = zp.astype(np.float64)
+    g_s = float(np.sum(g * (codes.astype(np.float64) - inside * z64 / float(s))))
+    dz = g * inside
+    dz[kstar] += g_s * (float(clip) / 7.0) * float(np.sign(z64[kstar]))
+    return dz, g_s * float(absmax) / 7.0
+
+
+def calib_linear(x: np.ndarray, w: np.ndarray, target: np.ndarray, sigma: np.ndarray,
+                 clip_a: float, clip_w: np.ndarray, dtype: str = "fp16",
+                 operands: str = "fp64") -> dict:
+    """Reconstruction loss of one W4A4 fake-quantized linear and its gradients.
+
+    x [M, K] (the pruned sequence's input rows) and w [N, K] in storage
+    dtype; target [M, N] fp32 is the full-precision layer output; sigma [K]
+    > 0 the diagonal channel scales; clip_a the activation clipping factor
+    (one per layer: tokens vary at run time); clip_w [N] the per-output-
+    channel weight clipping factors.
+
+      X' = X diag(sigma)^-1 and W' = W diag(sigma) (the product is unchanged
+      in exact arithmetic, which lets calibration fold sigma into the model);
+      (cA, sA) = Q4 rows of X' with clip_a; (cW, sW) = Q4 rows of W' with
+      clip_w[n]; the fake-quantized output is Yq = (sA cA)(sW cW)^T, i.e.
+      Yq[m, n] = sA[m] sW[n] acc[m, n] with the exact integer acc;
+      loss = ||Yq - target||_F^2 / (M N)    (the per-sample term of the
+      calibration objective, m = M rows of width d = N).
+
+    Gradients (rounding passed straight through, see fq_row_backward), with
+    G = 2 (Yq - target) / (M N):
+      dL/d(sA cA) = G (sW cW),   dL/d(sW cW) = G^T (sA cA);
+      d sigma_k  = sum_m dX'[m, k] (-X[m, k] / sigma_k^2) + sum_n dW'[n, k] W[n, k];
+      d clip_a   = sum over rows m of their dclip;  d clip_w[n] = row n's dclip.
+
+    operands="fp64": everything after the quantizer in float64.
+    operands="bf16": the two contractions take bf16 operands, as a mixed-
+    precision calibration runs them: R = fl32(fl32(fl32(acc sA[m]) sW[n]) -
+    target), and the operands are bf16(fl32(R sW[n])) and bf16(fl32(R sA[m]))
+    (nearest, ties to even); the loss is sum R^2 / (M N); the codes and
+    the rest stay exact / float64.
+
+    Returns a dict with loss, grad_sigma [K], grad_clip_a, grad_clip_w [N]
+    (float64) and the quantizer outputs of both sides."""
+    M, K = x.shape
+    N = w.shape[0]
+    sig = np.asarray(sigma, dtype=np.float32)
+    cw_clip = np.asarray(clip_w, dtype=np.float32).reshape(N)
+    cA, sA, aA, kA, xp = quant_rows_scaled(x, sig, True, np.float32(clip_a), dtype)
+    cW, sW, aW, kW, wp = quant_rows_scaled(w, sig, False, cw_clip, dtype)
+    acc = int_gemm(cA, cW).astype(np.float64)
+    T = np.asarray(target, dtype=np.float32)
+    if operands == "fp64":
+        R = sA.astype(np.float64)[:, None] * sW.astype(np.float64)[None, :] * acc - T
+        P1 = R * sW.astype(np.float64)[None, :]
+        P2 = R * sA.astype(np.float64)[:, None]
+    elif operands == "bf16":
+        y32 = (acc.astype(np.float32) * sA[:, None]).astype(np.float32)
+        y32 = (y32 * sW[None, :]).astype(np.float32)
+        R32 = (y32 - T).astype(np.float32)
+        P1 = as_f32(f32_to_bf16_rne((R32 * sW[None, :]).astype(np.float32)), "bf16")
+        P2 = as_f32(f32_to_bf16_rne((R32 * sA[:, None]).astype(np.float32)), "bf16")
+        R = R32.astype(np.float64)
+        P1 = P1.astype(np.float64)
+        P2 = P2.astype(np.float64)
+    else:
+        raise ValueError(operands)
+    scale = 2.0 / (M * N)
+    loss = float(np.sum(R * R)) / (M * N)
+    gA = scale * (P1 @ cW.astype(np.float64))            # dL/d(sA cA)  [M, K]
+    gW = scale * (P2.T @ cA.astype(np.float64))          # dL/d(sW cW)  [N, K]
+    dxp = np.zeros((M, K), dtype=np.float64)
+    dwp = np.zeros((N, K), dtype=np.float64)
+    dclip_a = 0.0
+    dclip_w = np.zeros(N, dtype=np.float64)
+    for m in range(M):
+        dxp[m], dc = fq_row_backward(xp[m], sA[m], clip_a, cA[m], aA[m], kA[m], gA[m])
+        dclip_a += dc
+    for n in range(N):
+        dwp[n], dclip_w[n] = fq_row_backward(wp[n], sW[n], cw_clip[n], cW[n], aW[n], kW[n],
+                                             gW[n])
+    x64 = as_f32(x, dtype).astype(np.float64)
+    w64 = as_f32(w, dtype).astype(np.float64)
+    s64 = sig.astype(np.float64)
+    grad_sigma = np.sum(dxp * (-x64 / (s64 * s64)[None, :]), axis=0) + np.sum(dwp * w64, axis=0)
+    return {"loss": loss, "grad_sigma": grad_sigma, "grad_clip_a": dclip_a,
+            "grad_clip_w": dclip_w, "a_codes": cA, "a_scales": sA, "a_absmax": aA,
+            "a_kstar": kA, "w_codes": cW, "w_scales": sW, "w_absmax": aW, "w_kstar": kW}

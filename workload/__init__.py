@@ -267,3 +267,44 @@ def random_features(seed: int, rows: int, cols: int, dtype: str = "fp16",
         ch = g.choice(cols, size=outliers, replace=False)
         x[:, ch] *= np.float32(scale)
     return encode(x, dtype)
+
+
+@dataclass
+class CalibProblem:
+    """Inputs of one calibration step of one linear (see calib_problem)."""
+    x: np.ndarray          # [M, K] storage dtype: block input rows of the pruned sequence
+    w: np.ndarray          # [N, K] storage dtype: the frozen full-precision weight
+    target: np.ndarray     # [M, N] float32: the full-precision layer output
+    sigma: np.ndarray      # [K] float32 > 0: diagonal channel scales
+    clip_a: float          # activation clipping factor
+    clip_w: np.ndarray     # [N] float32: weight clipping factors
+    dtype: str
+
+
+def calib_problem(seed: int, M: int, N: int, K: int, dtype: str = "fp16",
+                  clip_a: float = 0.9, w_std: float = WEIGHT_STD) -> CalibProblem:
+    """Seeded stand-in for one calibration step on a pruned sequence
+    (Sec. 3.3, Appendix B.3: block inputs captured after the selector, frozen
+    weights, learnable diagonal scales and clipping factors mid-optimization).
+
+    * x: the activation recipe above (N(0, 1), 8 outlier channels x20);
+    * w: N(0, w_std^2);
+    * sigma: exp(0.3 N(0, 1)), times 20^0.3 on x's outlier channels (the
+      direction in which scales initialized from activation and weight ranges
+      start: outlier channels are divided down);
+    * clip_w: U(0.75, 1) per output channel;
+    * target: x @ w^T in float64 from the stored values, rounded to fp32.
+    No quantizer, gradient or calibration arithmetic happens here."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([SEED, 2000, seed])))
+    x32 = g.standard_normal((M, K), dtype=np.float32)
+    ch = g.choice(K, size=min(N_OUTLIER, K), replace=False)
+    x32[:, ch] *= np.float32(OUTLIER_SCALE)
+    w32 = g.standard_normal((N, K), dtype=np.float32) * np.float32(w_std)
+    sigma = np.exp(np.float32(0.3) * g.standard_normal(K, dtype=np.float32)).astype(np.float32)
+    sigma[ch] *= np.float32(OUTLIER_SCALE ** 0.3)
+    clip_w = g.uniform(0.75, 1.0, N).astype(np.float32)
+    x = encode(x32, dtype)
+    w = encode(w32, dtype)
+    xf, wf = to_f32(x, dtype).astype(np.float64), to_f32(w, dtype).astype(np.float64)
+    target = (xf @ wf.T).astype(np.float32)
+    return CalibProblem(x, w, target, sigma.astype(np.float32), float(clip_a), clip_w, dtype)
