@@ -208,6 +208,72 @@ int p4q_attention_prefill(p4q_dtype dt, int B, int L, int H, int D,
                           void *out, int64_t ld_out, int causal, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Channel-scaled per-row quantizer (Sec. 3.3 and Appendix B.3: the diagonal
+ * channel scales and clipping factors that calibration learns, applied
+ * before RTN; also the folded-weight quantization after calibration).
+ *
+ *   z'[r][k] = fl32(z[r][k] / sigma[k])   (divide = 1: activation channels)
+ *            = fl32(z[r][k] * sigma[k])   (divide = 0: weight input channels)
+ *   (codes[r], scales[r]) = Q4(z'[r]; c_r),  c_r = clip_rows[r] or clip
+ *   absmax[r] = max_k |z'[r][k]|,  kstar[r] = the lowest k attaining it
+ *
+ * Layouts: z [R, ldz] of dt; sigma fp32 [K] (> 0, z' finite); codes uint8
+ *   [R, K/2] packed as p4q_quant_act's; scales, absmax fp32 [R]; kstar int32
+ *   [R].  absmax and kstar may be NULL; clip_rows may be NULL (then clip,
+ *   in (0, 1], serves every row; given, its entries should lie in (0, 1]).
+ * Limits: R >= 1, K % 32 == 0, K <= 16384, ldz >= K and ldz % 8 == 0; z,
+ *   sigma and codes 16-byte aligned.
+ * ---------------------------------------------------------------------- */
+int p4q_quant_scaled(p4q_dtype dt, int R, int K, const void *z, int64_t ldz,
+                     const float *sigma, int divide, float clip,
+                     const float *clip_rows, uint8_t *codes, float *scales,
+                     float *absmax, int32_t *kstar, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Pruning-aware calibration step of one W4A4 linear (Sec. 3.3, Eq.
+ * p4q_pruning_aware_calibration: the per-sample mean squared error between
+ * the fake-quantized and the full-precision outputs on the pruned sequence;
+ * Appendix B.3: diagonal channel scales and weight / activation clipping
+ * factors are the learnable parameters).
+ *
+ *   X' = X / sigma, W' = W * sigma (per channel, as p4q_quant_scaled);
+ *   (cA, sA) = Q4 rows of X' with clip_a; (cW, sW) = Q4 rows of W' with
+ *   clip_w[n]; acc = cA cW^T (exact int32, int8 MFMA);
+ *   R[m][n] = fl32(fl32(fl32(acc sA[m]) sW[n]) - target[m][n]);
+ *   loss = sum R^2 / (M N)
+ * and the gradients of loss with respect to sigma, clip_a and clip_w:
+ * rounding passes gradients straight through, the clamp only where the
+ * rounded quotient lies in [-8, 7], a row's maximum to its lowest-index
+ * element.  The two contractions of the backward pass take bf16 operands
+ * bf16(R sW[n]) and bf16(R sA[m]) (nearest even) against the exact codes,
+ * with fp32 accumulation; every reduction after them is fp32 per tile and
+ * float64 across tiles.
+ *
+ * Layouts: x [M, ldx] and w [N, ldw] of dt (the block input rows of the
+ *   pruned sequence; the frozen weight); target fp32 [M, ldt] (the
+ *   full-precision layer output); sigma fp32 [K] > 0; clip_w fp32 [N] in
+ *   (0, 1]; outputs loss fp32 [1], grad_sigma fp32 [K], grad_clip_a fp32
+ *   [1], grad_clip_w fp32 [N].
+ * Workspace: p4q_calib_linear_workspace_bytes(M, N, K) bytes, 256-byte
+ *   aligned, caller-owned; nothing of it is read before being written.
+ * Limits: M >= 1, N % 64 == 0, K % 128 == 0, K <= 16384, M N and N K
+ *   < 2^31; ldx, ldw >= K and multiples of 8; ldt >= N, multiple of 4;
+ *   clip_a in (0, 1]; x, w, target, sigma 16-byte aligned.
+ * The scatter of the row maxima's shares uses float64 atomics: results can
+ *   differ between runs in the last bits of float64 sums, far below the
+ *   fp32 outputs' precision.
+ * ---------------------------------------------------------------------- */
+size_t p4q_calib_linear_workspace_bytes(int M, int N, int K);
+
+int p4q_calib_linear_grad(p4q_dtype dt, int M, int N, int K,
+                          const void *x, int64_t ldx, const void *w, int64_t ldw,
+                          const float *target, int64_t ldt, const float *sigma,
+                          float clip_a, const float *clip_w, float *loss,
+                          float *grad_sigma, float *grad_clip_a,
+                          float *grad_clip_w, void *ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * W4A4 linear (Appendix B.3: RTN int4 weights and activations for W4A4
  * inference): an integer GEMM on the codes and a dequant epilogue.
  *

@@ -35,6 +35,12 @@ SIGNATURES = {
                                    _vp, _vp, _vp]),
     "p4q_attention_prefill": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp,
                                        _c_i64, _vp, _c_i64, _c_int, _vp]),
+    "p4q_quant_scaled": (_c_int, [_c_int, _c_int, _c_int, _vp, _c_i64, _vp, _c_int, _c_float, _vp,
+                                  _vp, _vp, _vp, _vp, _vp]),
+    "p4q_calib_linear_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int]),
+    "p4q_calib_linear_grad": (_c_int, [_c_int, _c_int, _c_int, _c_int, _vp, _c_i64, _vp, _c_i64,
+                                       _vp, _c_i64, _vp, _c_float, _vp, _vp, _vp, _vp, _vp, _vp,
+                                       _c_size, _vp]),
     "p4q_w4a4_linear_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int]),
     "p4q_w4a4_linear": (_c_int, [_c_int, _c_int, _c_int, _vp, _vp, _vp, _vp, _c_int, _vp,
                                  _c_i64, _vp, _vp, _c_size, _vp]),

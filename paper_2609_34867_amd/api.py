@@ -11,7 +11,7 @@ from typing import Optional, Tuple
 
 import torch
 
-from ._lib import P4Q_BF16, P4Q_FP16, check, lib
+from ._lib import P4Q_BF16, P4Q_ERR_INVALID_ARG, P4Q_FP16, P4QError, check, lib
 
 
 def version() -> str:
@@ -211,6 +211,80 @@ def attention_prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, B: int,
                                      _stream(q.device))
     check(st)
     return out
+
+
+# --------------------------------------------------------------------------- calibration
+def quant_scaled(z: torch.Tensor, sigma: torch.Tensor, divide: bool, clip: float = 1.0,
+                 clip_rows: Optional[torch.Tensor] = None):
+    """Channel-scaled per-row quantizer (p4q_quant_scaled): z [R, K] (row
+    stride may exceed K), sigma fp32 [K]; z' = z / sigma (divide) or z * sigma
+    -> (codes uint8 [R, K/2], scales fp32 [R], absmax fp32 [R], kstar int32 [R])."""
+    _need_gpu(z, sigma, clip_rows)
+    if z.dim() != 2 or z.stride(1) != 1:
+        raise ValueError("z must be 2-D with unit column stride")
+    R, K = z.shape
+    if sigma.shape != (K,) or sigma.dtype != torch.float32 or not sigma.is_contiguous():
+        raise ValueError("sigma must be a contiguous fp32 [K] tensor")
+    if clip_rows is not None and (clip_rows.shape != (R,) or clip_rows.dtype != torch.float32
+                                  or not clip_rows.is_contiguous()):
+        raise ValueError("clip_rows must be a contiguous fp32 [R] tensor")
+    dev = z.device
+    codes = torch.empty((R, K // 2), dtype=torch.uint8, device=dev)
+    scales = torch.empty((R,), dtype=torch.float32, device=dev)
+    absmax = torch.empty((R,), dtype=torch.float32, device=dev)
+    kstar = torch.empty((R,), dtype=torch.int32, device=dev)
+    st = lib().p4q_quant_scaled(_dtype_code(z.dtype), R, K, _ptr(z), z.stride(0), _ptr(sigma),
+                                int(bool(divide)), ctypes.c_float(clip),
+                                _ptr(clip_rows) if clip_rows is not None else None, _ptr(codes),
+                                _ptr(scales), _ptr(absmax), _ptr(kstar), _stream(dev))
+    check(st)
+    return codes, scales, absmax, kstar
+
+
+def calib_linear_workspace(M: int, N: int, K: int, device) -> torch.Tensor:
+    n = lib().p4q_calib_linear_workspace_bytes(M, N, K)
+    if n == 0:
+        raise P4QError(P4Q_ERR_INVALID_ARG, f"unsupported calibration shape M={M} N={N} K={K}")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def calib_linear_grad(x: torch.Tensor, w: torch.Tensor, target: torch.Tensor,
+                      sigma: torch.Tensor, clip_a: float, clip_w: torch.Tensor,
+                      workspace: Optional[torch.Tensor] = None, out=None):
+    """One calibration step of a W4A4 fake-quantized linear
+    (p4q_calib_linear_grad): x [M, K], w [N, K] (same dtype), target fp32
+    [M, N], sigma fp32 [K], clip_w fp32 [N] -> (loss [1], grad_sigma [K],
+    grad_clip_a [1], grad_clip_w [N]), all fp32 device tensors.  `out` may
+    hold those four tensors to be written in place."""
+    _need_gpu(x, w, target, sigma, clip_w)
+    for t, name in ((x, "x"), (w, "w"), (target, "target")):
+        if t.dim() != 2 or t.stride(1) != 1:
+            raise ValueError(f"{name} must be 2-D with unit column stride")
+    M, K = x.shape
+    N = w.shape[0]
+    if w.shape[1] != K or w.dtype != x.dtype:
+        raise ValueError("w must be [N, K] of x's dtype")
+    if target.shape != (M, N) or target.dtype != torch.float32:
+        raise ValueError("target must be fp32 [M, N]")
+    for t, n, name in ((sigma, K, "sigma"), (clip_w, N, "clip_w")):
+        if t.shape != (n,) or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous fp32 [{n}] tensor")
+    dev = x.device
+    if out is None:
+        out = (torch.empty(1, dtype=torch.float32, device=dev),
+               torch.empty(K, dtype=torch.float32, device=dev),
+               torch.empty(1, dtype=torch.float32, device=dev),
+               torch.empty(N, dtype=torch.float32, device=dev))
+    if workspace is None:
+        workspace = calib_linear_workspace(M, N, K, dev)
+    loss, gs, gca, gcw = out
+    st = lib().p4q_calib_linear_grad(_dtype_code(x.dtype), M, N, K, _ptr(x), x.stride(0), _ptr(w),
+                                     w.stride(0), _ptr(target), target.stride(0), _ptr(sigma),
+                                     ctypes.c_float(clip_a), _ptr(clip_w), _ptr(loss), _ptr(gs),
+                                     _ptr(gca), _ptr(gcw), _ptr(workspace), workspace.numel(),
+                                     _stream(dev))
+    check(st)
+    return loss, gs, gca, gcw
 
 
 # --------------------------------------------------------------------------- W4A4 linear

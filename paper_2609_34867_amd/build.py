@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 BUILD_DIR = os.path.join(REPO, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "libp4q.so")
 
-SOURCES = ["p4q_api.hip", "quant_act.hip", "prologue.hip", "select.hip", "diversity.hip",
+SOURCES = ["p4q_api.hip", "quant_act.hip", "prologue.hip", "select.hip", "diversity.hip", "calib.hip",
            "w4a4_gemm.hip", "attention.hip"]
 
 ARCH = "gfx950"

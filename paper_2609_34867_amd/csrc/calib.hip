@@ -1,0 +1,758 @@
+// Pruning-aware calibration mechanics (P4Q Sec. 3.3, Eq.
+// p4q_pruning_aware_calibration; Appendix B.3): the reconstruction loss of one
+// W4A4 fake-quantized linear on a pruned sequence and its gradients with
+// respect to the learnable diagonal channel scales sigma and the activation /
+// weight clipping factors.  Rounding passes gradients straight through; the
+// clamp passes them where the rounded quotient lies in [-8, 7]; a row's
+// maximum passes its share to its lowest-index element.
+//
+// One step, stream-ordered:
+//   1. k_quant_scaled (x2): X' = fl32(X / sigma), W' = fl32(W * sigma); per
+//      row Q4 with its clipping factor -> packed codes, scale, row maximum
+//      and the maximum's lowest index.
+//   2. k_codes_bf16t (x2): the codes transposed to bf16 [K][rows], the
+//      contraction operands of the backward products (int4 codes are exact
+//      in bf16).
+//   3. The W4A4 GEMM (int8 MFMA) -> acc[M][N] int32.
+//   4. k_calib_residual: R = fl32(fl32(fl32(acc sA) sW) - T); the bf16
+//      operands P1 = bf16(R sW) [M][N] and P2^T = bf16(R sA) [N][Mp]; partial
+//      sums of R^2.
+//   5. k_calib_bwd (x2, bf16 MFMA, fp32 accumulation): dL/dXq ~ P1 Cw and
+//      dL/dWq ~ P2^T Ca are never stored.  The epilogue recomputes each
+//      element's transformed value z' and rounding decision and reduces its
+//      tile to per-row sums of g (code - inside u) and per-column sums of
+//      g inside z' (u = z'/s).  Both are linear in g, so the contraction is
+//      split freely across work-groups, each writing its own partial slot.
+//   6. k_calib_rows: per row g_s (deterministic sum of the slots), the clip
+//      gradients, and the row maximum's share g_s clip absmax / 7, added to
+//      its column with float64 atomics.
+//   7. k_calib_cols: with colX / colW the per-column totals of both sides,
+//      d sigma_k = (2 / (M N)) (colW_k - colX_k) / sigma_k (the product
+//      X W^T is unchanged when sigma divides one side and multiplies the
+//      other); the loss and the activation clip gradient.
+// The factor 2 / (M N) of the mean squared error is applied once, at the end.
+#include "p4q_internal.h"
+#include "q4_device.h"
+
+#include <algorithm>
+
+namespace p4q {
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ uint32_t bf16_rne(float v) {
+    const uint32_t u = __float_as_uint(v);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <bool BF16>
+__device__ __forceinline__ float half_to_f32(uint16_t h) {
+    if constexpr (BF16) return __uint_as_float((uint32_t)h << 16);
+    else return (float)__builtin_bit_cast(_Float16, h);
+}
+
+// z' of one stored value: correctly rounded fp32 division (activations) or
+// product (weights)
+template <bool DIV>
+__device__ __forceinline__ float transform(float z, float sg) {
+    if constexpr (DIV) return z / sg;
+    else return __fmul_rn(z, sg);
+}
+
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o);
+        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o);
+        v = max_u64(v, ((uint64_t)hi << 32) | lo);
+    }
+    return v;
+}
+
+__device__ __forceinline__ double block_sum(double v, double *red) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    const int t = threadIdx.x;
+    if ((t & 63) == 0) red[t >> 6] = v;
+    __syncthreads();
+    double s = 0.0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) s += red[w];
+    return s;
+}
+
+// ---------------------------------------------------------------------------
+// 1. Transformed per-row quantizer.  One 256-thread work-group per row; the
+//    transformed row stays in registers (CH chunks of 8 values per thread,
+//    K <= 2048 CH).  The row maximum and its lowest index come from one
+//    64-bit maximum over (|z'| bits, ~k).
+// ---------------------------------------------------------------------------
+template <int CH, bool BF16, bool DIV>
+__global__ __launch_bounds__(kThreads) void k_quant_scaled(
+    const uint8_t *__restrict__ z, int64_t ldz_bytes, int nchunk, const float *__restrict__ sigma,
+    float clip, const float *__restrict__ clip_rows, uint8_t *__restrict__ codes,
+    int64_t ldc_bytes, float *__restrict__ scales, float *__restrict__ absmax,
+    int32_t *__restrict__ kstar) {
+    __shared__ uint64_t s_key[kThreads / 64];
+    const int row = blockIdx.x, t = threadIdx.x;
+    const uint4 *src = reinterpret_cast<const uint4 *>(z + (int64_t)row * ldz_bytes);
+    const float4 *sg4 = reinterpret_cast<const float4 *>(sigma);
+
+    float zp[CH][8];
+    uint64_t key = 0;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const int q = t + kThreads * c;
+        if (q < nchunk) {
+            const uint4 v = load_nt(src + q);
+            const float4 s0 = sg4[2 * q], s1 = sg4[2 * q + 1];
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+            const float sg[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                zp[c][2 * i] = transform<DIV>(lo_f32<BF16>(w[i]), sg[2 * i]);
+                zp[c][2 * i + 1] = transform<DIV>(hi_f32<BF16>(w[i]), sg[2 * i + 1]);
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t k = (uint32_t)(8 * q + e);
+                key = max_u64(key, ((uint64_t)__float_as_uint(__builtin_fabsf(zp[c][e])) << 32) | ~k);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) zp[c][e] = 0.0f;
+        }
+    }
+    key = wave_max_u64(key);
+    if ((t & 63) == 0) s_key[t >> 6] = key;
+    __syncthreads();
+    key = max_u64(max_u64(s_key[0], s_key[1]), max_u64(s_key[2], s_key[3]));
+    const float a = __uint_as_float((uint32_t)(key >> 32));
+    const float cl = clip_rows ? clip_rows[row] : clip;
+    const float s = __fmul_rn(cl, a) / 7.0f;
+    if (t == 0) {
+        scales[row] = s;
+        if (absmax) absmax[row] = a;
+        if (kstar) kstar[row] = (int32_t)~(uint32_t)key;
+    }
+
+    uint32_t *dst = reinterpret_cast<uint32_t *>(codes + (int64_t)row * ldc_bytes);
+    const bool tiny = !(s >= kTinyScale);
+    const float r = tiny ? 0.0f : 1.0f / s;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const int q = t + kThreads * c;
+        uint32_t packed = 0u;
+        if (s != 0.0f) {
+            uint32_t w[8];
+            float fm = 0.0f;
+            if (!tiny) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    float tq = __builtin_fmaf(zp[c][e], r, kRneMagic);
+                    const float qq = tq - kRneMagic;
+                    fm = __builtin_fmaxf(fm, __builtin_fabsf(__builtin_fmaf(zp[c][e], r, -qq)));
+                    tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
+                    w[e] = __float_as_uint(tq);
+                }
+            }
+            // a value within 2^-19 of a rounding boundary somewhere in the
+            // wave (or a tiny scale): this chunk by exact division
+            if (tiny || __any(fm > kNearHalf)) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) w[e] = q4_exact(zp[c][e], s);
+            }
+            packed = pack_nibbles(w);
+        }
+        if (q < nchunk) dst[q] = packed;
+    }
+}
+
+template <int CH, bool BF16, bool DIV>
+hipError_t launch_qs(int R, int nchunk, const void *z, int64_t ldz_bytes, const float *sigma,
+                     float clip, const float *clip_rows, uint8_t *codes, int64_t ldc_bytes,
+                     float *scales, float *absmax, int32_t *kstar, hipStream_t stream) {
+    hipLaunchKernelGGL((k_quant_scaled<CH, BF16, DIV>), dim3(R), dim3(kThreads), 0, stream,
+                       static_cast<const uint8_t *>(z), ldz_bytes, nchunk, sigma, clip, clip_rows,
+                       codes, ldc_bytes, scales, absmax, kstar);
+    return hipGetLastError();
+}
+
+template <bool BF16, bool DIV>
+hipError_t launch_qs_typed(int R, int K, const void *z, int64_t ldz, const float *sigma,
+                           float clip, const float *clip_rows, uint8_t *codes, float *scales,
+                           float *absmax, int32_t *kstar, hipStream_t stream) {
+    const int nchunk = K / 8;
+    const int per = (nchunk + kThreads - 1) / kThreads;      // <= 8 (K <= 16384)
+#define P4Q_QS(N)                                                                          \
+    return launch_qs<N, BF16, DIV>(R, nchunk, z, ldz * 2, sigma, clip, clip_rows, codes,  \
+                                   K / 2, scales, absmax, kstar, stream)
+    if (per <= 1) P4Q_QS(1);
+    if (per <= 2) P4Q_QS(2);
+    if (per <= 4) P4Q_QS(4);
+    if (per <= 6) P4Q_QS(6);
+    P4Q_QS(8);
+#undef P4Q_QS
+}
+
+// ---------------------------------------------------------------------------
+// 2. Packed codes [R][K/2] -> bf16 [K][ldo], rows R..ldo-1 of the output's
+//    columns zero.  64 (rows) x 128 (k) tiles through LDS as int8.
+// ---------------------------------------------------------------------------
+constexpr int kT8Stride = 132;        // bytes per LDS row: rows 32 apart land 32 banks apart
+
+__global__ __launch_bounds__(kThreads) void k_codes_bf16t(const uint8_t *__restrict__ codes,
+                                                          int R, int Kb,
+                                                          uint16_t *__restrict__ out,
+                                                          int64_t ldo) {
+    __shared__ __attribute__((aligned(16))) uint8_t s8[64 * kT8Stride];
+    const int t = threadIdx.x;
+    const int r0 = blockIdx.x * 64, k0 = blockIdx.y * 128;
+    {
+        const int rl = t >> 2, c = t & 3, r = r0 + rl;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (r < R) v = *reinterpret_cast<const uint4 *>(codes + (int64_t)r * Kb + k0 / 2 + 16 * c);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        uint32_t *d = reinterpret_cast<uint32_t *>(s8 + rl * kT8Stride + 32 * c);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            // nibbles k = 8i .. 8i+7 -> sign-extended bytes, k order
+            uint32_t o[2] = {0u, 0u};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int nib = (int)((w[i] >> (4 * e)) & 0xFu);
+                const uint32_t b = (uint32_t)(uint8_t)(int8_t)((nib ^ 8) - 8);
+                o[e >> 2] |= b << (8 * (e & 3));
+            }
+            d[2 * i] = o[0];
+            d[2 * i + 1] = o[1];
+        }
+    }
+    __syncthreads();
+    {
+        const int kl = t >> 1, h = t & 1;
+        uint32_t pk[16];
+#pragma unroll
+        for (int e = 0; e < 32; e += 2) {
+            const float a = (float)(int8_t)s8[(32 * h + e) * kT8Stride + kl];
+            const float b = (float)(int8_t)s8[(32 * h + e + 1) * kT8Stride + kl];
+            pk[e >> 1] = (__float_as_uint(a) >> 16) | (__float_as_uint(b) & 0xFFFF0000u);
+        }
+        uint4 *dst = reinterpret_cast<uint4 *>(out + (int64_t)(k0 + kl) * ldo + r0 + 32 * h);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            dst[q] = make_uint4(pk[4 * q], pk[4 * q + 1], pk[4 * q + 2], pk[4 * q + 3]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 4. Residual, bf16 contraction operands and loss partials.  64 x 64 tiles;
+//    grid (N / 64, Mp / 64).  The grid also clears the float64 scatter
+//    targets of k_calib_rows.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_calib_residual(
+    const int32_t *__restrict__ acc, const float *__restrict__ sa, const float *__restrict__ sw,
+    const float *__restrict__ T, int64_t ldt, int M, int N, int Mp, uint16_t *__restrict__ P1,
+    uint16_t *__restrict__ P2T, double *__restrict__ loss_part, double *__restrict__ corr,
+    int ncorr) {
+    __shared__ __attribute__((aligned(16))) uint16_t tr[64 * 72];   // [n][m] bf16(R sA)
+    __shared__ double red[kThreads / 64];
+    const int t = threadIdx.x;
+    const int n0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
+    const int bid = blockIdx.y * gridDim.x + blockIdx.x;
+    const int nb = gridDim.x * gridDim.y;
+    for (int i = bid * kThreads + t; i < ncorr; i += nb * kThreads) corr[i] = 0.0;
+
+    const int cn = 4 * (t & 15);
+    const float4 swv = *reinterpret_cast<const float4 *>(sw + n0 + cn);
+    const float swa[4] = {swv.x, swv.y, swv.z, swv.w};
+    double l2 = 0.0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int ml = (t >> 4) + 16 * i, m = m0 + ml;
+        if (m < M) {
+            const int4 a = *reinterpret_cast<const int4 *>(acc + (int64_t)m * N + n0 + cn);
+            const float4 tv = *reinterpret_cast<const float4 *>(T + (int64_t)m * ldt + n0 + cn);
+            const int av[4] = {a.x, a.y, a.z, a.w};
+            const float ta[4] = {tv.x, tv.y, tv.z, tv.w};
+            const float s = sa[m];
+            uint32_t p[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float y = __fmul_rn(__fmul_rn((float)av[e], s), swa[e]);
+                const float r = __fsub_rn(y, ta[e]);
+                l2 += (double)r * (double)r;
+                p[e] = bf16_rne(__fmul_rn(r, swa[e]));
+                tr[(cn + e) * 72 + ml] = (uint16_t)bf16_rne(__fmul_rn(r, s));
+            }
+            *reinterpret_cast<uint2 *>(P1 + (int64_t)m * N + n0 + cn) =
+                make_uint2(p[0] | (p[1] << 16), p[2] | (p[3] << 16));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) tr[(cn + e) * 72 + ml] = 0;
+        }
+    }
+    __syncthreads();
+    {
+        const int nl = t >> 2, c = t & 3;
+        const uint4 *sp = reinterpret_cast<const uint4 *>(tr + nl * 72 + 16 * c);
+        uint4 *dp = reinterpret_cast<uint4 *>(P2T + (int64_t)(n0 + nl) * Mp + m0 + 16 * c);
+        dp[0] = sp[0];
+        dp[1] = sp[1];
+    }
+    const double s = block_sum(l2, red);
+    if (t == 0) loss_part[bid] = s;
+}
+
+// ---------------------------------------------------------------------------
+// 5. Backward contraction O[i][k] = sum_j P[i][j] C[k][j] (bf16 operands,
+//    fp32 accumulation on v_mfma_f32_32x32x16_bf16) with the fused reduction
+//    epilogue.  128 x 128 tiles, 4 wavefronts of 64 x 64 (2 x 2 MFMA tiles),
+//    64 j per stage, two LDS stages filled by buffer_load ... lds (rows past
+//    I read as zeros).  LDS rows are 128 bytes; 16-byte chunk c of row r sits
+//    at chunk c ^ ((r >> 1) & 7), so the 16 rows one fragment read touches
+//    hit distinct banks.
+//    grid (Kd / 128, ceil(I / 128), splits); split z covers j in
+//    [z js, min(J, (z + 1) js)).  Outputs: rowpart[(kt splits + z) I + i],
+//    colpart[(it splits + z) Kd + k].
+// ---------------------------------------------------------------------------
+constexpr int BB = 128;
+constexpr int BJ = 64;
+constexpr int kHalfStage = BB * BJ * 2;        // 16 KB: one operand
+constexpr int kStage = 2 * kHalfStage;
+constexpr int kZStride = 288;                  // bytes per row of the epilogue's Z tile
+
+__device__ __forceinline__ v4i buffer_rsrc(const void *base, uint32_t bytes) {
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    return v4i{(int)(uint32_t)b, (int)((b >> 32) & 0xFFFFu), (int)bytes, 0x00020000};
+}
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(v4i desc, uint32_t voffset, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voffset), "s"(desc), "s"(lds)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ v16f mfma_bf16(uint4 a, uint4 b, v16f c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, a),
+                                                   __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
+}
+
+template <bool BF16, bool DIV>
+__global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
+    const uint16_t *__restrict__ P, int64_t ldp, const uint16_t *__restrict__ C, int64_t ldc,
+    int I, int J, int js, const uint16_t *__restrict__ Z, int64_t ldz,
+    const float *__restrict__ sigma, const float *__restrict__ srow, int Kd,
+    float *__restrict__ rowpart, float *__restrict__ colpart) {
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * kStage];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int wi = wave >> 1, wk = wave & 1;
+    const int kt = blockIdx.x, it = blockIdx.y, split = blockIdx.z, nsplit = gridDim.z;
+    const int i0 = it * BB, k0 = kt * BB;
+    const int jb = split * js;
+    const int nst = max(0, min(J - jb, js)) / BJ;
+
+    const v4i dP = buffer_rsrc(P + (int64_t)i0 * ldp, (uint32_t)(min(I - i0, BB) * ldp * 2));
+    const v4i dC = buffer_rsrc(C + (int64_t)k0 * ldc, (uint32_t)(BB * ldc * 2));
+    // DMA: one 1 KB instruction fills 8 LDS rows; lane L -> row +L/8, slot
+    // L%8, which holds chunk (L%8) ^ ((row >> 1) & 7).  Wave w copies rows
+    // [32w, 32w + 32) of both operands.
+    uint32_t voP[4], voC[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        const int row = 32 * wave + 8 * n + (lane >> 3);
+        const uint32_t lc = (uint32_t)((lane & 7) ^ ((row >> 1) & 7));
+        voP[n] = (uint32_t)(row * ldp * 2) + lc * 16u;
+        voC[n] = (uint32_t)(row * ldc * 2) + lc * 16u;
+    }
+    const uint32_t lds0 = (uint32_t)(size_t)(lds_ptr_t)smem +
+                          (uint32_t)__builtin_amdgcn_readfirstlane(wave) * 32u * 128u;
+    auto issue = [&](int slot, int st) __attribute__((always_inline)) {
+        const uint32_t jo = (uint32_t)(jb + st * BJ) * 2u;
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            lds_dma16(dP, voP[n] + jo, lds0 + slot * kStage + n * 1024);
+            lds_dma16(dC, voC[n] + jo, lds0 + slot * kStage + kHalfStage + n * 1024);
+        }
+    };
+
+    v16f acc[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[x][y][e] = 0.0f;
+
+    // fragment rows: A (P) rows wi*64 + 32x + l%32, B (C) rows wk*64 + 32y + l%32
+    const int r32 = lane & 31, g2 = lane >> 5;
+    uint32_t fa[2], fb[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        fa[x] = (uint32_t)((wi * 64 + 32 * x + r32) * 128);
+        fb[x] = (uint32_t)(kHalfStage + (wk * 64 + 32 * x + r32) * 128);
+    }
+    const uint32_t swz = (uint32_t)(((wi * 64 + r32) >> 1) & 7);    // same for x = 0, 1 and for B
+    if (nst > 0) issue(0, 0);
+    for (int st = 0; st < nst; ++st) {
+        // stage st has landed from every wave, and every wave is done with
+        // stage st - 1, whose slot the next DMA overwrites
+        asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+        if (st + 1 < nst) issue((st + 1) & 1, st + 1);
+        const uint8_t *base = smem + (st & 1) * kStage;
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+            const uint32_t ch = (((uint32_t)(2 * s4 + g2)) ^ swz) * 16u;
+            uint4 a[2], b[2];
+#pragma unroll
+            for (int x = 0; x < 2; ++x) {
+                a[x] = *reinterpret_cast<const uint4 *>(base + fa[x] + ch);
+                b[x] = *reinterpret_cast<const uint4 *>(base + fb[x] + ch);
+            }
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y) acc[x][y] = mfma_bf16(a[x], b[y], acc[x][y]);
+        }
+    }
+
+    // ---- epilogue: Z tile, row scales and sigma to LDS ----
+    __syncthreads();
+    uint8_t *zs = smem;
+    float *s_s = reinterpret_cast<float *>(smem + BB * kZStride);    // row scale
+    float *s_r = s_s + BB;                                           // 1 / scale (0: exact path)
+    float *s_g = s_r + BB;                                           // sigma of the tile's columns
+    float *rowred = s_g + BB;                                        // [2][128]
+    float *colred = rowred + 2 * BB;                                 // [2][128]
+    for (int c = t; c < BB * 16; c += kThreads) {
+        const int r = c >> 4, q = c & 15, i = i0 + r;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (i < I) v = *reinterpret_cast<const uint4 *>(Z + (int64_t)i * ldz + k0 + 8 * q);
+        *reinterpret_cast<uint4 *>(zs + r * kZStride + 16 * q) = v;
+    }
+    if (t < BB) {
+        const float s = (i0 + t < I) ? srow[i0 + t] : 0.0f;
+        s_s[t] = s;
+        s_r[t] = (s >= kTinyScale) ? 1.0f / s : 0.0f;
+        s_g[t] = sigma[k0 + t];
+    }
+    __syncthreads();
+
+    float rowv[32];
+#pragma unroll
+    for (int v = 0; v < 32; ++v) rowv[v] = 0.0f;
+    float colv[2] = {0.0f, 0.0f};
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+        const int kl = wk * 64 + 32 * y + r32;
+        const float sg = s_g[kl];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int il = wi * 64 + 32 * x + 8 * (e >> 2) + 4 * g2 + (e & 3);
+                const float g = acc[x][y][e];
+                const float zf = half_to_f32<BF16>(
+                    *reinterpret_cast<const uint16_t *>(zs + il * kZStride + 2 * kl));
+                const float zp = transform<DIV>(zf, sg);
+                const float s = s_s[il], rs = s_r[il];
+                float rc = 0.0f, cc = 0.0f;
+                if (s != 0.0f) {
+                    float u = 0.0f, rho = 0.0f;
+                    bool exact = (rs == 0.0f);
+                    if (!exact) {
+                        const float tq = __builtin_fmaf(zp, rs, kRneMagic);
+                        rho = tq - kRneMagic;
+                        u = zp * rs;
+                        exact = __builtin_fabsf(__builtin_fmaf(zp, rs, -rho)) > kNearHalf;
+                    }
+                    if (exact) {
+                        u = zp / s;
+                        rho = __builtin_rintf(u);
+                    }
+                    const bool inside = (rho >= -8.0f) && (rho <= 7.0f);
+                    const float q = __builtin_amdgcn_fmed3f(rho, -8.0f, 7.0f);
+                    rc = g * (inside ? q - u : q);
+                    cc = inside ? g * zp : 0.0f;
+                }
+                rowv[16 * x + e] += rc;
+                colv[y] += cc;
+            }
+        }
+    }
+    // rows: the 32 values of each half-wave summed over its 32 lanes by a
+    // halving exchange; lane l ends with value index l % 32
+#pragma unroll
+    for (int m = 16; m >= 1; m >>= 1) {
+        const bool up = (lane & m) != 0;
+#pragma unroll
+        for (int v = 0; v < m; ++v) {
+            const float send = up ? rowv[v] : rowv[v + m];
+            const float keep = up ? rowv[v + m] : rowv[v];
+            rowv[v] = keep + __shfl_xor(send, m);
+        }
+    }
+    {
+        const int v = r32, x = v >> 4, e = v & 15;
+        const int il = wi * 64 + 32 * x + 8 * (e >> 2) + 4 * g2 + (e & 3);
+        rowred[wk * BB + il] = rowv[0];
+    }
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+        const float c = colv[y] + __shfl_xor(colv[y], 32);
+        if (g2 == 0) colred[wi * BB + wk * 64 + 32 * y + r32] = c;
+    }
+    __syncthreads();
+    if (t < BB) {
+        if (i0 + t < I)
+            rowpart[((int64_t)kt * nsplit + split) * I + i0 + t] = rowred[t] + rowred[BB + t];
+    } else {
+        const int k = t - BB;
+        colpart[((int64_t)it * nsplit + split) * Kd + k0 + k] = colred[k] + colred[BB + k];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 6. Rows: g_s, clip gradients, the row maximum's share scattered to its
+//    column.  Blocks [0, nbA) hold activation rows, the rest weight rows.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_calib_rows(
+    const float *__restrict__ rowA, int nsA, int M, const float *__restrict__ sA,
+    const float *__restrict__ aA, const int32_t *__restrict__ kA, float clip_a,
+    const float *__restrict__ rowW, int nsW, int N, const float *__restrict__ sW,
+    const float *__restrict__ aW, const int32_t *__restrict__ kW,
+    const float *__restrict__ clip_w, int nbA, double scale, double *__restrict__ corrA,
+    double *__restrict__ corrW, double *__restrict__ dclipa_part,
+    float *__restrict__ grad_clip_w) {
+    __shared__ double red[kThreads / 64];
+    const int t = threadIdx.x;
+    if ((int)blockIdx.x < nbA) {
+        const int m = blockIdx.x * kThreads + t;
+        double part = 0.0;
+        if (m < M) {
+            double gs = 0.0;
+            for (int s = 0; s < nsA; ++s) gs += (double)rowA[(int64_t)s * M + m];
+            const double a = (double)aA[m];
+            if (sA[m] != 0.0f) atomicAdd(&corrA[kA[m]], gs * (double)clip_a * a / 7.0);
+            part = gs * a / 7.0;
+        }
+        const double s = block_sum(part, red);
+        if (t == 0) dclipa_part[blockIdx.x] = s;
+    } else {
+        const int n = (blockIdx.x - nbA) * kThreads + t;
+        if (n < N) {
+            double gs = 0.0;
+            for (int s = 0; s < nsW; ++s) gs += (double)rowW[(int64_t)s * N + n];
+            const double a = (double)aW[n];
+            if (sW[n] != 0.0f) atomicAdd(&corrW[kW[n]], gs * (double)clip_w[n] * a / 7.0);
+            grad_clip_w[n] = (float)(scale * gs * a / 7.0);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 7. Columns: d sigma; block 0 also reduces the loss and d clip_a (fixed
+//    order).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_calib_cols(
+    const float *__restrict__ colA, int nslA, const float *__restrict__ colW, int nslW,
+    const double *__restrict__ corrA, const double *__restrict__ corrW,
+    const float *__restrict__ sigma, int K, double scale, float *__restrict__ grad_sigma,
+    const double *__restrict__ loss_part, int nloss, double inv_mn, float *__restrict__ loss,
+    const double *__restrict__ dclipa_part, int nbA, float *__restrict__ grad_clip_a) {
+    __shared__ double red[kThreads / 64];
+    const int t = threadIdx.x;
+    const int k = blockIdx.x * kThreads + t;
+    if (k < K) {
+        double cx = corrA[k], cw = corrW[k];
+        for (int s = 0; s < nslA; ++s) cx += (double)colA[(int64_t)s * K + k];
+        for (int s = 0; s < nslW; ++s) cw += (double)colW[(int64_t)s * K + k];
+        grad_sigma[k] = (float)(scale * (cw - cx) / (double)sigma[k]);
+    }
+    if (blockIdx.x == 0) {
+        double l = 0.0;
+        for (int i = t; i < nloss; i += kThreads) l += loss_part[i];
+        l = block_sum(l, red);
+        __syncthreads();
+        double c = 0.0;
+        for (int i = t; i < nbA; i += kThreads) c += dclipa_part[i];
+        c = block_sum(c, red);
+        if (t == 0) {
+            loss[0] = (float)(l * inv_mn);
+            grad_clip_a[0] = (float)(scale * c);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+inline size_t up256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+struct CalibPlan {
+    int Mp, nsA, jsA, nsW, jsW, nbA, nloss, tilesMA, tilesNW;
+};
+
+CalibPlan calib_plan(int M, int N, int K) {
+    CalibPlan p;
+    p.Mp = (M + 63) / 64 * 64;
+    const int kt = K / BB;
+    p.tilesMA = (M + BB - 1) / BB;
+    p.tilesNW = (N + BB - 1) / BB;
+    auto splits = [](int tiles, int J, int &ns, int &js) {
+        // about two work-groups per CU of 256, at least 4 stages per split
+        int want = (512 + tiles - 1) / tiles;
+        want = std::max(1, std::min(want, J / (4 * BJ)));
+        js = ((J + want - 1) / want + BJ - 1) / BJ * BJ;
+        ns = (J + js - 1) / js;
+    };
+    splits(p.tilesMA * kt, N, p.nsA, p.jsA);
+    splits(p.tilesNW * kt, p.Mp, p.nsW, p.jsW);
+    p.nbA = (M + kThreads - 1) / kThreads;
+    p.nloss = (N / 64) * (p.Mp / 64);
+    return p;
+}
+
+struct CalibWs {
+    uint8_t *codesA, *codesW;
+    float *sA, *aA, *sW, *aW;
+    int32_t *kA, *kW;
+    uint16_t *CaT, *CwT, *P1, *P2T;
+    int32_t *acc;
+    double *loss_part, *corr, *dclipa_part;
+    float *rowA, *colA, *rowW, *colW;
+};
+
+size_t calib_carve(const CalibPlan &p, int M, int N, int K, uint8_t *base, CalibWs *w) {
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        uint8_t *q = base ? base + off : nullptr;
+        off += up256(bytes);
+        return q;
+    };
+    const int kt = K / BB;
+    CalibWs c;
+    c.codesA = take((size_t)M * K / 2);
+    c.codesW = take((size_t)N * K / 2);
+    c.sA = reinterpret_cast<float *>(take((size_t)M * 4));
+    c.aA = reinterpret_cast<float *>(take((size_t)M * 4));
+    c.kA = reinterpret_cast<int32_t *>(take((size_t)M * 4));
+    c.sW = reinterpret_cast<float *>(take((size_t)N * 4));
+    c.aW = reinterpret_cast<float *>(take((size_t)N * 4));
+    c.kW = reinterpret_cast<int32_t *>(take((size_t)N * 4));
+    c.CaT = reinterpret_cast<uint16_t *>(take((size_t)K * p.Mp * 2));
+    c.CwT = reinterpret_cast<uint16_t *>(take((size_t)K * N * 2));
+    c.acc = reinterpret_cast<int32_t *>(take((size_t)M * N * 4));
+    c.P1 = reinterpret_cast<uint16_t *>(take((size_t)M * N * 2));
+    c.P2T = reinterpret_cast<uint16_t *>(take((size_t)N * p.Mp * 2));
+    c.loss_part = reinterpret_cast<double *>(take((size_t)p.nloss * 8));
+    c.corr = reinterpret_cast<double *>(take((size_t)2 * K * 8));
+    c.dclipa_part = reinterpret_cast<double *>(take((size_t)p.nbA * 8));
+    c.rowA = reinterpret_cast<float *>(take((size_t)kt * p.nsA * M * 4));
+    c.colA = reinterpret_cast<float *>(take((size_t)p.tilesMA * p.nsA * K * 4));
+    c.rowW = reinterpret_cast<float *>(take((size_t)kt * p.nsW * N * 4));
+    c.colW = reinterpret_cast<float *>(take((size_t)p.tilesNW * p.nsW * K * 4));
+    if (w) *w = c;
+    return off;
+}
+
+template <bool BF16>
+hipError_t calib_typed(int M, int N, int K, const void *x, int64_t ldx, const void *w,
+                       int64_t ldw, const float *target, int64_t ldt, const float *sigma,
+                       float clip_a, const float *clip_w, float *loss, float *grad_sigma,
+                       float *grad_clip_a, float *grad_clip_w, void *ws, hipStream_t stream) {
+    const CalibPlan p = calib_plan(M, N, K);
+    CalibWs c;
+    calib_carve(p, M, N, K, static_cast<uint8_t *>(ws), &c);
+    hipError_t e;
+    // 1. transformed quantizers
+    if ((e = launch_qs_typed<BF16, true>(M, K, x, ldx, sigma, clip_a, nullptr, c.codesA, c.sA,
+                                         c.aA, c.kA, stream)) != hipSuccess)
+        return e;
+    if ((e = launch_qs_typed<BF16, false>(N, K, w, ldw, sigma, 1.0f, clip_w, c.codesW, c.sW,
+                                          c.aW, c.kW, stream)) != hipSuccess)
+        return e;
+    // 2. transposed bf16 codes
+    hipLaunchKernelGGL(k_codes_bf16t, dim3(p.Mp / 64, K / 128), dim3(kThreads), 0, stream,
+                       c.codesA, M, K / 2, c.CaT, (int64_t)p.Mp);
+    hipLaunchKernelGGL(k_codes_bf16t, dim3(N / 64, K / 128), dim3(kThreads), 0, stream,
+                       c.codesW, N, K / 2, c.CwT, (int64_t)N);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // 3. forward W4A4 GEMM (its bf16 output lands in P1, rewritten below)
+    if ((e = launch_w4a4_gemm(M, N, K, c.codesA, c.sA, c.codesW, c.sW, P4Q_BF16, c.P1, N, c.acc,
+                              nullptr, 0, stream)) != hipSuccess)
+        return e;
+    // 4. residual
+    hipLaunchKernelGGL(k_calib_residual, dim3(N / 64, p.Mp / 64), dim3(kThreads), 0, stream,
+                       c.acc, c.sA, c.sW, target, ldt, M, N, p.Mp, c.P1, c.P2T, c.loss_part,
+                       c.corr, 2 * K);
+    // 5. backward contractions with fused reductions
+    hipLaunchKernelGGL((k_calib_bwd<BF16, true>), dim3(K / BB, p.tilesMA, p.nsA),
+                       dim3(kThreads), 0, stream, c.P1, (int64_t)N, c.CwT, (int64_t)N, M, N,
+                       p.jsA, static_cast<const uint16_t *>(x), ldx, sigma, c.sA, K, c.rowA,
+                       c.colA);
+    hipLaunchKernelGGL((k_calib_bwd<BF16, false>), dim3(K / BB, p.tilesNW, p.nsW),
+                       dim3(kThreads), 0, stream, c.P2T, (int64_t)p.Mp, c.CaT, (int64_t)p.Mp, N,
+                       p.Mp, p.jsW, static_cast<const uint16_t *>(w), ldw, sigma, c.sW, K,
+                       c.rowW, c.colW);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // 6-7. finish
+    const double scale = 2.0 / ((double)M * (double)N);
+    const int nbW = (N + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(k_calib_rows, dim3(p.nbA + nbW), dim3(kThreads), 0, stream, c.rowA,
+                       (K / BB) * p.nsA, M, c.sA, c.aA, c.kA, clip_a, c.rowW, (K / BB) * p.nsW,
+                       N, c.sW, c.aW, c.kW, clip_w, p.nbA, scale, c.corr, c.corr + K,
+                       c.dclipa_part, grad_clip_w);
+    hipLaunchKernelGGL(k_calib_cols, dim3((K + kThreads - 1) / kThreads), dim3(kThreads), 0,
+                       stream, c.colA, p.tilesMA * p.nsA, c.colW, p.tilesNW * p.nsW, c.corr,
+                       c.corr + K, sigma, K, scale, grad_sigma, c.loss_part, p.nloss,
+                       1.0 / ((double)M * (double)N), loss, c.dclipa_part, p.nbA, grad_clip_a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_quant_scaled(p4q_dtype dt, int R, int K, const void *z, int64_t ldz,
+                               const float *sigma, int divide, float clip, const float *clip_rows,
+                               uint8_t *codes, float *scales, float *absmax, int32_t *kstar,
+                               hipStream_t stream) {
+    if (dt == P4Q_BF16)
+        return divide ? launch_qs_typed<true, true>(R, K, z, ldz, sigma, clip, clip_rows, codes,
+                                                    scales, absmax, kstar, stream)
+                      : launch_qs_typed<true, false>(R, K, z, ldz, sigma, clip, clip_rows, codes,
+                                                     scales, absmax, kstar, stream);
+    return divide ? launch_qs_typed<false, true>(R, K, z, ldz, sigma, clip, clip_rows, codes,
+                                                 scales, absmax, kstar, stream)
+                  : launch_qs_typed<false, false>(R, K, z, ldz, sigma, clip, clip_rows, codes,
+                                                  scales, absmax, kstar, stream);
+}
+
+size_t calib_linear_workspace_bytes(int M, int N, int K) {
+    return calib_carve(calib_plan(M, N, K), M, N, K, nullptr, nullptr);
+}
+
+hipError_t launch_calib_linear(p4q_dtype dt, int M, int N, int K, const void *x, int64_t ldx,
+                               const void *w, int64_t ldw, const float *target, int64_t ldt,
+                               const float *sigma, float clip_a, const float *clip_w,
+                               float *loss, float *grad_sigma, float *grad_clip_a,
+                               float *grad_clip_w, void *ws, hipStream_t stream) {
+    if (dt == P4Q_BF16)
+        return calib_typed<true>(M, N, K, x, ldx, w, ldw, target, ldt, sigma, clip_a, clip_w,
+                                 loss, grad_sigma, grad_clip_a, grad_clip_w, ws, stream);
+    return calib_typed<false>(M, N, K, x, ldx, w, ldw, target, ldt, sigma, clip_a, clip_w, loss,
+                              grad_sigma, grad_clip_a, grad_clip_w, ws, stream);
+}
+
+}  // namespace p4q

@@ -223,4 +223,69 @@ int p4q_w4a4_linear(int M, int N_out, int K_in, const uint8_t *a_codes, const fl
                       "p4q_w4a4_linear");
 }
 
+int p4q_quant_scaled(p4q_dtype dt, int R, int K, const void *z, int64_t ldz, const float *sigma,
+                     int divide, float clip, const float *clip_rows, uint8_t *codes,
+                     float *scales, float *absmax, int32_t *kstar, hipStream_t stream) {
+    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_quant_scaled: dtype %d", (int)dt);
+    if (R <= 0 || K <= 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_scaled: R=%d K=%d", R, K);
+    if (K % 32 != 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_scaled: K=%d not a multiple of 32", K);
+    if (K > 16384) return fail(P4Q_ERR_UNSUPPORTED, "p4q_quant_scaled: K=%d > 16384", K);
+    if (ldz < K || ldz % 8 != 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_scaled: ldz=%lld (need >= K, multiple of 8)", (long long)ldz);
+    if (divide != 0 && divide != 1) return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_scaled: divide=%d", divide);
+    if (!clip_rows && !(clip > 0.0f && clip <= 1.0f))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_scaled: clip=%g outside (0, 1]", (double)clip);
+    if (!z || !sigma || !codes || !scales) return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_scaled: null pointer");
+    if (!aligned(z, 16) || !aligned(sigma, 16) || !aligned(codes, 16) || !aligned(scales, 4) ||
+        (clip_rows && !aligned(clip_rows, 4)) || (absmax && !aligned(absmax, 4)) || (kstar && !aligned(kstar, 4)))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_quant_scaled: misaligned pointer");
+    return hip_status(p4q::launch_quant_scaled(dt, R, K, z, ldz, sigma, divide, clip, clip_rows, codes,
+                                               scales, absmax, kstar, stream),
+                      "p4q_quant_scaled");
+}
+
+static int calib_shape_error(int M, int N, int K) {
+    if (M <= 0 || N <= 0 || K <= 0) return P4Q_ERR_INVALID_ARG;
+    if (N % 64 != 0 || K % 128 != 0) return P4Q_ERR_INVALID_ARG;
+    if (K > 16384 || M > (1 << 20) || N > (1 << 20) || (int64_t)M * N > (1LL << 31) ||
+        (int64_t)N * K > (1LL << 31))
+        return P4Q_ERR_UNSUPPORTED;
+    return P4Q_OK;
+}
+
+size_t p4q_calib_linear_workspace_bytes(int M, int N, int K) {
+    if (calib_shape_error(M, N, K) != P4Q_OK) return 0;
+    return p4q::calib_linear_workspace_bytes(M, N, K);
+}
+
+int p4q_calib_linear_grad(p4q_dtype dt, int M, int N, int K, const void *x, int64_t ldx,
+                          const void *w, int64_t ldw, const float *target, int64_t ldt,
+                          const float *sigma, float clip_a, const float *clip_w, float *loss,
+                          float *grad_sigma, float *grad_clip_a, float *grad_clip_w, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_calib_linear_grad: dtype %d", (int)dt);
+    const int se = calib_shape_error(M, N, K);
+    if (se != P4Q_OK)
+        return fail(se, "p4q_calib_linear_grad: M=%d N=%d K=%d (need N %% 64 == 0, K %% 128 == 0, "
+                    "K <= 16384, M*N and N*K < 2^31)", M, N, K);
+    if (ldx < K || ldx % 8 != 0 || ldw < K || ldw % 8 != 0 || ldt < N || ldt % 4 != 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_linear_grad: ldx=%lld ldw=%lld ldt=%lld",
+                    (long long)ldx, (long long)ldw, (long long)ldt);
+    if (!(clip_a > 0.0f && clip_a <= 1.0f))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_linear_grad: clip_a=%g outside (0, 1]", (double)clip_a);
+    if (!x || !w || !target || !sigma || !clip_w || !loss || !grad_sigma || !grad_clip_a || !grad_clip_w)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_linear_grad: null pointer");
+    if (!aligned(x, 16) || !aligned(w, 16) || !aligned(target, 16) || !aligned(sigma, 16) ||
+        !aligned(clip_w, 4) || !aligned(loss, 4) || !aligned(grad_sigma, 4) ||
+        !aligned(grad_clip_a, 4) || !aligned(grad_clip_w, 4) || (ws && !aligned(ws, 256)))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_linear_grad: misaligned pointer");
+    const size_t need = p4q::calib_linear_workspace_bytes(M, N, K);
+    if (!ws || ws_bytes < need)
+        return fail(P4Q_ERR_WORKSPACE, "p4q_calib_linear_grad: workspace %zu < %zu bytes", ws_bytes, need);
+    return hip_status(p4q::launch_calib_linear(dt, M, N, K, x, ldx, w, ldw, target, ldt, sigma, clip_a,
+                                               clip_w, loss, grad_sigma, grad_clip_a, grad_clip_w, ws,
+                                               stream),
+                      "p4q_calib_linear_grad");
+}
+
 }  // extern "C"

@@ -66,6 +66,18 @@ hipError_t launch_diversity(int B, int N, int K, int n0, int kd, const int32_t *
                             const float *cls_attn, int64_t *mp, int32_t *mq, int32_t *stages,
                             int32_t *idx_out, hipStream_t stream);
 
+// ---- calibration mechanics (calib.hip) ---------------------------------------
+hipError_t launch_quant_scaled(p4q_dtype dt, int R, int K, const void *z, int64_t ldz,
+                               const float *sigma, int divide, float clip, const float *clip_rows,
+                               uint8_t *codes, float *scales, float *absmax, int32_t *kstar,
+                               hipStream_t stream);
+size_t calib_linear_workspace_bytes(int M, int N, int K);
+hipError_t launch_calib_linear(p4q_dtype dt, int M, int N, int K, const void *x, int64_t ldx,
+                               const void *w, int64_t ldw, const float *target, int64_t ldt,
+                               const float *sigma, float clip_a, const float *clip_w,
+                               float *loss, float *grad_sigma, float *grad_clip_a,
+                               float *grad_clip_w, void *ws, hipStream_t stream);
+
 // ---- W4A4 GEMM ---------------------------------------------------------------
 // G_b = C_b C_b^T for b < B, C_b = codes + b * n * (k/2) packed [n, k/2];
 // G int32 [B][n][n].

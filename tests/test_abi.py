@@ -229,6 +229,77 @@ def test_linear_validation(kw, status):
     assert linear(**kw) == status
 
 
+def qscaled(**kw):
+    a = dict(dt=0, R=4, K=64, z=ALIGNED, ldz=64, sigma=ALIGNED, divide=1, clip=1.0, clip_rows=None,
+             codes=ALIGNED, scales=ALIGNED, absmax=None, kstar=None)
+    a.update(kw)
+    return L.lib().p4q_quant_scaled(a["dt"], a["R"], a["K"], a["z"], a["ldz"], a["sigma"],
+                                    a["divide"], ctypes.c_float(a["clip"]), a["clip_rows"],
+                                    a["codes"], a["scales"], a["absmax"], a["kstar"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(R=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=48), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=16384 + 32, ldz=16384 + 32), L.P4Q_ERR_UNSUPPORTED),
+    (dict(ldz=60), L.P4Q_ERR_INVALID_ARG),
+    (dict(ldz=68), L.P4Q_ERR_INVALID_ARG),
+    (dict(divide=2), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip=0.0), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip=1.5), L.P4Q_ERR_INVALID_ARG),
+    (dict(sigma=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(sigma=ALIGNED + 4), L.P4Q_ERR_INVALID_ARG),
+    (dict(codes=ALIGNED + 8), L.P4Q_ERR_INVALID_ARG),
+    (dict(dt=3), L.P4Q_ERR_UNSUPPORTED),
+])
+def test_quant_scaled_validation(kw, status):
+    assert qscaled(**kw) == status
+    assert L.lib().p4q_last_error() != b""
+
+
+def calib(**kw):
+    a = dict(dt=0, M=8, N=64, K=128, x=ALIGNED, ldx=128, w=ALIGNED, ldw=128, t=ALIGNED, ldt=64,
+             sigma=ALIGNED, clip_a=1.0, clip_w=ALIGNED, loss=ALIGNED, gs=ALIGNED, gca=ALIGNED,
+             gcw=ALIGNED, ws=ALIGNED, ws_bytes=1 << 30)
+    a.update(kw)
+    return L.lib().p4q_calib_linear_grad(a["dt"], a["M"], a["N"], a["K"], a["x"], a["ldx"],
+                                         a["w"], a["ldw"], a["t"], a["ldt"], a["sigma"],
+                                         ctypes.c_float(a["clip_a"]), a["clip_w"], a["loss"],
+                                         a["gs"], a["gca"], a["gcw"], a["ws"], a["ws_bytes"],
+                                         None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(M=0), L.P4Q_ERR_INVALID_ARG),
+    (dict(N=96), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=192, ldx=192, ldw=192), L.P4Q_ERR_INVALID_ARG),
+    (dict(K=16384 + 128, ldx=16384 + 128, ldw=16384 + 128), L.P4Q_ERR_UNSUPPORTED),
+    (dict(ldx=120), L.P4Q_ERR_INVALID_ARG),
+    (dict(ldw=132), L.P4Q_ERR_INVALID_ARG),
+    (dict(ldt=62), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip_a=0.0), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip_a=1.01), L.P4Q_ERR_INVALID_ARG),
+    (dict(clip_w=None), L.P4Q_ERR_INVALID_ARG),
+    (dict(t=ALIGNED + 4), L.P4Q_ERR_INVALID_ARG),
+    (dict(ws=ALIGNED + 16), L.P4Q_ERR_INVALID_ARG),
+    (dict(ws=None), L.P4Q_ERR_WORKSPACE),
+    (dict(ws_bytes=1024), L.P4Q_ERR_WORKSPACE),
+    (dict(dt=2), L.P4Q_ERR_UNSUPPORTED),
+])
+def test_calib_validation(kw, status):
+    assert calib(**kw) == status
+    assert L.lib().p4q_last_error() != b""
+
+
+def test_calib_workspace_size():
+    f = L.lib().p4q_calib_linear_workspace_bytes
+    assert f(8, 96, 128) == 0 and f(0, 64, 128) == 0
+    small, big = f(384, 12288, 4096), f(385, 12288, 4096)
+    # at least codes, transposed bf16 codes, acc and the two bf16 operands
+    assert small >= 384 * 12288 * (4 + 2 + 2) + 4096 * (384 + 12288) * 2
+    assert big > small
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     import paper_2609_34867_amd as p4q
