@@ -47,6 +47,7 @@ def parse():
     ap.add_argument("--config", default="next7b_b16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode GEMV measurement")
+    ap.add_argument("--no-calib", action="store_true", help="skip the calibration-step measurement")
     ap.add_argument("--no-select-full", action="store_true",
                     help="skip the three-stage selector measurement")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -380,6 +381,49 @@ def attention(cfg, dev, reps=20):
             "mfma_frac": round(flops / us / 1e6 / FP16_PEAK_TFLOPS, 4)}
 
 
+def calibration(dev, reps=20, M=384, N=12288, K=4096):
+    """One pruning-aware calibration step of a W4A4 fake-quantized linear
+    (loss + gradients for the diagonal scales and clipping factors) at the
+    LLaVA-NeXT-7B q|k|v shape on one pruned calibration sample: M = 320 kept
+    visual + 64 text tokens, N = 3 x 4096, K = 4096.  Synthetic inputs of the
+    workload's calibration recipe (seeded on the GPU: the host generator's
+    float64 target matmul would dominate the set-up)."""
+    import torch
+    import paper_2609_34867_amd as p4q
+    g = torch.Generator(device=dev).manual_seed(11)
+    x = torch.randn((M, K), generator=g, device=dev, dtype=torch.float32)
+    ch = torch.randperm(K, generator=g, device=dev)[:8]
+    x[:, ch] *= 20.0
+    w = torch.randn((N, K), generator=g, device=dev, dtype=torch.float32) * 0.02
+    x, w = x.to(torch.float16), w.to(torch.float16)
+    target = x.float() @ w.float().T
+    sigma = torch.exp(0.3 * torch.randn(K, generator=g, device=dev))
+    sigma[ch] *= 20.0 ** 0.3
+    clip_w = 0.75 + 0.25 * torch.rand(N, generator=g, device=dev)
+    ws = p4q.calib_linear_workspace(M, N, K, dev)
+    outs = (torch.empty(1, device=dev), torch.empty(K, device=dev), torch.empty(1, device=dev),
+            torch.empty(N, device=dev))
+    run = lambda: p4q.calib_linear_grad(x, w, target, sigma, 0.9, clip_w, workspace=ws, out=outs)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    mnk = M * N * K
+    # time the matrix units need at their dense peaks: the int8 forward GEMM
+    # (2MNK ops) and the two bf16 backward products (2MNK flops each)
+    floor_us = 2 * mnk / (INT8_PEAK_TOPS * 1e6) + 4 * mnk / (FP16_PEAK_TFLOPS * 1e6)
+    return {"workload": f"calibration step of one W4A4 linear: M={M} (320 kept visual + 64 text "
+                        f"tokens), N={N} (q|k|v), K={K}, fp16; loss + d sigma, d clip_a, d clip_w",
+            "us": round(us, 2), "steps_per_s": round(1e6 / us, 1),
+            "mfma_floor_us": round(floor_us, 2), "mfma_frac": round(floor_us / us, 4)}
+
+
 def copy_calibration(dev, nbytes=1 << 30, reps=5):
     """A plain device-to-device copy of known size, run so that the HBM
     counters (FETCH_SIZE, WRITE_SIZE) can be scaled to bytes: the counter
@@ -482,6 +526,8 @@ def main():
     }
     res["prologue_rmsnorm_quant"] = prologue(cfg, st, dev)
     res["attention_prefill"] = attention(cfg, dev)
+    if not args.no_calib:
+        res["calibration_step"] = calibration(dev)
     if not args.no_select_full:
         res["selector_full"] = selector_full(cfg, dev)
     if not args.no_decode:

@@ -8,8 +8,10 @@
 //
 // One step, stream-ordered:
 //   1. k_quant_scaled (x2): X' = fl32(X / sigma), W' = fl32(W * sigma); per
-//      row Q4 with its clipping factor -> packed codes, scale, row maximum
-//      and the maximum's lowest index.
+//      row Q4 with its clipping factor -> packed codes, scale, row maximum,
+//      the maximum's lowest index, and one bit per value telling whether the
+//      rounded quotient lay inside [-8, 7] (the activation side also keeps
+//      X' in fp32).
 //   2. k_codes_bf16t (x2): the codes transposed to bf16 [K][rows], the
 //      contraction operands of the backward products (int4 codes are exact
 //      in bf16).
@@ -18,11 +20,12 @@
 //      operands P1 = bf16(R sW) [M][N] and P2^T = bf16(R sA) [N][Mp]; partial
 //      sums of R^2.
 //   5. k_calib_bwd (x2, bf16 MFMA, fp32 accumulation): dL/dXq ~ P1 Cw and
-//      dL/dWq ~ P2^T Ca are never stored.  The epilogue recomputes each
-//      element's transformed value z' and rounding decision and reduces its
-//      tile to per-row sums of g (code - inside u) and per-column sums of
-//      g inside z' (u = z'/s).  Both are linear in g, so the contraction is
-//      split freely across work-groups, each writing its own partial slot.
+//      dL/dWq ~ P2^T Ca are never stored.  The epilogue takes each element's
+//      code and inside bit from step 1 (the quantizer's own decisions, so no
+//      division happens here) and reduces its tile to per-row sums of
+//      g (code - inside z'/s) and per-column sums of g inside z'.  Both are
+//      linear in g, so the contraction is split freely across work-groups,
+//      each writing its own partial slot.
 //   6. k_calib_rows: per row g_s (deterministic sum of the slots), the clip
 //      gradients, and the row maximum's share g_s clip absmax / 7, added to
 //      its column with float64 atomics.
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(kThreads) void k_quant_scaled(
     const uint8_t *__restrict__ z, int64_t ldz_bytes, int nchunk, const float *__restrict__ sigma,
     float clip, const float *__restrict__ clip_rows, uint8_t *__restrict__ codes,
     int64_t ldc_bytes, float *__restrict__ scales, float *__restrict__ absmax,
-    int32_t *__restrict__ kstar) {
+    int32_t *__restrict__ kstar, float *__restrict__ zprime, uint8_t *__restrict__ inside) {
     __shared__ uint64_t s_key[kThreads / 64];
     const int row = blockIdx.x, t = threadIdx.x;
     const uint4 *src = reinterpret_cast<const uint4 *>(z + (int64_t)row * ldz_bytes);
@@ -120,6 +123,11 @@ __global__ __launch_bounds__(kThreads) void k_quant_scaled(
             for (int i = 0; i < 4; ++i) {
                 zp[c][2 * i] = transform<DIV>(lo_f32<BF16>(w[i]), sg[2 * i]);
                 zp[c][2 * i + 1] = transform<DIV>(hi_f32<BF16>(w[i]), sg[2 * i + 1]);
+            }
+            if (zprime) {
+                float4 *zo = reinterpret_cast<float4 *>(zprime + (int64_t)row * (8 * nchunk) + 8 * q);
+                zo[0] = make_float4(zp[c][0], zp[c][1], zp[c][2], zp[c][3]);
+                zo[1] = make_float4(zp[c][4], zp[c][5], zp[c][6], zp[c][7]);
             }
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -150,51 +158,64 @@ __global__ __launch_bounds__(kThreads) void k_quant_scaled(
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
         const int q = t + kThreads * c;
-        uint32_t packed = 0u;
+        uint32_t packed = 0u, ins = 0xFFu;
         if (s != 0.0f) {
             uint32_t w[8];
             float fm = 0.0f;
+            ins = 0u;
             if (!tiny) {
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    float tq = __builtin_fmaf(zp[c][e], r, kRneMagic);
+                    const float tq = __builtin_fmaf(zp[c][e], r, kRneMagic);
                     const float qq = tq - kRneMagic;
                     fm = __builtin_fmaxf(fm, __builtin_fabsf(__builtin_fmaf(zp[c][e], r, -qq)));
-                    tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
-                    w[e] = __float_as_uint(tq);
+                    const float tc = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
+                    ins |= (uint32_t)(tc == tq) << e;
+                    w[e] = __float_as_uint(tc);
                 }
             }
             // a value within 2^-19 of a rounding boundary somewhere in the
             // wave (or a tiny scale): this chunk by exact division
             if (tiny || __any(fm > kNearHalf)) {
+                ins = 0u;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) w[e] = q4_exact(zp[c][e], s);
+                for (int e = 0; e < 8; ++e) {
+                    const float rq = __builtin_rintf(zp[c][e] / s);
+                    const float cq = __builtin_amdgcn_fmed3f(rq, -8.0f, 7.0f);
+                    ins |= (uint32_t)(cq == rq) << e;
+                    w[e] = (uint32_t)(int)cq;
+                }
             }
             packed = pack_nibbles(w);
         }
-        if (q < nchunk) dst[q] = packed;
+        if (q < nchunk) {
+            dst[q] = packed;
+            if (inside) inside[(int64_t)row * nchunk + q] = (uint8_t)ins;
+        }
     }
 }
 
 template <int CH, bool BF16, bool DIV>
 hipError_t launch_qs(int R, int nchunk, const void *z, int64_t ldz_bytes, const float *sigma,
                      float clip, const float *clip_rows, uint8_t *codes, int64_t ldc_bytes,
-                     float *scales, float *absmax, int32_t *kstar, hipStream_t stream) {
+                     float *scales, float *absmax, int32_t *kstar, float *zprime,
+                     uint8_t *inside, hipStream_t stream) {
     hipLaunchKernelGGL((k_quant_scaled<CH, BF16, DIV>), dim3(R), dim3(kThreads), 0, stream,
                        static_cast<const uint8_t *>(z), ldz_bytes, nchunk, sigma, clip, clip_rows,
-                       codes, ldc_bytes, scales, absmax, kstar);
+                       codes, ldc_bytes, scales, absmax, kstar, zprime, inside);
     return hipGetLastError();
 }
 
 template <bool BF16, bool DIV>
 hipError_t launch_qs_typed(int R, int K, const void *z, int64_t ldz, const float *sigma,
                            float clip, const float *clip_rows, uint8_t *codes, float *scales,
-                           float *absmax, int32_t *kstar, hipStream_t stream) {
+                           float *absmax, int32_t *kstar, hipStream_t stream,
+                           float *zprime = nullptr, uint8_t *inside = nullptr) {
     const int nchunk = K / 8;
     const int per = (nchunk + kThreads - 1) / kThreads;      // <= 8 (K <= 16384)
 #define P4Q_QS(N)                                                                          \
     return launch_qs<N, BF16, DIV>(R, nchunk, z, ldz * 2, sigma, clip, clip_rows, codes,  \
-                                   K / 2, scales, absmax, kstar, stream)
+                                   K / 2, scales, absmax, kstar, zprime, inside, stream)
     if (per <= 1) P4Q_QS(1);
     if (per <= 2) P4Q_QS(2);
     if (per <= 4) P4Q_QS(4);
@@ -315,11 +336,12 @@ __global__ __launch_bounds__(kThreads) void k_calib_residual(
 // ---------------------------------------------------------------------------
 // 5. Backward contraction O[i][k] = sum_j P[i][j] C[k][j] (bf16 operands,
 //    fp32 accumulation on v_mfma_f32_32x32x16_bf16) with the fused reduction
-//    epilogue.  128 x 128 tiles, 4 wavefronts of 64 x 64 (2 x 2 MFMA tiles),
-//    64 j per stage, two LDS stages filled by buffer_load ... lds (rows past
-//    I read as zeros).  LDS rows are 128 bytes; 16-byte chunk c of row r sits
-//    at chunk c ^ ((r >> 1) & 7), so the 16 rows one fragment read touches
-//    hit distinct banks.
+//    epilogue.  128 x 128 tiles, 4 wavefronts of 64 (i) x 64 (k), each 2 x 2
+//    MFMA tiles with C as the first operand, so that a lane's accumulators
+//    hold four consecutive k of one i; 64 j per stage, two LDS stages filled
+//    by buffer_load ... lds (rows past I read as zeros).  LDS rows are 128
+//    bytes; 16-byte chunk c of row r sits at chunk c ^ ((r >> 1) & 7), so the
+//    16 rows one fragment read touches hit distinct banks.
 //    grid (Kd / 128, ceil(I / 128), splits); split z covers j in
 //    [z js, min(J, (z + 1) js)).  Outputs: rowpart[(kt splits + z) I + i],
 //    colpart[(it splits + z) Kd + k].
@@ -328,7 +350,15 @@ constexpr int BB = 128;
 constexpr int BJ = 64;
 constexpr int kHalfStage = BB * BJ * 2;        // 16 KB: one operand
 constexpr int kStage = 2 * kHalfStage;
-constexpr int kZStride = 288;                  // bytes per row of the epilogue's Z tile
+// epilogue LDS rows (bytes); strides chosen so that the 32 rows a half-wave
+// reads at one column offset fall in distinct banks
+constexpr int kZStride = 264;                  // 128 16-bit values + 8
+constexpr int kCStride = 68;                   // 64 bytes of packed codes + 4
+constexpr int kBStride = 20;                   // 16 bytes of inside bits + 4
+constexpr int kOffC = BB * kZStride;
+constexpr int kOffB = kOffC + BB * kCStride;
+constexpr int kOffS = kOffB + BB * kBStride;
+static_assert(kOffS + 10 * BB * 4 <= 2 * kStage, "epilogue LDS");
 
 __device__ __forceinline__ v4i buffer_rsrc(const void *base, uint32_t bytes) {
     const uint64_t b = reinterpret_cast<uint64_t>(base);
@@ -350,12 +380,19 @@ __device__ __forceinline__ v16f mfma_bf16(uint4 a, uint4 b, v16f c) {
                                                    __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
 }
 
+// Epilogue per element (g = the contraction's value at (i, k), z' the
+// transformed input, code and inside bit as the quantizer decided them,
+// f = z'/s - code, taken only where inside):
+//   row sum i    += g (code - inside z'/s) = inside ? -g f : g code
+//   column sum k += inside ? g z' : 0
 template <bool BF16, bool DIV>
 __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
     const uint16_t *__restrict__ P, int64_t ldp, const uint16_t *__restrict__ C, int64_t ldc,
     int I, int J, int js, const uint16_t *__restrict__ Z, int64_t ldz,
-    const float *__restrict__ sigma, const float *__restrict__ srow, int Kd,
-    float *__restrict__ rowpart, float *__restrict__ colpart) {
+    const float *__restrict__ zprime, const uint8_t *__restrict__ codes,
+    const uint8_t *__restrict__ inside, const float *__restrict__ sigma,
+    const float *__restrict__ srow, int Kd, float *__restrict__ rowpart,
+    float *__restrict__ colpart) {
     __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * kStage];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int wi = wave >> 1, wk = wave & 1;
@@ -388,6 +425,8 @@ __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
         }
     };
 
+    // acc[kx][iy]: rows k = wk*64 + 32kx + 8(r/4) + 4(l/32) + r%4, column
+    // i = wi*64 + 32iy + l%32
     v16f acc[2][2];
 #pragma unroll
     for (int x = 0; x < 2; ++x)
@@ -396,15 +435,44 @@ __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[x][y][e] = 0.0f;
 
-    // fragment rows: A (P) rows wi*64 + 32x + l%32, B (C) rows wk*64 + 32y + l%32
     const int r32 = lane & 31, g2 = lane >> 5;
-    uint32_t fa[2], fb[2];
+    uint32_t fp[2], fc[2];
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-        fa[x] = (uint32_t)((wi * 64 + 32 * x + r32) * 128);
-        fb[x] = (uint32_t)(kHalfStage + (wk * 64 + 32 * x + r32) * 128);
+        fp[x] = (uint32_t)((wi * 64 + 32 * x + r32) * 128);
+        fc[x] = (uint32_t)(kHalfStage + (wk * 64 + 32 * x + r32) * 128);
     }
-    const uint32_t swz = (uint32_t)(((wi * 64 + r32) >> 1) & 7);    // same for x = 0, 1 and for B
+    const uint32_t swz = (uint32_t)((r32 >> 1) & 7);    // (row >> 1) & 7 of every fragment row
+
+    // the epilogue's inputs, fetched now so that their latency overlaps the
+    // first stage's: weight tile (16-bit), packed codes, inside bits, row
+    // scale and sigma
+    const int64_t cb = Kd / 2, ib = Kd / 8;                  // row bytes of codes, inside bits
+    uint4 zpre[DIV ? 1 : 8], cpre[2], bpre = make_uint4(0u, 0u, 0u, 0u);
+    float spre = 0.0f, gpre = 0.0f;
+    if constexpr (!DIV) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const int idx = t + kThreads * c, r = idx >> 4, q = idx & 15, i = i0 + r;
+            zpre[c] = (i < I) ? *reinterpret_cast<const uint4 *>(Z + (int64_t)i * ldz + k0 + 8 * q)
+                              : make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        const int idx = t + kThreads * c, r = idx >> 2, q = idx & 3, i = i0 + r;
+        cpre[c] = (i < I) ? *reinterpret_cast<const uint4 *>(codes + (int64_t)i * cb + k0 / 2 + 16 * q)
+                          : make_uint4(0u, 0u, 0u, 0u);
+    }
+    if (t < BB) {
+        const int i = i0 + t;
+        if (i < I) {
+            bpre = *reinterpret_cast<const uint4 *>(inside + (int64_t)i * ib + k0 / 8);
+            spre = srow[i];
+        }
+        gpre = sigma[k0 + t];
+    }
+
     if (nst > 0) issue(0, 0);
     for (int st = 0; st < nst; ++st) {
         // stage st has landed from every wave, and every wave is done with
@@ -418,8 +486,8 @@ __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
             uint4 a[2], b[2];
 #pragma unroll
             for (int x = 0; x < 2; ++x) {
-                a[x] = *reinterpret_cast<const uint4 *>(base + fa[x] + ch);
-                b[x] = *reinterpret_cast<const uint4 *>(base + fb[x] + ch);
+                a[x] = *reinterpret_cast<const uint4 *>(base + fc[x] + ch);
+                b[x] = *reinterpret_cast<const uint4 *>(base + fp[x] + ch);
             }
 #pragma unroll
             for (int x = 0; x < 2; ++x)
@@ -428,91 +496,117 @@ __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
         }
     }
 
-    // ---- epilogue: Z tile, row scales and sigma to LDS ----
+    // ---- epilogue: the tile's inputs, codes and inside bits to LDS ----
     __syncthreads();
-    uint8_t *zs = smem;
-    float *s_s = reinterpret_cast<float *>(smem + BB * kZStride);    // row scale
-    float *s_r = s_s + BB;                                           // 1 / scale (0: exact path)
-    float *s_g = s_r + BB;                                           // sigma of the tile's columns
-    float *rowred = s_g + BB;                                        // [2][128]
-    float *colred = rowred + 2 * BB;                                 // [2][128]
-    for (int c = t; c < BB * 16; c += kThreads) {
-        const int r = c >> 4, q = c & 15, i = i0 + r;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (i < I) v = *reinterpret_cast<const uint4 *>(Z + (int64_t)i * ldz + k0 + 8 * q);
-        *reinterpret_cast<uint4 *>(zs + r * kZStride + 16 * q) = v;
+    float *s_r = reinterpret_cast<float *>(smem + kOffS);    // 1 / (s P)
+    float *s_p = s_r + BB;                                   // P = 1, or 2^64 for s < 2^-100
+    float *s_m = s_p + BB;                                   // 1, or 0 (zero row / past I)
+    float *s_g = s_m + BB;                                   // sigma of the tile's columns
+    float *rowred = s_g + BB;                                // [2][128]
+    float *colred = rowred + 2 * BB;                         // [2][128]
+    if constexpr (!DIV) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const int idx = t + kThreads * c, r = idx >> 4, q = idx & 15;
+            uint2 *d = reinterpret_cast<uint2 *>(smem + r * kZStride + 16 * q);
+            d[0] = make_uint2(zpre[c].x, zpre[c].y);
+            d[1] = make_uint2(zpre[c].z, zpre[c].w);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        const int idx = t + kThreads * c, r = idx >> 2, q = idx & 3;
+        uint32_t *d = reinterpret_cast<uint32_t *>(smem + kOffC + r * kCStride + 16 * q);
+        d[0] = cpre[c].x; d[1] = cpre[c].y; d[2] = cpre[c].z; d[3] = cpre[c].w;
     }
     if (t < BB) {
-        const float s = (i0 + t < I) ? srow[i0 + t] : 0.0f;
-        s_s[t] = s;
-        s_r[t] = (s >= kTinyScale) ? 1.0f / s : 0.0f;
-        s_g[t] = sigma[k0 + t];
+        uint32_t *d = reinterpret_cast<uint32_t *>(smem + kOffB + t * kBStride);
+        d[0] = bpre.x; d[1] = bpre.y; d[2] = bpre.z; d[3] = bpre.w;
+        const float s = spre;
+        const bool tiny = s < 0x1p-100f;
+        const float pw = tiny ? 0x1p64f : 1.0f;
+        s_r[t] = (s != 0.0f) ? 1.0f / (s * pw) : 0.0f;
+        s_p[t] = pw;
+        s_m[t] = (s != 0.0f) ? 1.0f : 0.0f;
+        s_g[t] = gpre;
     }
     __syncthreads();
 
-    float rowv[32];
+    float rowv[2] = {0.0f, 0.0f};
+    float colv[32];
 #pragma unroll
-    for (int v = 0; v < 32; ++v) rowv[v] = 0.0f;
-    float colv[2] = {0.0f, 0.0f};
+    for (int v = 0; v < 32; ++v) colv[v] = 0.0f;
+    float rs[2], pw[2], gm[2];
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
-        const int kl = wk * 64 + 32 * y + r32;
-        const float sg = s_g[kl];
+        const int il = wi * 64 + 32 * y + r32;
+        rs[y] = s_r[il];
+        pw[y] = s_p[il];
+        gm[y] = s_m[il];
+    }
+    const int ish = 4 * g2;                   // bit of k = kb within its inside byte
 #pragma unroll
-        for (int x = 0; x < 2; ++x) {
+    for (int x = 0; x < 2; ++x) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int il = wi * 64 + 32 * x + 8 * (e >> 2) + 4 * g2 + (e & 3);
-                const float g = acc[x][y][e];
-                const float zf = half_to_f32<BF16>(
-                    *reinterpret_cast<const uint16_t *>(zs + il * kZStride + 2 * kl));
-                const float zp = transform<DIV>(zf, sg);
-                const float s = s_s[il], rs = s_r[il];
-                float rc = 0.0f, cc = 0.0f;
-                if (s != 0.0f) {
-                    float u = 0.0f, rho = 0.0f;
-                    bool exact = (rs == 0.0f);
-                    if (!exact) {
-                        const float tq = __builtin_fmaf(zp, rs, kRneMagic);
-                        rho = tq - kRneMagic;
-                        u = zp * rs;
-                        exact = __builtin_fabsf(__builtin_fmaf(zp, rs, -rho)) > kNearHalf;
-                    }
-                    if (exact) {
-                        u = zp / s;
-                        rho = __builtin_rintf(u);
-                    }
-                    const bool inside = (rho >= -8.0f) && (rho <= 7.0f);
-                    const float q = __builtin_amdgcn_fmed3f(rho, -8.0f, 7.0f);
-                    rc = g * (inside ? q - u : q);
-                    cc = inside ? g * zp : 0.0f;
+        for (int rg = 0; rg < 4; ++rg) {
+            const int kb = wk * 64 + 32 * x + 8 * rg + 4 * g2;      // 4 consecutive k
+            const float4 sg = *reinterpret_cast<const float4 *>(s_g + kb);
+            const float sgv[4] = {sg.x, sg.y, sg.z, sg.w};
+#pragma unroll
+            for (int y = 0; y < 2; ++y) {
+                const int il = wi * 64 + 32 * y + r32;
+                float zp[4];
+                if constexpr (DIV) {
+                    const float4 v = *reinterpret_cast<const float4 *>(
+                        zprime + (int64_t)min(i0 + il, I - 1) * Kd + k0 + kb);
+                    zp[0] = v.x; zp[1] = v.y; zp[2] = v.z; zp[3] = v.w;
+                } else {
+                    const uint2 v = *reinterpret_cast<const uint2 *>(smem + il * kZStride + 2 * kb);
+                    zp[0] = __fmul_rn(half_to_f32<BF16>((uint16_t)(v.x & 0xFFFFu)), sgv[0]);
+                    zp[1] = __fmul_rn(half_to_f32<BF16>((uint16_t)(v.x >> 16)), sgv[1]);
+                    zp[2] = __fmul_rn(half_to_f32<BF16>((uint16_t)(v.y & 0xFFFFu)), sgv[2]);
+                    zp[3] = __fmul_rn(half_to_f32<BF16>((uint16_t)(v.y >> 16)), sgv[3]);
                 }
-                rowv[16 * x + e] += rc;
-                colv[y] += cc;
+                const uint32_t cw = *reinterpret_cast<const uint16_t *>(
+                    smem + kOffC + il * kCStride + kb / 2);
+                const uint32_t bw = (uint32_t)smem[kOffB + il * kBStride + kb / 8] >> ish;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float g = acc[x][y][4 * rg + e] * gm[y];
+                    const float q = (float)(((int)(cw << (28 - 4 * e))) >> 28);
+                    const bool in = (bw >> e) & 1u;
+                    const float f = __builtin_fmaf(zp[e] * pw[y], rs[y], -q);
+                    rowv[y] = __builtin_fmaf(g, in ? -f : q, rowv[y]);
+                    colv[16 * x + 4 * rg + e] = __builtin_fmaf(in ? g : 0.0f, zp[e],
+                                                               colv[16 * x + 4 * rg + e]);
+                }
             }
         }
     }
-    // rows: the 32 values of each half-wave summed over its 32 lanes by a
-    // halving exchange; lane l ends with value index l % 32
+    // columns: the 32 values of each half-wave summed over its 32 lanes (the
+    // i direction) by a halving exchange; lane l ends with value index l % 32
 #pragma unroll
     for (int m = 16; m >= 1; m >>= 1) {
         const bool up = (lane & m) != 0;
 #pragma unroll
         for (int v = 0; v < m; ++v) {
-            const float send = up ? rowv[v] : rowv[v + m];
-            const float keep = up ? rowv[v + m] : rowv[v];
-            rowv[v] = keep + __shfl_xor(send, m);
+            // the asm keeps the two selects on values: a select between two
+            // elements of the array would otherwise become an indexed access
+            float lo = colv[v], hi = colv[v + m];
+            asm volatile("" : "+v"(lo), "+v"(hi));
+            const float send = up ? lo : hi;
+            const float keep = up ? hi : lo;
+            colv[v] = keep + __shfl_xor(send, m);
         }
     }
     {
-        const int v = r32, x = v >> 4, e = v & 15;
-        const int il = wi * 64 + 32 * x + 8 * (e >> 2) + 4 * g2 + (e & 3);
-        rowred[wk * BB + il] = rowv[0];
+        const int v = r32, x = v >> 4, rg = (v >> 2) & 3, e = v & 3;
+        colred[wi * BB + wk * 64 + 32 * x + 8 * rg + 4 * g2 + e] = colv[0];
     }
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
-        const float c = colv[y] + __shfl_xor(colv[y], 32);
-        if (g2 == 0) colred[wi * BB + wk * 64 + 32 * y + r32] = c;
+        const float r = rowv[y] + __shfl_xor(rowv[y], 32);
+        if (g2 == 0) rowred[wk * BB + wi * 64 + 32 * y + r32] = r;
     }
     __syncthreads();
     if (t < BB) {
@@ -525,9 +619,43 @@ __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
 }
 
 // ---------------------------------------------------------------------------
-// 6. Rows: g_s, clip gradients, the row maximum's share scattered to its
-//    column.  Blocks [0, nbA) hold activation rows, the rest weight rows.
+// 6-7. Finishing sums over the partial slots, in a fixed order: RB rows (or
+//    columns) per 256-thread block, the slots dealt round-robin to 256 / RB
+//    groups of RB threads, each thread keeping four loads in flight.
 // ---------------------------------------------------------------------------
+template <int G>
+__device__ __forceinline__ double slot_sum(const float *__restrict__ p, int n, int64_t stride,
+                                           int g) {
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+    int s = g;
+    for (; s + 3 * G < n; s += 4 * G) {
+        a0 += (double)p[(int64_t)s * stride];
+        a1 += (double)p[(int64_t)(s + G) * stride];
+        a2 += (double)p[(int64_t)(s + 2 * G) * stride];
+        a3 += (double)p[(int64_t)(s + 3 * G) * stride];
+    }
+    for (; s < n; s += G) a0 += (double)p[(int64_t)s * stride];
+    return (a0 + a1) + (a2 + a3);
+}
+
+// groups' partial sums -> the total for row / column t (valid in t < RB)
+template <int RB>
+__device__ __forceinline__ double group_total(double v, double *part) {
+    const int t = threadIdx.x;
+    part[t] = v;
+    __syncthreads();
+    double s = 0.0;
+    if (t < RB)
+        for (int g = 0; g < kThreads / RB; ++g) s += part[RB * g + t];
+    return s;
+}
+
+constexpr int kRowsA = 16;     // activation rows per block (their slots are many)
+constexpr int kRowsW = 64;     // weight rows, columns per block
+
+// 6. Rows: g_s, the clip gradients, and the row maximum's share scattered
+//    to its column.  Blocks [0, nbA) hold activation rows, the rest weight
+//    rows.
 __global__ __launch_bounds__(kThreads) void k_calib_rows(
     const float *__restrict__ rowA, int nsA, int M, const float *__restrict__ sA,
     const float *__restrict__ aA, const int32_t *__restrict__ kA, float clip_a,
@@ -536,25 +664,28 @@ __global__ __launch_bounds__(kThreads) void k_calib_rows(
     const float *__restrict__ clip_w, int nbA, double scale, double *__restrict__ corrA,
     double *__restrict__ corrW, double *__restrict__ dclipa_part,
     float *__restrict__ grad_clip_w) {
-    __shared__ double red[kThreads / 64];
+    __shared__ double part[kThreads];
     const int t = threadIdx.x;
     if ((int)blockIdx.x < nbA) {
-        const int m = blockIdx.x * kThreads + t;
-        double part = 0.0;
-        if (m < M) {
-            double gs = 0.0;
-            for (int s = 0; s < nsA; ++s) gs += (double)rowA[(int64_t)s * M + m];
-            const double a = (double)aA[m];
-            if (sA[m] != 0.0f) atomicAdd(&corrA[kA[m]], gs * (double)clip_a * a / 7.0);
-            part = gs * a / 7.0;
+        const int m = blockIdx.x * kRowsA + (t % kRowsA);
+        const double gs = group_total<kRowsA>(
+            m < M ? slot_sum<kThreads / kRowsA>(rowA + m, nsA, M, t / kRowsA) : 0.0, part);
+        if (t < 64) {
+            double v = 0.0;
+            if (t < kRowsA && m < M) {
+                const double a = (double)aA[m];
+                if (sA[m] != 0.0f) atomicAdd(&corrA[kA[m]], gs * (double)clip_a * a / 7.0);
+                v = gs * a / 7.0;
+            }
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+            if (t == 0) dclipa_part[blockIdx.x] = v;
         }
-        const double s = block_sum(part, red);
-        if (t == 0) dclipa_part[blockIdx.x] = s;
     } else {
-        const int n = (blockIdx.x - nbA) * kThreads + t;
-        if (n < N) {
-            double gs = 0.0;
-            for (int s = 0; s < nsW; ++s) gs += (double)rowW[(int64_t)s * N + n];
+        const int n = (blockIdx.x - nbA) * kRowsW + (t % kRowsW);
+        const double gs = group_total<kRowsW>(
+            n < N ? slot_sum<kThreads / kRowsW>(rowW + n, nsW, N, t / kRowsW) : 0.0, part);
+        if (t < kRowsW && n < N) {
             const double a = (double)aW[n];
             if (sW[n] != 0.0f) atomicAdd(&corrW[kW[n]], gs * (double)clip_w[n] * a / 7.0);
             grad_clip_w[n] = (float)(scale * gs * a / 7.0);
@@ -562,36 +693,33 @@ __global__ __launch_bounds__(kThreads) void k_calib_rows(
     }
 }
 
-// ---------------------------------------------------------------------------
-// 7. Columns: d sigma; block 0 also reduces the loss and d clip_a (fixed
-//    order).
-// ---------------------------------------------------------------------------
+// 7. Columns: d sigma; block 0 also reduces the loss and d clip_a.
 __global__ __launch_bounds__(kThreads) void k_calib_cols(
     const float *__restrict__ colA, int nslA, const float *__restrict__ colW, int nslW,
     const double *__restrict__ corrA, const double *__restrict__ corrW,
     const float *__restrict__ sigma, int K, double scale, float *__restrict__ grad_sigma,
     const double *__restrict__ loss_part, int nloss, double inv_mn, float *__restrict__ loss,
     const double *__restrict__ dclipa_part, int nbA, float *__restrict__ grad_clip_a) {
+    __shared__ double part[kThreads];
     __shared__ double red[kThreads / 64];
-    const int t = threadIdx.x;
-    const int k = blockIdx.x * kThreads + t;
-    if (k < K) {
-        double cx = corrA[k], cw = corrW[k];
-        for (int s = 0; s < nslA; ++s) cx += (double)colA[(int64_t)s * K + k];
-        for (int s = 0; s < nslW; ++s) cw += (double)colW[(int64_t)s * K + k];
-        grad_sigma[k] = (float)(scale * (cw - cx) / (double)sigma[k]);
-    }
+    const int t = threadIdx.x, c = t % kRowsW, g = t / kRowsW;
+    const int k = blockIdx.x * kRowsW + c;      // K % 64 == 0
+    const double cx = group_total<kRowsW>(slot_sum<kThreads / kRowsW>(colA + k, nslA, K, g), part);
+    __syncthreads();
+    const double cw = group_total<kRowsW>(slot_sum<kThreads / kRowsW>(colW + k, nslW, K, g), part);
+    if (t < kRowsW)
+        grad_sigma[k] = (float)(scale * ((cw + corrW[k]) - (cx + corrA[k])) / (double)sigma[k]);
     if (blockIdx.x == 0) {
         double l = 0.0;
         for (int i = t; i < nloss; i += kThreads) l += loss_part[i];
         l = block_sum(l, red);
         __syncthreads();
-        double c = 0.0;
-        for (int i = t; i < nbA; i += kThreads) c += dclipa_part[i];
-        c = block_sum(c, red);
+        double cl = 0.0;
+        for (int i = t; i < nbA; i += kThreads) cl += dclipa_part[i];
+        cl = block_sum(cl, red);
         if (t == 0) {
             loss[0] = (float)(l * inv_mn);
-            grad_clip_a[0] = (float)(scale * c);
+            grad_clip_a[0] = (float)(scale * cl);
         }
     }
 }
@@ -620,7 +748,7 @@ CalibPlan calib_plan(int M, int N, int K) {
     };
     splits(p.tilesMA * kt, N, p.nsA, p.jsA);
     splits(p.tilesNW * kt, p.Mp, p.nsW, p.jsW);
-    p.nbA = (M + kThreads - 1) / kThreads;
+    p.nbA = (M + kRowsA - 1) / kRowsA;
     p.nloss = (N / 64) * (p.Mp / 64);
     return p;
 }
@@ -630,6 +758,8 @@ struct CalibWs {
     float *sA, *aA, *sW, *aW;
     int32_t *kA, *kW;
     uint16_t *CaT, *CwT, *P1, *P2T;
+    float *xprime;
+    uint8_t *insA, *insW;
     int32_t *acc;
     double *loss_part, *corr, *dclipa_part;
     float *rowA, *colA, *rowW, *colW;
@@ -652,6 +782,9 @@ size_t calib_carve(const CalibPlan &p, int M, int N, int K, uint8_t *base, Calib
     c.sW = reinterpret_cast<float *>(take((size_t)N * 4));
     c.aW = reinterpret_cast<float *>(take((size_t)N * 4));
     c.kW = reinterpret_cast<int32_t *>(take((size_t)N * 4));
+    c.xprime = reinterpret_cast<float *>(take((size_t)M * K * 4));
+    c.insA = take((size_t)M * K / 8);
+    c.insW = take((size_t)N * K / 8);
     c.CaT = reinterpret_cast<uint16_t *>(take((size_t)K * p.Mp * 2));
     c.CwT = reinterpret_cast<uint16_t *>(take((size_t)K * N * 2));
     c.acc = reinterpret_cast<int32_t *>(take((size_t)M * N * 4));
@@ -679,10 +812,10 @@ hipError_t calib_typed(int M, int N, int K, const void *x, int64_t ldx, const vo
     hipError_t e;
     // 1. transformed quantizers
     if ((e = launch_qs_typed<BF16, true>(M, K, x, ldx, sigma, clip_a, nullptr, c.codesA, c.sA,
-                                         c.aA, c.kA, stream)) != hipSuccess)
+                                         c.aA, c.kA, stream, c.xprime, c.insA)) != hipSuccess)
         return e;
     if ((e = launch_qs_typed<BF16, false>(N, K, w, ldw, sigma, 1.0f, clip_w, c.codesW, c.sW,
-                                          c.aW, c.kW, stream)) != hipSuccess)
+                                          c.aW, c.kW, stream, nullptr, c.insW)) != hipSuccess)
         return e;
     // 2. transposed bf16 codes
     hipLaunchKernelGGL(k_codes_bf16t, dim3(p.Mp / 64, K / 128), dim3(kThreads), 0, stream,
@@ -701,21 +834,21 @@ hipError_t calib_typed(int M, int N, int K, const void *x, int64_t ldx, const vo
     // 5. backward contractions with fused reductions
     hipLaunchKernelGGL((k_calib_bwd<BF16, true>), dim3(K / BB, p.tilesMA, p.nsA),
                        dim3(kThreads), 0, stream, c.P1, (int64_t)N, c.CwT, (int64_t)N, M, N,
-                       p.jsA, static_cast<const uint16_t *>(x), ldx, sigma, c.sA, K, c.rowA,
-                       c.colA);
+                       p.jsA, static_cast<const uint16_t *>(x), ldx, c.xprime, c.codesA, c.insA,
+                       sigma, c.sA, K, c.rowA, c.colA);
     hipLaunchKernelGGL((k_calib_bwd<BF16, false>), dim3(K / BB, p.tilesNW, p.nsW),
                        dim3(kThreads), 0, stream, c.P2T, (int64_t)p.Mp, c.CaT, (int64_t)p.Mp, N,
-                       p.Mp, p.jsW, static_cast<const uint16_t *>(w), ldw, sigma, c.sW, K,
-                       c.rowW, c.colW);
+                       p.Mp, p.jsW, static_cast<const uint16_t *>(w), ldw, c.xprime, c.codesW,
+                       c.insW, sigma, c.sW, K, c.rowW, c.colW);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // 6-7. finish
     const double scale = 2.0 / ((double)M * (double)N);
-    const int nbW = (N + kThreads - 1) / kThreads;
+    const int nbW = (N + kRowsW - 1) / kRowsW;
     hipLaunchKernelGGL(k_calib_rows, dim3(p.nbA + nbW), dim3(kThreads), 0, stream, c.rowA,
                        (K / BB) * p.nsA, M, c.sA, c.aA, c.kA, clip_a, c.rowW, (K / BB) * p.nsW,
                        N, c.sW, c.aW, c.kW, clip_w, p.nbA, scale, c.corr, c.corr + K,
                        c.dclipa_part, grad_clip_w);
-    hipLaunchKernelGGL(k_calib_cols, dim3((K + kThreads - 1) / kThreads), dim3(kThreads), 0,
+    hipLaunchKernelGGL(k_calib_cols, dim3(K / kRowsW), dim3(kThreads), 0,
                        stream, c.colA, p.tilesMA * p.nsA, c.colW, p.tilesNW * p.nsW, c.corr,
                        c.corr + K, sigma, K, scale, grad_sigma, c.loss_part, p.nloss,
                        1.0 / ((double)M * (double)N), loss, c.dclipa_part, p.nbA, grad_clip_a);
