@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode GEMV measurement")
     ap.add_argument("--no-calib", action="store_true", help="skip the calibration-step measurement")
+    ap.add_argument("--calib-only", action="store_true",
+                    help="measure only the calibration step (for profiling it alone)")
     ap.add_argument("--no-select-full", action="store_true",
                     help="skip the three-stage selector measurement")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -469,6 +471,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.copy_calibration:
         copy_calibration(dev)
+        return
+    if args.calib_only:
+        print(json.dumps({"calibration_step": calibration(dev)}), flush=True)
         return
     st = setup(cfg, dev)
     for i in range(args.warmup):
