@@ -135,7 +135,7 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
                                                       int32_t *__restrict__ stats,
                                                       int64_t *__restrict__ keys,
                                                       uint32_t *__restrict__ vcodes) {
-    extern __shared__ uint2 s_cc[];          // [JMAX][64*CH] uint2, zero-padded
+    extern __shared__ uint32_t s_cc[];       // [JMAX][64*CH] packed int4, zero-padded
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63;
     // wave-uniform (keeps the row buffer descriptor in SGPRs)
@@ -149,7 +149,16 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
         const uint2 *g = reinterpret_cast<const uint2 *>(ccodes + (int64_t)b * J * d);
         for (int q = threadIdx.x; q < JMAX * kChunks; q += 256) {
             const int j = q / kChunks, c = q - j * kChunks;
-            s_cc[q] = (j < J && c < nchunk) ? g[j * nchunk + c] : make_uint2(0, 0);
+            uint32_t pk = 0u;
+            if (j < J && c < nchunk) {
+                const uint2 u = g[j * nchunk + c];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    pk |= ((u.x >> (8 * e)) & 0xFu) << (4 * e);
+                    pk |= ((u.y >> (8 * e)) & 0xFu) << (4 * e + 16);
+                }
+            }
+            s_cc[q] = pk;
         }
     }
     __syncthreads();
@@ -198,42 +207,53 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
         const uint32_t mbits = wave_max_u32(max(m2 & 0xFFFFu, m2 >> 16));
         const float s = row_scale<CLIP1>(mag_to_f32<BF16>(mbits), clip);
 
-        uint2 cv[CH];                                        // int8 codes, 8 per chunk
+        uint32_t cv[CH];                                     // packed int4 codes, 8 per chunk
 #pragma unroll
-        for (int c = 0; c < CH; ++c) cv[c] = make_uint2(0, 0);
+        for (int c = 0; c < CH; ++c) cv[c] = 0u;
         // packed int4 copy of the codes, when asked for (the Gram matrix of
         // the diversity stage is computed from it)
         uint32_t *vrow = vcodes ? vcodes + ((int64_t)b * N + row0 + r) * (d / 8) : nullptr;
-        if (s == 0.0f && vrow) {
-#pragma unroll
-            for (int c = 0; c < CH; ++c)
-                if (lane + 64 * c < nchunk) vrow[lane + 64 * c] = 0u;
-        }
         if (s != 0.0f) {
             const bool tiny = !(s >= kTinyScale);
             const float rc = tiny ? 0.0f : 1.0f / s;
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 uint32_t w[8];
-                uint32_t near = 0;
+                float fm = 0.0f;      // largest |x r - rne(x r)| of the chunk
                 if (!tiny) {
-                    q4_chunk_fast<BF16, CLIP1>(v[c], rc, w, near);
-                    cv[c] = make_uint2(bytes4(w[0], w[1], w[2], w[3]), bytes4(w[4], w[5], w[6], w[7]));
+                    const uint32_t x4[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            const float x = h ? hi_f32<BF16>(x4[i]) : lo_f32<BF16>(x4[i]);
+                            float tq = __builtin_fmaf(x, rc, kRneMagic);
+                            const float qq = tq - kRneMagic;
+                            fm = __builtin_fmaxf(fm, __builtin_fabsf(__builtin_fmaf(x, rc, -qq)));
+                            if constexpr (!CLIP1)
+                                tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
+                            w[2 * i + h] = __float_as_uint(tq);
+                        }
+                    }
                 }
                 // wave-uniform and rare: some lane holds a value of this chunk
                 // within 2^-19 of a rounding boundary (exact fp16 ratios such as
                 // x = a/2 land on ties), or the scale is tiny.  Only this chunk
                 // is recomputed by exact division.
-                if (tiny || __any((int)near)) {
+                if (tiny || __any(fm > kNearHalf)) {
                     uint4 vc = v[c];
                     // opaque copy: keeps the exact path's fp16 -> fp32 conversions
                     // from being hoisted into (and paid on) the fast path
                     asm volatile("" : "+v"(vc.x), "+v"(vc.y), "+v"(vc.z), "+v"(vc.w));
                     q4_chunk_exact<BF16>(vc, s, w);
-                    cv[c] = make_uint2(bytes4(w[0], w[1], w[2], w[3]), bytes4(w[4], w[5], w[6], w[7]));
                 }
-                if (vrow && lane + 64 * c < nchunk) vrow[lane + 64 * c] = pack_nibbles(w);
+                cv[c] = pack_nibbles(w);
             }
+        }
+        if (vrow) {
+#pragma unroll
+            for (int c = 0; c < CH; ++c)
+                if (lane + 64 * c < nchunk) vrow[lane + 64 * c] = cv[c];
         }
 
         int nv = 0;
@@ -242,14 +262,11 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
         for (int j = 0; j < JMAX; ++j) dj[j] = 0;
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
-            nv = __builtin_amdgcn_sdot4((int)cv[c].x, (int)cv[c].x, nv, false);
-            nv = __builtin_amdgcn_sdot4((int)cv[c].y, (int)cv[c].y, nv, false);
+            nv = __builtin_amdgcn_sdot8((int)cv[c], (int)cv[c], nv, false);
 #pragma unroll
-            for (int j = 0; j < JMAX; ++j) {
-                const uint2 cc = s_cc[j * kChunks + lane + 64 * c];
-                dj[j] = __builtin_amdgcn_sdot4((int)cv[c].x, (int)cc.x, dj[j], false);
-                dj[j] = __builtin_amdgcn_sdot4((int)cv[c].y, (int)cc.y, dj[j], false);
-            }
+            for (int j = 0; j < JMAX; ++j)
+                dj[j] = __builtin_amdgcn_sdot8((int)cv[c], (int)s_cc[j * kChunks + lane + 64 * c],
+                                               dj[j], false);
         }
         int part[8];
 #pragma unroll
@@ -547,7 +564,7 @@ __global__ __launch_bounds__(256) void k_select_gather(const uint4 *__restrict__
 template <int CH, int JMAX, bool BF16, bool CLIP1>
 hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const void *vis,
                         const SelectWorkspace &ws, hipStream_t stream) {
-    const size_t lds = (size_t)JMAX * 64 * CH * 8;
+    const size_t lds = (size_t)JMAX * 64 * CH * 4;
     // Rows per wavefront: enough that the whole grid is resident at once
     // (one wave of blocks, no partly filled last wave).
     static int resident = 0;                      // blocks per CU x CUs, per instantiation
