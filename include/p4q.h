@@ -284,8 +284,12 @@ int p4q_calib_linear_grad(p4q_dtype dt, int M, int N, int K,
  *   packed as above (both K-contiguous); a_scales fp32 [M]; w_scales fp32
  *   [N_out]; y [M, ldy] of out_dt; acc_out int32 [M, N_out] or NULL (when
  *   given, the raw accumulators are stored too).
- * Workspace: p4q_w4a4_linear_workspace_bytes(M, N_out, K_in) bytes (may be
- *   0; ws may then be NULL).
+ * Workspace (optional): p4q_w4a4_linear_workspace_bytes(M, N_out, K_in)
+ *   bytes, 16-byte aligned.  It is nonzero for small M (fewer 128 x 128
+ *   output tiles than CUs, M < 1024): given that much, the call splits K
+ *   across work-groups and sums the exact int32 partials in a second kernel;
+ *   with ws NULL, smaller or misaligned it runs unsplit.  The results are
+ *   identical either way (integer sums).
  * Limits: M >= 1, N_out >= 1, K_in % 32 == 0, 32 <= K_in <= 131072,
  *   ldy >= N_out; code pointers 16-byte aligned, y 4-byte aligned.
  * ---------------------------------------------------------------------- */

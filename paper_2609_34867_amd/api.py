@@ -298,7 +298,10 @@ def w4a4_linear(a_codes: torch.Tensor, a_scales: torch.Tensor, w_codes: torch.Te
                 y: Optional[torch.Tensor] = None, acc_out: Optional[torch.Tensor] = None,
                 return_acc: bool = False, workspace: Optional[torch.Tensor] = None):
     """W4A4 linear (p4q_w4a4_linear): a_codes [M, K_in/2], w_codes [N_out, K_in/2]
-    -> y [M, N_out] (out_dtype); also the int32 accumulators when return_acc."""
+    -> y [M, N_out] (out_dtype); also the int32 accumulators when return_acc.
+    Without `workspace` one of the size the library asks for is allocated
+    (small M splits K across work-groups with it); a smaller one, e.g.
+    empty, runs the unsplit kernel.  Results are identical either way."""
     _need_gpu(a_codes, a_scales, w_codes, w_scales)
     M, kb = a_codes.shape
     N_out, kb2 = w_codes.shape

@@ -215,9 +215,6 @@ int p4q_w4a4_linear(int M, int N_out, int K_in, const uint8_t *a_codes, const fl
         !aligned(w_scales, 4) || (acc_out && !aligned(acc_out, 4)))
         return fail(P4Q_ERR_INVALID_ARG, "p4q_w4a4_linear: misaligned pointer");
     if ((int64_t)M > 65535LL * 128) return fail(P4Q_ERR_UNSUPPORTED, "p4q_w4a4_linear: M too large");
-    const size_t need = p4q::gemm_workspace_bytes(M, N_out, K_in);
-    if (need > 0 && (!ws || ws_bytes < need))
-        return fail(P4Q_ERR_WORKSPACE, "p4q_w4a4_linear: workspace %zu < %zu bytes", ws_bytes, need);
     return hip_status(p4q::launch_w4a4_gemm(M, N_out, K_in, a_codes, a_scales, w_codes, w_scales,
                                             out_dt, y, ldy, acc_out, ws, ws_bytes, stream),
                       "p4q_w4a4_linear");

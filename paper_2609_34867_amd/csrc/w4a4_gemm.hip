@@ -162,6 +162,197 @@ __global__ __launch_bounds__(kThreads) void k_w4a4_gemm(const uint8_t *__restric
 
 
 // ---------------------------------------------------------------------------
+// Small-M kernel (M < 1024: one image's pruned sequence): the same 128 x 128
+// tile as k_w4a4_gemm, computed by 8 wavefronts in two K-slices.  At these M
+// there are only 1-2 tiles per CU; two slices put two wavefronts of the tile
+// on every SIMD, so one's LDS reads, unpacking and barrier waits overlap the
+// other's MFMAs, with no partial sums leaving the chip: slice 1 hands its
+// accumulators to slice 0 through LDS at the end.
+//  * Stage = 256 k (two 64-byte halves of a 128-byte LDS row per operand
+//    row; slice s reads half s).  16-byte chunk c of row r sits at chunk
+//    c ^ ((r >> 1) & 7): the 16 rows of one fragment read hit distinct banks.
+//  * Global -> registers -> LDS double buffering, as k_w4a4_gemm.
+// ---------------------------------------------------------------------------
+constexpr int KS_THREADS = 512;
+constexpr int KS_ROW = 128;                 // LDS row bytes (256 k)
+constexpr int KS_STAGE = 2 * BM * KS_ROW;   // A and W: 32 KB
+
+__device__ __forceinline__ int ks_off(int row, int c) {
+    return row * KS_ROW + ((c ^ ((row >> 1) & 7)) << 4);
+}
+
+// SPLIT: blockIdx.z covers k-tiles [z kps, (z + 1) kps) and the block
+// writes its exact partial sums to part[z][M][N] (int32) instead of y; a
+// second kernel adds the partials and applies the epilogue.
+template <bool BF16OUT, bool SPLIT>
+__global__ __launch_bounds__(KS_THREADS, 2) void k_w4a4_gemm_ks(
+    const uint8_t *__restrict__ A, const float *__restrict__ sa, const uint8_t *__restrict__ W,
+    const float *__restrict__ sw, int M, int N, int Kb, void *__restrict__ y, int64_t ldy,
+    int32_t *__restrict__ acc_out, int kps, int32_t *__restrict__ part) {
+    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * KS_STAGE];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int slice = wave >> 2, wm = (wave >> 1) & 1, wn = wave & 1;
+    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+    const int kt_all = (Kb + KS_ROW - 1) / KS_ROW;
+    const int kt0 = SPLIT ? (int)blockIdx.z * kps : 0;
+    const int ktiles = SPLIT ? min(kps, kt_all - kt0) : kt_all;
+
+    // staging: per operand 128 rows x 8 chunks = 1024 chunks, 2 per thread
+    int lrow[2], lc[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int q = t + KS_THREADS * i;
+        lrow[i] = q >> 3;
+        lc[i] = q & 7;
+    }
+    uint4 ra[2], rb[2];
+    auto gload = [&](int kt) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int kbyte = (kt0 + kt) * KS_ROW + lc[i] * 16;
+            const int ar = m0 + lrow[i], br = n0 + lrow[i];
+            ra[i] = (ar < M && kbyte < Kb)
+                        ? *reinterpret_cast<const uint4 *>(A + (int64_t)ar * Kb + kbyte)
+                        : make_uint4(0, 0, 0, 0);
+            rb[i] = (br < N && kbyte < Kb)
+                        ? *reinterpret_cast<const uint4 *>(W + (int64_t)br * Kb + kbyte)
+                        : make_uint4(0, 0, 0, 0);
+        }
+    };
+    auto sstore = [&](int st) {
+        uint8_t *sA = smem + st * KS_STAGE, *sB = sA + BM * KS_ROW;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            *reinterpret_cast<uint4 *>(sA + ks_off(lrow[i], lc[i])) = ra[i];
+            *reinterpret_cast<uint4 *>(sB + ks_off(lrow[i], lc[i])) = rb[i];
+        }
+    };
+
+    v4i acc[4][4];
+#pragma unroll
+    for (int f = 0; f < 4; ++f)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acc[f][g] = v4i{0, 0, 0, 0};
+
+    if (ktiles > 0) gload(0);
+    sstore(0);
+    __syncthreads();
+    const int c = 4 * slice + (lane >> 4);       // this lane's chunk of a row
+    for (int kt = 0; kt < ktiles; ++kt) {
+        const int st = kt & 1;
+        if (kt + 1 < ktiles) gload(kt + 1);
+        const uint8_t *sA = smem + st * KS_STAGE, *sB = sA + BM * KS_ROW;
+        v4i a0[4], a1[4], b0[4], b1[4];
+#pragma unroll
+        for (int f = 0; f < 4; ++f) {
+            const int ar = wm * 64 + f * 16 + (lane & 15);
+            const uint4 pa = *reinterpret_cast<const uint4 *>(sA + ks_off(ar, c));
+            a0[f] = v4i{(int)nib_lo(pa.x), (int)nib_hi(pa.x), (int)nib_lo(pa.y), (int)nib_hi(pa.y)};
+            a1[f] = v4i{(int)nib_lo(pa.z), (int)nib_hi(pa.z), (int)nib_lo(pa.w), (int)nib_hi(pa.w)};
+            const int br = wn * 64 + f * 16 + (lane & 15);
+            const uint4 pb = *reinterpret_cast<const uint4 *>(sB + ks_off(br, c));
+            b0[f] = v4i{(int)nib_lo(pb.x), (int)nib_hi(pb.x), (int)nib_lo(pb.y), (int)nib_hi(pb.y)};
+            b1[f] = v4i{(int)nib_lo(pb.z), (int)nib_hi(pb.z), (int)nib_lo(pb.w), (int)nib_hi(pb.w)};
+        }
+#pragma unroll
+        for (int f = 0; f < 4; ++f)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                acc[f][g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0[f], b0[g], acc[f][g], 0, 0, 0);
+#pragma unroll
+        for (int f = 0; f < 4; ++f)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                acc[f][g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1[f], b1[g], acc[f][g], 0, 0, 0);
+        if (kt + 1 < ktiles) sstore(st ^ 1);
+        __syncthreads();
+    }
+
+    // slice 1 -> LDS ([wave][register][lane], 16 KB per wavefront), slice 0 adds
+    int32_t *red = reinterpret_cast<int32_t *>(smem) + (wave & 3) * (64 * 64);
+    if (slice == 1) {
+#pragma unroll
+        for (int f = 0; f < 4; ++f)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) red[((f * 4 + g) * 4 + e) * 64 + lane] = acc[f][g][e];
+    }
+    __syncthreads();
+    if (slice == 1) return;
+#pragma unroll
+    for (int f = 0; f < 4; ++f)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[f][g][e] += red[((f * 4 + g) * 4 + e) * 64 + lane];
+
+    // epilogue: lane holds rows 4*(lane>>4)+e, column lane&15 of each 16x16 tile
+    if constexpr (SPLIT) {
+        int32_t *pz = part + (int64_t)blockIdx.z * M * N;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int n = n0 + wn * 64 + g * 16 + (lane & 15);
+#pragma unroll
+            for (int f = 0; f < 4; ++f)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int m = m0 + wm * 64 + f * 16 + 4 * (lane >> 4) + e;
+                    if (m < M && n < N) pz[(int64_t)m * N + n] = acc[f][g][e] >> 8;
+                }
+        }
+        return;
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const int n = n0 + wn * 64 + g * 16 + (lane & 15);
+        const float swn = (n < N) ? sw[n] : 0.0f;
+#pragma unroll
+        for (int f = 0; f < 4; ++f) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int m = m0 + wm * 64 + f * 16 + 4 * (lane >> 4) + e;
+                if (m < M && n < N) {
+                    const int v = acc[f][g][e] >> 8;
+                    const float t1 = __fmul_rn((float)v, sa[m]);
+                    store_out<BF16OUT>(y, (int64_t)m * ldy + n, __fmul_rn(t1, swn));
+                    if (acc_out) acc_out[(int64_t)m * N + n] = v;
+                }
+            }
+        }
+    }
+}
+
+// sum of the S partial accumulators (exact integers), then the epilogue of
+// the unsplit kernels; 4 consecutive outputs per thread (N % 4 == 0)
+template <bool BF16OUT>
+__global__ __launch_bounds__(256) void k_splitk_epilogue(const int32_t *__restrict__ part, int S,
+                                                         int M, int N, const float *__restrict__ sa,
+                                                         const float *__restrict__ sw,
+                                                         void *__restrict__ y, int64_t ldy,
+                                                         int32_t *__restrict__ acc_out) {
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t total = (int64_t)M * N / 4;
+    if (q >= total) return;
+    const int64_t o = 4 * q;
+    const int m = (int)(o / N), n = (int)(o % N);
+    int4 v = *reinterpret_cast<const int4 *>(part + o);
+    for (int z = 1; z < S; ++z) {
+        const int4 p = *reinterpret_cast<const int4 *>(part + (int64_t)z * M * N + o);
+        v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+    }
+    const int vv[4] = {v.x, v.y, v.z, v.w};
+    const float sam = sa[m];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        store_out<BF16OUT>(y, (int64_t)m * ldy + n + e, __fmul_rn(__fmul_rn((float)vv[e], sam), sw[n + e]));
+    if (acc_out) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc_out[o + e] = vv[e];
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Large-M kernel: 256 (m) x 128 (n) block tile, 4 wavefronts of 128 x 64
 // (4 x 8 tiles of v_mfma_i32_16x16x64_i8, 128 accumulator registers), and
 // at most 256 registers per lane, so TWO blocks are resident per CU: one
@@ -639,11 +830,31 @@ __global__ __launch_bounds__(64 * G_WAVES) void k_w4a4_gemv(const uint8_t *__res
 
 }  // namespace
 
-size_t gemm_workspace_bytes(int, int, int) { return 0; }
+// Small-M shapes with fewer 128 x 128 tiles than CUs split K across
+// work-groups (exact int32 partials, summed by the epilogue kernel):
+// S = ceil(256 / tiles), at most 4, each slice at least 4 k-tiles of 256.
+// Not for the decode GEMV or the large-M kernel (M >= 1024 and N >= 1024),
+// nor when N % 4 != 0 (the epilogue writes 4 outputs per thread).
+static int small_m_splits(int M, int N, int K) {
+    if (M <= 16 || (M >= 1024 && N >= 1024) || N % 4 != 0) return 1;
+    const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    const int kt_all = (K / 2 + KS_ROW - 1) / KS_ROW;
+    if (tiles >= 256) return 1;
+    int S = (256 + tiles - 1) / tiles;
+    S = std::min(S, 4);
+    S = std::min(S, kt_all / 4);
+    return std::max(S, 1);
+}
+
+size_t gemm_workspace_bytes(int M, int N, int K) {
+    const int S = small_m_splits(M, N, K);
+    return S > 1 ? (size_t)S * M * N * 4 : 0;
+}
 
 hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *sa,
                             const uint8_t *w, const float *sw, p4q_dtype out_dt, void *y,
-                            int64_t ldy, int32_t *acc_out, void *, size_t, hipStream_t stream) {
+                            int64_t ldy, int32_t *acc_out, void *ws, size_t ws_bytes,
+                            hipStream_t stream) {
     const bool bf16 = (out_dt == P4Q_BF16);
     // decode kernel: 32-bit buffer offsets need N * K_in / 2 < 2^31
     if (M <= 16 && K <= 128 * G_WAVES * G_MAX_BATCH && (int64_t)N * (K / 2) < 0x7FFF0000LL) {
@@ -686,12 +897,32 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
         return acc_out ? go(k_w4a4_gemm_2cu<false, true, true>) : go(k_w4a4_gemm_2cu<false, false, true>);
     }
     const dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
+    const int S = small_m_splits(M, N, K);
+    if (S > 1 && ws && ((uintptr_t)ws & 15) == 0 && ws_bytes >= gemm_workspace_bytes(M, N, K)) {
+        const int kt_all = (K / 2 + KS_ROW - 1) / KS_ROW, kps = (kt_all + S - 1) / S;
+        int32_t *part = static_cast<int32_t *>(ws);
+        const dim3 gs(grid.x, grid.y, (kt_all + kps - 1) / kps);
+        const int Sr = (int)gs.z;
+        const unsigned eb = (unsigned)(((int64_t)M * N / 4 + 255) / 256);
+        if (bf16) {
+            hipLaunchKernelGGL((k_w4a4_gemm_ks<true, true>), gs, dim3(KS_THREADS), 0, stream, a, sa,
+                               w, sw, M, N, K / 2, y, ldy, acc_out, kps, part);
+            hipLaunchKernelGGL(k_splitk_epilogue<true>, dim3(eb), dim3(256), 0, stream, part, Sr, M,
+                               N, sa, sw, y, ldy, acc_out);
+        } else {
+            hipLaunchKernelGGL((k_w4a4_gemm_ks<false, true>), gs, dim3(KS_THREADS), 0, stream, a, sa,
+                               w, sw, M, N, K / 2, y, ldy, acc_out, kps, part);
+            hipLaunchKernelGGL(k_splitk_epilogue<false>, dim3(eb), dim3(256), 0, stream, part, Sr, M,
+                               N, sa, sw, y, ldy, acc_out);
+        }
+        return hipGetLastError();
+    }
     if (bf16)
-        hipLaunchKernelGGL(k_w4a4_gemm<true>, grid, dim3(kThreads), 0, stream, a, sa, w, sw, M, N,
-                           K / 2, y, ldy, acc_out);
+        hipLaunchKernelGGL((k_w4a4_gemm_ks<true, false>), grid, dim3(KS_THREADS), 0, stream, a, sa,
+                           w, sw, M, N, K / 2, y, ldy, acc_out, 0, nullptr);
     else
-        hipLaunchKernelGGL(k_w4a4_gemm<false>, grid, dim3(kThreads), 0, stream, a, sa, w, sw, M,
-                           N, K / 2, y, ldy, acc_out);
+        hipLaunchKernelGGL((k_w4a4_gemm_ks<false, false>), grid, dim3(KS_THREADS), 0, stream, a, sa,
+                           w, sw, M, N, K / 2, y, ldy, acc_out, 0, nullptr);
     return hipGetLastError();
 }
 

@@ -124,3 +124,23 @@ def test_calib_llava_next_qkv():
     N = 12288, K = 4096) on one pruned calibration sample (M = 320 + 64)."""
     p = calib_problem(72, 384, 12288, 4096, "fp16", clip_a=0.9)
     compare(p, run_calib(p))
+
+
+def test_calib_llava_next_down_proj_bf16():
+    """down_proj's shape (K = 11008 inputs, 86 channel tiles) in bf16, on the
+    same pruned calibration sample."""
+    p = calib_problem(73, 384, 4096, 11008, "bf16", clip_a=0.8)
+    compare(p, run_calib(p))
+
+
+def test_calib_workspace_reuse_across_shapes():
+    """One workspace sized for the larger problem serves a smaller one; the
+    second call's results do not depend on what the first left behind."""
+    big = calib_problem(74, 256, 512, 1024, "fp16")
+    small = calib_problem(75, 40, 128, 256, "fp16")
+    ws = p4q.calib_linear_workspace(256, 512, 1024, torch.device("cuda:0"))
+    for p in (big, small):
+        out = p4q.calib_linear_grad(to_gpu(p.x), to_gpu(p.w), to_gpu(p.target), to_gpu(p.sigma),
+                                    p.clip_a, to_gpu(p.clip_w), workspace=ws)
+        torch.cuda.synchronize()
+        compare(p, [to_np(t).astype(np.float64) for t in out])

@@ -222,3 +222,23 @@ def test_decode_graph_replay_matches_eager():
         for r, yv in zip(ref, ys):
             assert torch.equal(r.view(torch.int16), yv.view(torch.int16)), rep
         del junk
+
+
+@pytest.mark.parametrize("shape", [(384, 4096, 11008), (256, 4096, 4096), (96, 512, 4096),
+                                   (704, 4096, 4096)])
+def test_small_m_split_k(shape):
+    """Batch-1 shapes (one image's pruned sequence): fewer 128 x 128 tiles
+    than CUs, so K is split across work-groups when the workspace is given.
+    Both paths must equal the oracle bit for bit."""
+    M, N, K = shape
+    assert p4q.lib().p4q_w4a4_linear_workspace_bytes(M, N, K) > 0
+    ap, sa, wp, sw = codes_for(M, N, K, seed=M + N)
+    racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
+    dev = torch.device("cuda:0")
+    empty = torch.empty(0, dtype=torch.uint8, device=dev)      # zero bytes: the unsplit path
+    for ws in (None, empty):
+        y, acc = p4q.w4a4_linear(to_gpu(ap), to_gpu(sa), to_gpu(wp), to_gpu(sw), torch.bfloat16,
+                                 return_acc=True, workspace=ws)
+        torch.cuda.synchronize()
+        assert (m := first_mismatch(to_np(acc), racc.astype(np.int32))) is None, m
+        assert (m := first_mismatch(bits(to_np(y)), bits(ry))) is None, m
