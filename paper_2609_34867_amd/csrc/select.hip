@@ -6,8 +6,8 @@
 //  2. k_select_score: one pass over the visual features.  Each wavefront
 //     holds one token row in registers, takes its absmax, quantizes it
 //     on-chip (the fake-quantized copy is never written), and forms the exact
-//     integer statistics D_ij = <cv_i, cq_j> and Nv_i = |cv_i|^2 with packed
-//     int8 dot products against concept codes staged in LDS.  It also turns
+//     integer statistics D_ij = <cv_i, cq_j> and Nv_i = |cv_i|^2 with 8-wide
+//     int4 dot products against packed concept codes staged in LDS.  It also turns
 //     (D_ij, Nv_i) into an exact integer order key (see exact_key).
 //  3. k_select_topk: one workgroup per sample.  For each concept in order it
 //     radix-selects the quota's largest (key, -index) composites among tokens

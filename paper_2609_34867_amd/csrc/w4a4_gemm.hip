@@ -53,6 +53,9 @@ __device__ __forceinline__ void store_out(void *y, int64_t off, float v) {
     }
 }
 
+// 128 x 128 tile, 4 wavefronts of 64 x 64, register-staged double
+// buffering.  Serves the code Gram matrices of images with fewer than 1024
+// tokens (y == nullptr: int32 accumulators only, no scales read).
 template <bool BF16OUT>
 __global__ __launch_bounds__(kThreads) void k_w4a4_gemm(const uint8_t *__restrict__ A,
                                                         const float *__restrict__ sa,
