@@ -153,6 +153,9 @@ __global__ __launch_bounds__(256, 2) void k_attention(const uint16_t *__restrict
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {                    // 32-key halves
             const int k0 = kt * kKT + 32 * hf;
+            // a half past this wavefront's last query holds only masked
+            // keys (weight 0): skipping it leaves m, lsum and O unchanged
+            if (CAUSAL && k0 > qw0 + kQW - 1) continue;
             // S^T = K Q^T: lane holds query c32, keys k0 + 8(r/4) + 4g + r%4
             v16f st = v16f{};
 #pragma unroll
