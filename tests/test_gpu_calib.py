@@ -144,3 +144,14 @@ def test_calib_workspace_reuse_across_shapes():
                                     p.clip_a, to_gpu(p.clip_w), workspace=ws)
         torch.cuda.synchronize()
         compare(p, [to_np(t).astype(np.float64) for t in out])
+
+
+def test_calib_heavy_clamping():
+    """Small clipping factors (most values saturate: the clamp's gradient
+    mask and the code range edges -8 / 7 dominate) on both sides."""
+    p = calib_problem(76, 130, 192, 512, "fp16", clip_a=0.2)
+    p.clip_w = np.random.default_rng(76).uniform(0.1, 0.3, 192).astype(np.float32)
+    ref = compare(p, run_calib(p))
+    # the activations' outlier channels set their row maxima, so fewer of
+    # their values saturate than the weights'
+    assert np.mean(np.abs(ref["a_codes"]) >= 7) > 0.02 and np.mean(np.abs(ref["w_codes"]) >= 7) > 0.3
