@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--no-calib", action="store_true", help="skip the calibration-step measurement")
     ap.add_argument("--calib-only", action="store_true",
                     help="measure only the calibration step (for profiling it alone)")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="measure only the decode GEMV layer (for profiling it alone)")
     ap.add_argument("--no-select-full", action="store_true",
                     help="skip the three-stage selector measurement")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -474,6 +476,9 @@ def main():
         return
     if args.calib_only:
         print(json.dumps({"calibration_step": calibration(dev)}), flush=True)
+        return
+    if args.decode_only:
+        print(json.dumps({"decode_gemv": decode_gemv(dev)}), flush=True)
         return
     st = setup(cfg, dev)
     for i in range(args.warmup):

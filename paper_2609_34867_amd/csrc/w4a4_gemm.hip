@@ -53,6 +53,18 @@ __device__ __forceinline__ void store_out(void *y, int64_t off, float v) {
     }
 }
 
+// bits of one output value (same roundings as store_out)
+template <bool BF16OUT>
+__device__ __forceinline__ uint32_t out_bits(float v) {
+    if constexpr (BF16OUT) {
+        const uint32_t u = __float_as_uint(v);
+        return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    } else {
+        asm volatile("" : "+v"(v));                          // see store_out
+        return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v);
+    }
+}
+
 // 128 x 128 tile, 4 wavefronts of 64 x 64, register-staged double
 // buffering.  Serves the code Gram matrices of images with fewer than 1024
 // tokens (y == nullptr: int32 accumulators only, no scales read).
@@ -703,45 +715,56 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
 // ---------------------------------------------------------------------------
 // Decode-shaped kernel (M <= 16): the weights are streamed from HBM once, so
 // the kernel is bound by HBM bandwidth and by how many bytes are in flight.
-// A 512-thread work-group computes 16 output rows (one MFMA fragment) at a
-// time; its 8 wavefronts split K into contiguous ranges of at most G_BATCH
-// 128-value k-tiles.  Work-groups are persistent: each walks row groups
-// blockIdx.x, blockIdx.x + gridDim.x, ... and loads the next group's
-// fragments before computing on the current ones, so HBM latency overlaps
-// with the MFMAs, the reduction and the epilogue.  Every weight byte is used
-// exactly once, so fragments go straight from HBM to registers.  The M
-// activation rows (zero-filled to 16 by the buffer range check) are the
-// MFMA's second operand.  Per k-tile, lane (r, c) loads the 16 bytes at
-// [64 kt + 16 c, +16) of weight row r and of activation row r; both operands
-// use the same k placement, so the MFMA sums every k exactly once.  The 8
-// partial accumulators are summed through LDS (integer sums: exact and
+// A work-group of NW wavefronts (8, or 16 for long rows) computes 16 output
+// rows (one MFMA fragment) at a time.  Work-groups are persistent: each walks row groups blockIdx.x,
+// blockIdx.x + gridDim.x, ... and loads the next group's weights before
+// computing on the current ones, so HBM latency overlaps with the MFMAs, the
+// reduction and the epilogue.
+//
+// The 16 rows of a group are one contiguous block of 16 * Kb bytes.  Each
+// wavefront loads 16 / NW whole rows of it, 1 KB of consecutive bytes per
+// instruction, and the block passes through LDS (row stride: an odd number of
+// 16-byte chunks, so the 16 rows of a fragment read fall in distinct banks)
+// to reach the MFMA layout.  Loading the fragments straight from HBM would
+// make every quarter-wavefront touch 16 rows with 16 bytes each.
+//
+// For the contraction, the NW wavefronts split K into contiguous ranges of at
+// most G_BATCH 128-value k-tiles.  Per k-tile, lane (r, c) takes the 16
+// bytes at [64 kt + 16 c, +16) of weight row r (from LDS) and of activation
+// row r (from HBM, once per wavefront; rows past M read as zeros): both
+// operands use the same k placement, so the MFMA sums every k exactly once.
+// The NW partial accumulators are summed through LDS (integer sums: exact and
 // order-independent) before the epilogue.
 // ---------------------------------------------------------------------------
 constexpr int G_ROWS = 16;
-constexpr int G_WAVES = 8;
-constexpr int G_MAX_BATCH = 14;             // k-tiles per wavefront: K_in <= 14336
+constexpr int G_MAX_KIN = 14336;            // 7 k-tiles for each of 16 wavefronts
 
 // range-checked 16-byte load: offsets at or past the range read as zeros
 __device__ __forceinline__ uint4 gbuf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
 }
 
-template <int G_BATCH, bool BF16OUT>
-__global__ __launch_bounds__(64 * G_WAVES) void k_w4a4_gemv(const uint8_t *__restrict__ A,
+template <int G_BATCH, int NW, bool BF16OUT>
+__global__ __launch_bounds__(64 * NW) void k_w4a4_gemv(const uint8_t *__restrict__ A,
                                                             const float *__restrict__ sa,
                                                             const uint8_t *__restrict__ W,
                                                             const float *__restrict__ sw, int M,
                                                             int N, int Kb, void *__restrict__ y,
                                                             int64_t ldy,
                                                             int32_t *__restrict__ acc_out) {
-    __shared__ v4i red[2][G_WAVES][64];                     // 16 KB, double-buffered
+    // Kb <= 64 NW G_BATCH, so a row holds at most 4 NW G_BATCH chunks of 16 bytes
+    __shared__ uint4 stage[G_ROWS * (4 * NW * G_BATCH + 1)];
+    __shared__ v4i red[NW][64];
+    constexpr int RPW = G_ROWS / NW;                        // rows staged per wavefront
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r = lane & 15, c = lane >> 4;
     const int ktiles = (Kb + 63) / 64;
-    const int kt0 = (int)((int64_t)ktiles * wave / G_WAVES);
-    const int nk = (int)((int64_t)ktiles * (wave + 1) / G_WAVES) - kt0;   // <= G_BATCH
+    const int kt0 = (int)((int64_t)ktiles * wave / NW);
+    const int nk = (int)((int64_t)ktiles * (wave + 1) / NW) - kt0;   // <= G_BATCH
     const int groups = (N + G_ROWS - 1) / G_ROWS;
+    const int kc = Kb >> 4;                                 // 16-byte chunks per row
+    const int rs = kc | 1;                                  // LDS row stride in chunks (odd)
 
     // whole-matrix descriptors: rows past N or M fall outside the ranges and
     // read as zero
@@ -755,11 +778,19 @@ __global__ __launch_bounds__(64 * G_WAVES) void k_w4a4_gemv(const uint8_t *__res
     for (int u = 0; u < G_BATCH; ++u)
         if (u < nk && 64 * (kt0 + u) + 16 * c < Kb) kin |= 1u << u;
 
+    // staging: chunk f = 64 u + lane of this wavefront's rows RPW wave, ...,
+    // RPW wave + RPW - 1 (bit u of sin: f < RPW kc); its LDS slot skips the
+    // padding
+    uint32_t sin = 0;
+#pragma unroll
+    for (int u = 0; u < G_BATCH; ++u)
+        if (64 * u + lane < RPW * kc) sin |= 1u << u;
+    const uint32_t soff = (uint32_t)(RPW * wave * Kb + 16 * lane);
     auto load_w = [&](int g, uint4 *w) {
-        const uint32_t base = (uint32_t)(g * G_ROWS) * (uint32_t)Kb + off;
+        const uint32_t base = (uint32_t)(g * G_ROWS) * (uint32_t)Kb + soff;
 #pragma unroll
         for (int u = 0; u < G_BATCH; ++u)
-            w[u] = gbuf_load16(dW, ((kin >> u) & 1) ? base + 64 * u : 0x80000000u);
+            w[u] = gbuf_load16(dW, ((sin >> u) & 1) ? base + 1024 * u : 0x80000000u);
     };
     auto unpack = [](uint32_t w0, uint32_t w1) {
         return v4i{(int)nib_lo(w0), (int)nib_hi(w0), (int)nib_lo(w1), (int)nib_hi(w1)};
@@ -780,6 +811,10 @@ __global__ __launch_bounds__(64 * G_WAVES) void k_w4a4_gemv(const uint8_t *__res
                                               dS, (uint32_t)(g * G_ROWS + 4 * (lane >> 4)) * 4u, 0, 0));
     };
 
+    // 4 consecutive outputs per lane go out as one 8-byte store when aligned
+    const bool vec_y = ((reinterpret_cast<uintptr_t>(y) & 7) == 0) && ((ldy & 3) == 0);
+    const bool vec_acc = ((reinterpret_cast<uintptr_t>(acc_out) & 15) == 0) && ((N & 3) == 0);
+
     int g = blockIdx.x;
     uint4 wc[G_BATCH];
     float4 swc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -787,47 +822,72 @@ __global__ __launch_bounds__(64 * G_WAVES) void k_w4a4_gemv(const uint8_t *__res
         load_w(g, wc);
         swc = load_sw(g);
     }
-    for (int it = 0; g < groups; g += gridDim.x, ++it) {
-        uint4 wn[G_BATCH];
-        float4 swn = make_float4(0.f, 0.f, 0.f, 0.f);
-        const int gn = g + gridDim.x;
-        if (gn < groups) {                                   // prefetch the next group
-            load_w(gn, wn);
-            swn = load_sw(gn);
+    for (; g < groups; g += gridDim.x) {
+        // the previous group's fragment reads ended at its reduction barrier
+#pragma unroll
+        for (int u = 0; u < G_BATCH; ++u) {
+            if ((sin >> u) & 1) {
+                const int f = 64 * u + lane;
+                stage[RPW * wave * rs + f + (RPW > 1 && f >= kc ? rs - kc : 0)] = wc[u];
+            }
         }
+        // with the block in LDS its registers take the next group's loads
+        const float4 sws = swc;
+        const int gn = g + gridDim.x;
+        if (gn < groups) {
+            load_w(gn, wc);
+            swc = load_sw(gn);
+        }
+        __syncthreads();
         v4i acc = v4i{0, 0, 0, 0};
 #pragma unroll
         for (int u = 0; u < G_BATCH; ++u) {
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack(wc[u].x, wc[u].y),
+            const uint4 wf = ((kin >> u) & 1) ? stage[r * rs + 4 * (kt0 + u) + c]
+                                              : make_uint4(0u, 0u, 0u, 0u);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack(wf.x, wf.y),
                                                         unpack(a[u].x, a[u].y), acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack(wc[u].z, wc[u].w),
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack(wf.z, wf.w),
                                                         unpack(a[u].z, a[u].w), acc, 0, 0, 0);
         }
-        const int buf = it & 1;
-        red[buf][wave][lane] = acc;
+        red[wave][lane] = acc;
         __syncthreads();
+        // wave 0 reads red before it reaches the next group's first barrier,
+        // and no wavefront writes red again before that barrier
         if (wave == 0) {
-            v4i s = red[buf][0][lane];
+            v4i s = red[0][lane];
 #pragma unroll
-            for (int w = 1; w < G_WAVES; ++w) s += red[buf][w][lane];
+            for (int w = 1; w < NW; ++w) s += red[w][lane];
             const int nb = g * G_ROWS + 4 * (lane >> 4);
-            const float swv[4] = {swc.x, swc.y, swc.z, swc.w};
+            const float swv[4] = {sws.x, sws.y, sws.z, sws.w};
             if (m < M) {
+                if (vec_y && nb + 3 < N) {                   // one 8-byte store per lane
+                    uint32_t h[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int n = nb + e;
-                    if (n < N) {
-                        const int v = s[e] >> 8;
-                        store_out<BF16OUT>(y, (int64_t)m * ldy + n,
-                                           __fmul_rn(__fmul_rn((float)v, sam), swv[e]));
-                        if (acc_out) acc_out[(int64_t)m * N + n] = v;
+                    for (int e = 0; e < 4; ++e)
+                        h[e] = out_bits<BF16OUT>(__fmul_rn(__fmul_rn((float)(s[e] >> 8), sam), swv[e]));
+                    *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(y) + (int64_t)m * ldy + nb) =
+                        make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                    if (acc_out) {
+                        if (vec_acc)
+                            *reinterpret_cast<v4i *>(acc_out + (int64_t)m * N + nb) =
+                                v4i{s[0] >> 8, s[1] >> 8, s[2] >> 8, s[3] >> 8};
+                        else
+                            for (int e = 0; e < 4; ++e) acc_out[(int64_t)m * N + nb + e] = s[e] >> 8;
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int n = nb + e;
+                        if (n < N) {
+                            const int v = s[e] >> 8;
+                            store_out<BF16OUT>(y, (int64_t)m * ldy + n,
+                                               __fmul_rn(__fmul_rn((float)v, sam), swv[e]));
+                            if (acc_out) acc_out[(int64_t)m * N + n] = v;
+                        }
                     }
                 }
             }
         }
-#pragma unroll
-        for (int u = 0; u < G_BATCH; ++u) wc[u] = wn[u];
-        swc = swn;
     }
 }
 
@@ -860,7 +920,7 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
                             hipStream_t stream) {
     const bool bf16 = (out_dt == P4Q_BF16);
     // decode kernel: 32-bit buffer offsets need N * K_in / 2 < 2^31
-    if (M <= 16 && K <= 128 * G_WAVES * G_MAX_BATCH && (int64_t)N * (K / 2) < 0x7FFF0000LL) {
+    if (M <= 16 && K <= G_MAX_KIN && (int64_t)N * (K / 2) < 0x7FFF0000LL) {
         static int cus = 0;
         if (cus == 0) {
             int dev = 0;
@@ -870,21 +930,23 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
                 cus = 256;
         }
         const int groups = (N + G_ROWS - 1) / G_ROWS;
-        const int per_wave = ((K + 127) / 128 + G_WAVES - 1) / G_WAVES;   // k-tiles per wavefront
-        auto go = [&](auto kern, int blocks_per_cu) {
-            hipLaunchKernelGGL(kern, dim3(min(groups, blocks_per_cu * cus)), dim3(64 * G_WAVES), 0,
+        const int ktiles = (K + 127) / 128;
+        auto go = [&](auto kern, int nw, int blocks_per_cu) {
+            hipLaunchKernelGGL(kern, dim3(min(groups, blocks_per_cu * cus)), dim3(64 * nw), 0,
                                stream, a, sa, w, sw, M, N, K / 2, y, ldy, acc_out);
             return hipGetLastError();
         };
-#define P4Q_GEMV(NB, BPC)                                                                   \
-    if (per_wave <= NB)                                                                    \
-        return bf16 ? go(k_w4a4_gemv<NB, true>, BPC) : go(k_w4a4_gemv<NB, false>, BPC);
-        P4Q_GEMV(2, 2)
-        P4Q_GEMV(4, 2)
-        P4Q_GEMV(6, 2)
-        P4Q_GEMV(8, 1)
-        P4Q_GEMV(11, 1)
-        P4Q_GEMV(14, 1)
+        // up to 6 k-tiles per wavefront: 8 wavefronts, two work-groups per CU;
+        // longer rows: 16 wavefronts (at most 7 k-tiles each), one per CU
+#define P4Q_GEMV(NB, NW, BPC)                                                               \
+    if (ktiles <= NB * NW)                                                                 \
+        return bf16 ? go(k_w4a4_gemv<NB, NW, true>, NW, BPC)                               \
+                    : go(k_w4a4_gemv<NB, NW, false>, NW, BPC);
+        P4Q_GEMV(2, 8, 2)
+        P4Q_GEMV(4, 8, 2)
+        P4Q_GEMV(6, 8, 2)
+        P4Q_GEMV(5, 16, 1)
+        P4Q_GEMV(7, 16, 1)
 #undef P4Q_GEMV
     }
     if (M >= 1024 && N >= 1024) {
