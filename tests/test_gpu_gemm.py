@@ -144,11 +144,14 @@ def test_llava_next_b16_fused_projections_sampled(members):
 
 
 @pytest.mark.parametrize("M", [1, 2, 4, 7, 16])
-@pytest.mark.parametrize("NK", [(5120, 5120), (5120, 13824), (1000, 4128), (33, 32), (47, 224)])
+@pytest.mark.parametrize("NK", [(5120, 5120), (5120, 13824), (1000, 4128), (33, 32), (47, 224),
+                                (200, 6176), (200, 8224), (72, 14336)])
 def test_decode_gemv_shapes(M, NK):
     """M <= 16 runs the HBM-streaming decode kernel: ragged N (not a multiple
-    of its 32-row groups), K not a multiple of its 128-value k-tiles, K split
-    unevenly over its 8 wavefronts, every M in the padded 16-row operand."""
+    of its 16-row groups), K not a multiple of its 128-value k-tiles, K split
+    unevenly over its wavefronts (8 up to K = 6144, 16 beyond: 6176 and 8224
+    are the first rows past a launch-shape boundary, 14336 the longest row),
+    every M in the padded 16-row operand."""
     N, K = NK
     check_full(*codes_for(M, N, K, 31 * M + N + K), "bf16" if M % 2 else "fp16")
 
