@@ -274,6 +274,70 @@ __global__ __launch_bounds__(kThreads) void k_codes_bf16t(const uint8_t *__restr
     }
 }
 
+// Wide variant for the weight codes (many rows): a 256-row x 128-k tile, so
+// each half-wavefront writes 512 consecutive bytes of one output row.  The
+// int8 tile sits in LDS as [row][32 words of 4 k]; word q of row r is stored
+// at slot q ^ g(r), g(r) = ((r >> 3) ^ ((r & 7) << 2)) & 31, so the 32 lanes
+// that read rows 8 rc + j (rc = 0 .. 31) at one word hit 32 distinct banks.
+constexpr int kTWide = 256;
+
+__device__ __forceinline__ int wide_swz(int r) { return ((r >> 3) ^ ((r & 7) << 2)) & 31; }
+
+__global__ __launch_bounds__(kThreads) void k_codes_bf16t_wide(const uint8_t *__restrict__ codes,
+                                                               int R, int Kb,
+                                                               uint16_t *__restrict__ out,
+                                                               int64_t ldo) {
+    __shared__ uint32_t s32[kTWide * 32];
+    const int t = threadIdx.x;
+    const int r0 = blockIdx.x * kTWide, k0 = blockIdx.y * 128;
+#pragma unroll
+    for (int p = 0; p < kTWide / 64; ++p) {
+        const int rl = 64 * p + (t >> 2), c = t & 3, r = r0 + rl;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (r < R) v = *reinterpret_cast<const uint4 *>(codes + (int64_t)r * Kb + k0 / 2 + 16 * c);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        const int g = wide_swz(rl);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            // nibbles k = 32 c + 8 i .. +7 -> sign-extended bytes, k order:
+            // words 8 c + 2 i and 8 c + 2 i + 1
+            uint32_t o[2] = {0u, 0u};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int nib = (int)((w[i] >> (4 * e)) & 0xFu);
+                const uint32_t b = (uint32_t)(uint8_t)(int8_t)((nib ^ 8) - 8);
+                o[e >> 2] |= b << (8 * (e & 3));
+            }
+            s32[rl * 32 + ((8 * c + 2 * i) ^ g)] = o[0];
+            s32[rl * 32 + ((8 * c + 2 * i + 1) ^ g)] = o[1];
+        }
+    }
+    __syncthreads();
+    // thread (rc, kq): rows 8 rc .. 8 rc + 7, k words kq, kq + 8, kq + 16, kq + 24
+    const int rc = t & 31, kq = t >> 5;
+    const bool in = r0 + 8 * rc < R;                         // R is a multiple of 8
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int kw = kq + 8 * i;
+        uint32_t wv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) wv[j] = s32[(8 * rc + j) * 32 + (kw ^ ((rc ^ (j << 2)) & 31))];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            uint32_t pk[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const float a = (float)(int8_t)(uint8_t)(wv[2 * m] >> (8 * e));
+                const float b = (float)(int8_t)(uint8_t)(wv[2 * m + 1] >> (8 * e));
+                pk[m] = (__float_as_uint(a) >> 16) | (__float_as_uint(b) & 0xFFFF0000u);
+            }
+            if (in)
+                *reinterpret_cast<uint4 *>(out + (int64_t)(k0 + 4 * kw + e) * ldo + r0 + 8 * rc) =
+                    make_uint4(pk[0], pk[1], pk[2], pk[3]);
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // 4. Residual, bf16 contraction operands and loss partials.  64 x 64 tiles;
 //    grid (N / 64, Mp / 64).  The grid also clears the float64 scatter
@@ -820,8 +884,12 @@ hipError_t calib_typed(int M, int N, int K, const void *x, int64_t ldx, const vo
     // 2. transposed bf16 codes
     hipLaunchKernelGGL(k_codes_bf16t, dim3(p.Mp / 64, K / 128), dim3(kThreads), 0, stream,
                        c.codesA, M, K / 2, c.CaT, (int64_t)p.Mp);
-    hipLaunchKernelGGL(k_codes_bf16t, dim3(N / 64, K / 128), dim3(kThreads), 0, stream,
-                       c.codesW, N, K / 2, c.CwT, (int64_t)N);
+    if (N >= 2048)
+        hipLaunchKernelGGL(k_codes_bf16t_wide, dim3((N + kTWide - 1) / kTWide, K / 128),
+                           dim3(kThreads), 0, stream, c.codesW, N, K / 2, c.CwT, (int64_t)N);
+    else
+        hipLaunchKernelGGL(k_codes_bf16t, dim3(N / 64, K / 128), dim3(kThreads), 0, stream,
+                           c.codesW, N, K / 2, c.CwT, (int64_t)N);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // 3. forward W4A4 GEMM (its bf16 output lands in P1, rewritten below)
     if ((e = launch_w4a4_gemm(M, N, K, c.codesA, c.sA, c.codesW, c.sW, P4Q_BF16, c.P1, N, c.acc,
