@@ -51,7 +51,13 @@ typedef enum p4q_status {
 
 typedef enum p4q_dtype {
     P4Q_FP16 = 0,
-    P4Q_BF16 = 1
+    P4Q_BF16 = 1,
+    /* Not dtypes: they widen the enumeration's range to every int, so that
+     * any value a caller passes is a valid p4q_dtype for the implementation
+     * (C++), and one other than the two above is rejected with
+     * P4Q_ERR_UNSUPPORTED instead of being undefined behaviour. */
+    P4Q_DTYPE_RANGE_MIN_ = -0x7FFFFFFF - 1,
+    P4Q_DTYPE_RANGE_MAX_ = 0x7FFFFFFF
 } p4q_dtype;
 
 /* Library version string, e.g. "p4q 0.1.0 gfx950". */

@@ -35,7 +35,7 @@ Acceleration"):
   W4A4 fake-quantized and the full-precision outputs on the pruned sequence,
   over diagonal channel scales and weight / activation clipping factors.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent (the same readings as the kernels):
 * code range [-8, 7], scale = fl32(fl32(c*absmax)/7); ties round half to even;
   x/s is a correctly rounded fp32 division; an all-zero row has scale 0;
 * the selector's fake quant uses the same per-token 4-bit quantizer (clip 1);
@@ -506,7 +506,7 @@ def quant_rows_scaled(z: np.ndarray, sigma: np.ndarray, divide: bool, clip,
 
 
 def fq_row_backward(zp: np.ndarray, s: float, clip: float, codes: np.ndarray,
-                    absmax: float, kstar: int, g: np.ndarray):
+                    absmax: float, kstar: int, g: np.ndarray, absolute: bool = False):
     """Gradient of one fake-quantized row F(z') = s * clamp(rne(z'/s), -8, 7),
     s = clip * max|z'| / 7, given the upstream gradient g = dL/dF.
 
@@ -516,21 +516,60 @@ def fq_row_backward(zp: np.ndarray, s: float, clip: float, codes: np.ndarray,
     With g_s = dL/ds = sum_k g_k (code_k - inside_k z'_k / s):
         dL/dz'_k  = inside_k g_k + [k = kstar] g_s (clip / 7) sign(z'_k)
         dL/dclip  = g_s * absmax / 7
-    A row with s = 0 has no gradient.  Returns (dz' float64 [L], dclip)."""
+    A row with s = 0 has no gradient.  With absolute=True (g >= 0) every
+    factor is taken in magnitude (the linear error-propagation form).
+    Returns (dz' float64 [L], dclip)."""
     if s == 0:
         return np.zeros(zp.shape, dtype=np.float64), 0.0
+    ab = np.abs if absolute else (lambda v: v)
     rho = np.rint(zp / np.float32(s))                  # the quotient's fp32 rounding decides
     inside = ((rho >= QMIN) & (rho <= QMAX)).astype(np.float64)
     z64 = zp.astype(np.float64)
-    g_s = float(np.sum(g * (codes.astype(np.float64) - inside * z64 / float(s))))
+    g_s = float(np.sum(g * ab(codes.astype(np.float64) - inside * z64 / float(s))))
     dz = g * inside
-    dz[kstar] += g_s * (float(clip) / 7.0) * float(np.sign(z64[kstar]))
+    sign = 1.0 if absolute else float(np.sign(z64[kstar]))
+    dz[kstar] += g_s * (float(clip) / 7.0) * sign
     return dz, g_s * float(absmax) / 7.0
+
+
+def _calib_backward(P1, P2, scale, q, absolute=False):
+    """The backward pass of calib_linear from its two contraction operands
+    P1 [M, N] (the residual times sW[n]) and P2 [M, N] (times sA[m]).
+
+    With absolute=False this is the gradient.  With absolute=True every
+    quantity is replaced by its magnitude and every sum by a sum of
+    magnitudes (P1, P2 are then non-negative arrays): the result bounds, per
+    output component, how far an error of size P1 / P2 in the operands can
+    move it (linear propagation)."""
+    ab = np.abs if absolute else (lambda v: v)
+    cA, cW = q["a_codes"].astype(np.float64), q["w_codes"].astype(np.float64)
+    gA = scale * (P1 @ ab(cW))                           # dL/d(sA cA)  [M, K]
+    gW = scale * (P2.T @ ab(cA))                         # dL/d(sW cW)  [N, K]
+
+    def side(g, zp, s, clip, codes, absmax, kstar):
+        """fq_row_backward over every row of one side."""
+        R = zp.shape[0]
+        dz = np.zeros(zp.shape, dtype=np.float64)
+        dclip = np.zeros(R, dtype=np.float64)
+        clip = np.broadcast_to(np.asarray(clip, dtype=np.float32), (R,))
+        for r in range(R):
+            dz[r], dclip[r] = fq_row_backward(zp[r], s[r], clip[r], codes[r], absmax[r],
+                                              kstar[r], g[r], absolute)
+        return dz, dclip
+
+    dxp, dca = side(gA, q["xp"], q["a_scales"], q["clip_a"], q["a_codes"], q["a_absmax"],
+                    q["a_kstar"])
+    dwp, dcw = side(gW, q["wp"], q["w_scales"], q["clip_w"], q["w_codes"], q["w_absmax"],
+                    q["w_kstar"])
+    s64 = q["sigma"].astype(np.float64)
+    grad_sigma = (np.sum(dxp * ab(-q["x64"] / (s64 * s64)[None, :]), axis=0)
+                  + np.sum(dwp * ab(q["w64"]), axis=0))
+    return grad_sigma, float(np.sum(dca)), dcw
 
 
 def calib_linear(x: np.ndarray, w: np.ndarray, target: np.ndarray, sigma: np.ndarray,
                  clip_a: float, clip_w: np.ndarray, dtype: str = "fp16",
-                 operands: str = "fp64") -> dict:
+                 operands: str = "fp64", bounds: bool = False) -> dict:
     """Reconstruction loss of one W4A4 fake-quantized linear and its gradients.
 
     x [M, K] (the pruned sequence's input rows) and w [N, K] in storage
@@ -553,15 +592,34 @@ def calib_linear(x: np.ndarray, w: np.ndarray, target: np.ndarray, sigma: np.nda
       d sigma_k  = sum_m dX'[m, k] (-X[m, k] / sigma_k^2) + sum_n dW'[n, k] W[n, k];
       d clip_a   = sum over rows m of their dclip;  d clip_w[n] = row n's dclip.
 
-    operands="fp64": everything after the quantizer in float64.
+    operands="fp64": everything after the quantizer in float64 -- the plain
+    definition.
     operands="bf16": the two contractions take bf16 operands, as a mixed-
     precision calibration runs them: R = fl32(fl32(fl32(acc sA[m]) sW[n]) -
     target), and the operands are bf16(fl32(R sW[n])) and bf16(fl32(R sA[m]))
     (nearest, ties to even); the loss is sum R^2 / (M N); the codes and
-    the rest stay exact / float64.
+    the rest stay exact / float64.  A diagnostic of that arithmetic only.
+
+    bounds=True (with operands="fp64") also returns, per output, a bound on
+    how far an evaluation that rounds the residual in fp32, the contraction
+    operands to bf16 and accumulates in fp32 can lie from the float64 result:
+      * operand error, per entry: |P^ - R sW| <= sW (1.01 * 2^-8 |R|
+        + 4 u (|Yq| + |R|)) with u = 2^-24 (the fp32 residual is within
+        3 u (|Yq| + |R|) of R; bf16 rounding is 2^-8 relative, fl32 of the
+        product 2^-24), and likewise with sA for the other operand;
+      * this error propagated linearly through the backward pass in
+        magnitude form (_calib_backward with absolute=True);
+      * plus (gamma_N + gamma_M + gamma_K + 2^-20) times the magnitude form
+        of the whole backward pass, gamma_n = n u / (1 - n u) being the
+        worst-case relative error of an fp32 sum of n terms (the two
+        contractions, the row and the column sums) and 2^-20 covering the
+        fp32 rounding of the few per-element products.
+    The loss bound is sum (2 |R| e + e^2) / (M N) + gamma_{MN} loss with
+    e = 3 u (|Yq| + |R|).
 
     Returns a dict with loss, grad_sigma [K], grad_clip_a, grad_clip_w [N]
-    (float64) and the quantizer outputs of both sides."""
+    (float64), the quantizer outputs of both sides and, with bounds, the
+    matching bound_* entries."""
     M, K = x.shape
     N = w.shape[0]
     sig = np.asarray(sigma, dtype=np.float32)
@@ -570,8 +628,9 @@ def calib_linear(x: np.ndarray, w: np.ndarray, target: np.ndarray, sigma: np.nda
     cW, sW, aW, kW, wp = quant_rows_scaled(w, sig, False, cw_clip, dtype)
     acc = int_gemm(cA, cW).astype(np.float64)
     T = np.asarray(target, dtype=np.float32)
+    Y = sA.astype(np.float64)[:, None] * sW.astype(np.float64)[None, :] * acc
     if operands == "fp64":
-        R = sA.astype(np.float64)[:, None] * sW.astype(np.float64)[None, :] * acc - T
+        R = Y - T
         P1 = R * sW.astype(np.float64)[None, :]
         P2 = R * sA.astype(np.float64)[:, None]
     elif operands == "bf16":
@@ -587,22 +646,29 @@ def calib_linear(x: np.ndarray, w: np.ndarray, target: np.ndarray, sigma: np.nda
         raise ValueError(operands)
     scale = 2.0 / (M * N)
     loss = float(np.sum(R * R)) / (M * N)
-    gA = scale * (P1 @ cW.astype(np.float64))            # dL/d(sA cA)  [M, K]
-    gW = scale * (P2.T @ cA.astype(np.float64))          # dL/d(sW cW)  [N, K]
-    dxp = np.zeros((M, K), dtype=np.float64)
-    dwp = np.zeros((N, K), dtype=np.float64)
-    dclip_a = 0.0
-    dclip_w = np.zeros(N, dtype=np.float64)
-    for m in range(M):
-        dxp[m], dc = fq_row_backward(xp[m], sA[m], clip_a, cA[m], aA[m], kA[m], gA[m])
-        dclip_a += dc
-    for n in range(N):
-        dwp[n], dclip_w[n] = fq_row_backward(wp[n], sW[n], cw_clip[n], cW[n], aW[n], kW[n],
-                                             gW[n])
-    x64 = as_f32(x, dtype).astype(np.float64)
-    w64 = as_f32(w, dtype).astype(np.float64)
-    s64 = sig.astype(np.float64)
-    grad_sigma = np.sum(dxp * (-x64 / (s64 * s64)[None, :]), axis=0) + np.sum(dwp * w64, axis=0)
-    return {"loss": loss, "grad_sigma": grad_sigma, "grad_clip_a": dclip_a,
-            "grad_clip_w": dclip_w, "a_codes": cA, "a_scales": sA, "a_absmax": aA,
-            "a_kstar": kA, "w_codes": cW, "w_scales": sW, "w_absmax": aW, "w_kstar": kW}
+    q = {"a_codes": cA, "a_scales": sA, "a_absmax": aA, "a_kstar": kA, "xp": xp,
+         "clip_a": np.float32(clip_a), "w_codes": cW, "w_scales": sW, "w_absmax": aW,
+         "w_kstar": kW, "wp": wp, "clip_w": cw_clip, "sigma": sig,
+         "x64": as_f32(x, dtype).astype(np.float64), "w64": as_f32(w, dtype).astype(np.float64)}
+    grad_sigma, dclip_a, dclip_w = _calib_backward(P1, P2, scale, q)
+    out = {"loss": loss, "grad_sigma": grad_sigma, "grad_clip_a": dclip_a,
+           "grad_clip_w": dclip_w, "a_codes": cA, "a_scales": sA, "a_absmax": aA,
+           "a_kstar": kA, "w_codes": cW, "w_scales": sW, "w_absmax": aW, "w_kstar": kW}
+    if bounds:
+        if operands != "fp64":
+            raise ValueError("bounds are taken around the float64 result")
+        u = 2.0 ** -24
+        gam = lambda n: n * u / (1.0 - n * u)
+        absR, absY = np.abs(R), np.abs(Y)
+        e = 4.0 * u * (absY + absR)
+        E1 = (1.01 * 2.0 ** -8 * absR + e) * sW.astype(np.float64)[None, :]
+        E2 = (1.01 * 2.0 ** -8 * absR + e) * sA.astype(np.float64)[:, None]
+        bs, bca, bcw = _calib_backward(E1, E2, scale, q, absolute=True)
+        ms, mca, mcw = _calib_backward(np.abs(P1), np.abs(P2), scale, q, absolute=True)
+        g = gam(N) + gam(M) + gam(K) + 2.0 ** -20
+        out["bound_grad_sigma"] = bs + g * ms
+        out["bound_grad_clip_a"] = bca + g * mca
+        out["bound_grad_clip_w"] = bcw + g * mcw
+        eR = 3.0 * u * (absY + absR)
+        out["bound_loss"] = float(np.sum(2.0 * absR * eR + eR * eR)) / (M * N) + gam(M * N) * loss
+    return out

@@ -8,7 +8,11 @@ from __future__ import annotations
 import ctypes
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libp4q.so")
+# P4Q_LIBRARY selects another build of the same library (for instance one
+# whose host code is compiled with address and undefined-behaviour
+# sanitizers); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("P4Q_LIBRARY") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libp4q.so")
 
 P4Q_OK, P4Q_ERR_INVALID_ARG, P4Q_ERR_UNSUPPORTED, P4Q_ERR_WORKSPACE, P4Q_ERR_HIP = range(5)
 P4Q_FP16, P4Q_BF16 = 0, 1

@@ -35,9 +35,48 @@ def _stream(dev: torch.device):
 
 
 def _need_gpu(*ts):
+    """Every given tensor on one GPU (checked after the shape and dtype checks,
+    so that those can be exercised without a device)."""
+    devs = {t.device for t in ts if t is not None}
     for t in ts:
         if t is not None and not t.is_cuda:
             raise ValueError("p4q tensors must live on the GPU")
+    if len(devs) > 1:
+        raise ValueError(f"p4q tensors of one call must share a device, got {sorted(map(str, devs))}")
+
+
+def _check(t: Optional[torch.Tensor], name: str, shape=None, dtype=None,
+           contiguous: bool = True) -> None:
+    """Shape, dtype and layout of a caller-supplied operand or output.  A
+    buffer that is too small or of the wrong type would make a kernel read
+    or write past its allocation, which the C ABI (plain pointers) cannot
+    detect, so every such tensor is checked here before any call."""
+    if t is None:
+        return
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if dtype is not None:
+        ok = t.dtype in dtype if isinstance(dtype, tuple) else t.dtype == dtype
+        if not ok:
+            raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _check_rows(t: torch.Tensor, name: str, rows: int, cols: int, dtype=None) -> None:
+    """A 2-D operand or output whose rows may be strided: [rows, cols] with
+    unit column stride and row stride >= cols."""
+    if t.dim() != 2 or t.shape[0] != rows or t.shape[1] != cols:
+        raise ValueError(f"{name} must have shape ({rows}, {cols}), got {tuple(t.shape)}")
+    if t.stride(1) != 1 or (rows > 1 and t.stride(0) < cols):
+        raise ValueError(f"{name} must have unit column stride and row stride >= {cols}")
+    if dtype is not None:
+        ok = t.dtype in dtype if isinstance(dtype, tuple) else t.dtype == dtype
+        if not ok:
+            raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+_F16 = (torch.float16, torch.bfloat16)
 
 
 # --------------------------------------------------------------------------- selector
@@ -45,6 +84,23 @@ def select_workspace(B: int, N: int, d: int, J: int, device) -> torch.Tensor:
     """Workspace for select(); its first B*N*(J+1) int32 hold D and Nv per token."""
     n = lib().p4q_select_workspace_bytes(B, N, d, J)
     return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def _selector_shapes(vis, concepts, text):
+    """(B, N, d, J, T) of the selector's inputs, after checking that they
+    agree and share a 16-bit float dtype."""
+    if vis.dim() != 3 or concepts.dim() != 3 or (text is not None and text.dim() != 3):
+        raise ValueError("vis, concepts and text must be 3-D [B, rows, d]")
+    B, N, d = vis.shape
+    J = concepts.shape[1]
+    T = 0 if text is None else text.shape[1]
+    if concepts.shape != (B, J, d) or (text is not None and text.shape != (B, T, d)):
+        raise ValueError("shape mismatch between vis, concepts and text")
+    for t, name in ((vis, "vis"), (concepts, "concepts"), (text, "text")):
+        _check(t, name, None, _F16)
+        if t is not None and t.dtype != vis.dtype:
+            raise ValueError("vis/concepts/text must share a dtype")
+    return B, N, d, J, T
 
 
 def select(vis: torch.Tensor, concepts: torch.Tensor, text: Optional[torch.Tensor], K: int,
@@ -55,15 +111,11 @@ def select(vis: torch.Tensor, concepts: torch.Tensor, text: Optional[torch.Tenso
 
     vis [B, N, d], concepts [B, J, d], text [B, T, d] or None; returns
     (idx int32 [B, K] ascending, tokens [B, K+T, d] = kept original rows + text)."""
-    _need_gpu(vis, concepts, text)
-    B, N, d = vis.shape
-    J = concepts.shape[1]
-    T = 0 if text is None else text.shape[1]
-    if concepts.shape != (B, J, d) or (text is not None and text.shape != (B, T, d)):
-        raise ValueError("shape mismatch between vis, concepts and text")
-    for t in (vis, concepts, text):
-        if t is not None and (t.dtype != vis.dtype or not t.is_contiguous()):
-            raise ValueError("vis/concepts/text must be contiguous and share a dtype")
+    B, N, d, J, T = _selector_shapes(vis, concepts, text)
+    _check(idx_out, "idx_out", (B, K), torch.int32)
+    _check(tokens_out, "tokens_out", (B, K + T, d), vis.dtype)
+    _check(workspace, "workspace", None, torch.uint8)
+    _need_gpu(vis, concepts, text, idx_out, tokens_out, workspace)
     dev = vis.device
     if idx_out is None:
         idx_out = torch.empty((B, K), dtype=torch.int32, device=dev)
@@ -107,17 +159,13 @@ def select_full(vis: torch.Tensor, concepts: torch.Tensor, cls_attn: torch.Tenso
     Returns (idx int32 [B, K] ascending, tokens [B, K+T, d]) and, when
     return_stages, also stages int32 [B, K] (query picks ascending, saliency
     picks ascending, diversity picks in pick order)."""
-    _need_gpu(vis, concepts, cls_attn, text)
-    B, N, d = vis.shape
-    J = concepts.shape[1]
-    T = 0 if text is None else text.shape[1]
-    if concepts.shape != (B, J, d) or (text is not None and text.shape != (B, T, d)):
-        raise ValueError("shape mismatch between vis, concepts and text")
-    if cls_attn.shape != (B, N) or cls_attn.dtype != torch.float32 or not cls_attn.is_contiguous():
-        raise ValueError("cls_attn must be contiguous fp32 [B, N]")
-    for t in (vis, concepts, text):
-        if t is not None and (t.dtype != vis.dtype or not t.is_contiguous()):
-            raise ValueError("vis/concepts/text must be contiguous and share a dtype")
+    B, N, d, J, T = _selector_shapes(vis, concepts, text)
+    _check(cls_attn, "cls_attn", (B, N), torch.float32)
+    _check(idx_out, "idx_out", (B, K), torch.int32)
+    _check(stages_out, "stages_out", (B, K), torch.int32)
+    _check(tokens_out, "tokens_out", (B, K + T, d), vis.dtype)
+    _check(workspace, "workspace", None, torch.uint8)
+    _need_gpu(vis, concepts, cls_attn, text, idx_out, stages_out, tokens_out, workspace)
     if kq is None or ks is None:
         dq, ds, _ = select_budgets(K)
         kq = dq if kq is None else kq
@@ -147,10 +195,13 @@ def quant_act(x: torch.Tensor, clip: float = 1.0, codes: Optional[torch.Tensor] 
               scales: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Per-row int4 quantize + pack (p4q_quant_act): x [M, K_in] (row stride may
     exceed K_in) -> (codes uint8 [M, K_in/2], scales fp32 [M])."""
-    _need_gpu(x)
-    if x.dim() != 2 or x.stride(1) != 1:
-        raise ValueError("x must be 2-D with unit column stride")
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D")
     M, K_in = x.shape
+    _check_rows(x, "x", M, K_in, _F16)
+    _check(codes, "codes", (M, K_in // 2), torch.uint8)
+    _check(scales, "scales", (M,), torch.float32)
+    _need_gpu(x, codes, scales)
     if codes is None:
         codes = torch.empty((M, K_in // 2), dtype=torch.uint8, device=x.device)
     if scales is None:
@@ -168,12 +219,15 @@ def rmsnorm_quant(x: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-5, clip:
     """Per-token int4 quantize + pack of RMSNorm(x) * gamma (p4q_rmsnorm_quant):
     x [M, d] (row stride may exceed d), gamma [d] of x's dtype -> (codes uint8
     [M, d/2], scales fp32 [M]); the normalized rows are never formed."""
-    _need_gpu(x, gamma)
-    if x.dim() != 2 or x.stride(1) != 1:
-        raise ValueError("x must be 2-D with unit column stride")
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D")
     M, d = x.shape
+    _check_rows(x, "x", M, d, _F16)
     if gamma.shape != (d,) or gamma.dtype != x.dtype or not gamma.is_contiguous():
         raise ValueError("gamma must be a contiguous [d] tensor of x's dtype")
+    _check(codes, "codes", (M, d // 2), torch.uint8)
+    _check(scales, "scales", (M,), torch.float32)
+    _need_gpu(x, gamma, codes, scales)
     if codes is None:
         codes = torch.empty((M, d // 2), dtype=torch.uint8, device=x.device)
     if scales is None:
@@ -193,7 +247,6 @@ def attention_prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, B: int,
     q, k, v: 2-D [B*L, >= H*128] views with a shared row stride (e.g. column
     slices of one fused q|k|v output); returns out [B*L, H*128] of the same
     dtype."""
-    _need_gpu(q, k, v, out)
     rows = q.shape[0]
     if rows % B:
         raise ValueError("rows must be B * L")
@@ -204,6 +257,11 @@ def attention_prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, B: int,
             raise ValueError("q, k, v must be 2-D [B*L, >= H*D] with unit column stride")
         if t.stride(0) != q.stride(0) or t.dtype != q.dtype:
             raise ValueError("q, k, v must share row stride and dtype")
+    if q.dtype not in _F16:
+        raise ValueError(f"q, k, v must be fp16 or bf16, got {q.dtype}")
+    if out is not None:
+        _check_rows(out, "out", rows, H * D, q.dtype)
+    _need_gpu(q, k, v, out)
     if out is None:
         out = torch.empty((rows, H * D), dtype=q.dtype, device=q.device)
     st = lib().p4q_attention_prefill(_dtype_code(q.dtype), B, L, H, D, _ptr(q), _ptr(k), _ptr(v),
@@ -219,15 +277,16 @@ def quant_scaled(z: torch.Tensor, sigma: torch.Tensor, divide: bool, clip: float
     """Channel-scaled per-row quantizer (p4q_quant_scaled): z [R, K] (row
     stride may exceed K), sigma fp32 [K]; z' = z / sigma (divide) or z * sigma
     -> (codes uint8 [R, K/2], scales fp32 [R], absmax fp32 [R], kstar int32 [R])."""
-    _need_gpu(z, sigma, clip_rows)
-    if z.dim() != 2 or z.stride(1) != 1:
-        raise ValueError("z must be 2-D with unit column stride")
+    if z.dim() != 2:
+        raise ValueError("z must be 2-D")
     R, K = z.shape
+    _check_rows(z, "z", R, K, _F16)
     if sigma.shape != (K,) or sigma.dtype != torch.float32 or not sigma.is_contiguous():
         raise ValueError("sigma must be a contiguous fp32 [K] tensor")
     if clip_rows is not None and (clip_rows.shape != (R,) or clip_rows.dtype != torch.float32
                                   or not clip_rows.is_contiguous()):
         raise ValueError("clip_rows must be a contiguous fp32 [R] tensor")
+    _need_gpu(z, sigma, clip_rows)
     dev = z.device
     codes = torch.empty((R, K // 2), dtype=torch.uint8, device=dev)
     scales = torch.empty((R,), dtype=torch.float32, device=dev)
@@ -256,7 +315,6 @@ def calib_linear_grad(x: torch.Tensor, w: torch.Tensor, target: torch.Tensor,
     [M, N], sigma fp32 [K], clip_w fp32 [N] -> (loss [1], grad_sigma [K],
     grad_clip_a [1], grad_clip_w [N]), all fp32 device tensors.  `out` may
     hold those four tensors to be written in place."""
-    _need_gpu(x, w, target, sigma, clip_w)
     for t, name in ((x, "x"), (w, "w"), (target, "target")):
         if t.dim() != 2 or t.stride(1) != 1:
             raise ValueError(f"{name} must be 2-D with unit column stride")
@@ -269,6 +327,15 @@ def calib_linear_grad(x: torch.Tensor, w: torch.Tensor, target: torch.Tensor,
     for t, n, name in ((sigma, K, "sigma"), (clip_w, N, "clip_w")):
         if t.shape != (n,) or t.dtype != torch.float32 or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous fp32 [{n}] tensor")
+    if x.dtype not in _F16:
+        raise ValueError(f"x and w must be fp16 or bf16, got {x.dtype}")
+    if out is not None:
+        if len(out) != 4:
+            raise ValueError("out must hold (loss, grad_sigma, grad_clip_a, grad_clip_w)")
+        for t, n, name in zip(out, (1, K, 1, N), ("loss", "grad_sigma", "grad_clip_a", "grad_clip_w")):
+            _check(t, name, (n,), torch.float32)
+    _check(workspace, "workspace", None, torch.uint8)
+    _need_gpu(x, w, target, sigma, clip_w, workspace, *(out or ()))
     dev = x.device
     if out is None:
         out = (torch.empty(1, dtype=torch.float32, device=dev),
@@ -302,14 +369,21 @@ def w4a4_linear(a_codes: torch.Tensor, a_scales: torch.Tensor, w_codes: torch.Te
     Without `workspace` one of the size the library asks for is allocated
     (small M splits K across work-groups with it); a smaller one, e.g.
     empty, runs the unsplit kernel.  Results are identical either way."""
-    _need_gpu(a_codes, a_scales, w_codes, w_scales)
+    if a_codes.dim() != 2 or w_codes.dim() != 2:
+        raise ValueError("a_codes and w_codes must be 2-D [rows, K_in/2]")
     M, kb = a_codes.shape
     N_out, kb2 = w_codes.shape
     if kb != kb2:
         raise ValueError("a_codes and w_codes disagree on K_in")
-    for t in (a_codes, w_codes, a_scales, w_scales):
-        if not t.is_contiguous():
-            raise ValueError("operands must be contiguous")
+    _check(a_codes, "a_codes", (M, kb), torch.uint8)
+    _check(w_codes, "w_codes", (N_out, kb), torch.uint8)
+    _check(a_scales, "a_scales", (M,), torch.float32)
+    _check(w_scales, "w_scales", (N_out,), torch.float32)
+    if y is not None:
+        _check_rows(y, "y", M, N_out, _F16)
+    _check(acc_out, "acc_out", (M, N_out), torch.int32)
+    _check(workspace, "workspace", None, torch.uint8)
+    _need_gpu(a_codes, a_scales, w_codes, w_scales, y, acc_out, workspace)
     K_in = 2 * kb
     dev = a_codes.device
     if y is None:

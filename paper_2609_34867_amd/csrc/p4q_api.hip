@@ -56,8 +56,14 @@ const char *p4q_status_string(int status) {
 
 const char *p4q_last_error(void) { return g_last_error; }
 
+// the selector's size limits (outside them p4q_select rejects the call)
+static bool select_shape_ok(int B, int N, int d, int J) {
+    return B > 0 && N > 0 && N <= 8192 && d >= 32 && d <= 16384 && d % 32 == 0 && J > 0 &&
+           J <= 8 && !(J > 4 && d > 8192);
+}
+
 size_t p4q_select_workspace_bytes(int B, int N, int d, int J) {
-    if (B <= 0 || N <= 0 || d <= 0 || J <= 0) return 0;
+    if (!select_shape_ok(B, N, d, J)) return 0;
     return p4q::select_workspace_bytes(B, N, d, J);
 }
 
@@ -93,7 +99,7 @@ int p4q_select(p4q_dtype dt, int B, int N, int d, const void *vis, const void *c
 }
 
 size_t p4q_select_full_workspace_bytes(int B, int N, int d, int J, int K) {
-    if (B <= 0 || N <= 0 || d <= 0 || J <= 0 || K <= 0) return 0;
+    if (!select_shape_ok(B, N, d, J) || d > 8192 || K <= 0 || K > N) return 0;
     return p4q::select_full_workspace_bytes(B, N, d, J, K);
 }
 
@@ -196,7 +202,9 @@ int p4q_attention_prefill(p4q_dtype dt, int B, int L, int H, int D, const void *
 }
 
 size_t p4q_w4a4_linear_workspace_bytes(int M, int N_out, int K_in) {
-    if (M <= 0 || N_out <= 0 || K_in <= 0) return 0;
+    if (M <= 0 || N_out <= 0 || K_in <= 0 || K_in % 32 != 0 || K_in > 131072 ||
+        (int64_t)M > 65535LL * 128)
+        return 0;
     return p4q::gemm_workspace_bytes(M, N_out, K_in);
 }
 
@@ -244,8 +252,8 @@ int p4q_quant_scaled(p4q_dtype dt, int R, int K, const void *z, int64_t ldz, con
 static int calib_shape_error(int M, int N, int K) {
     if (M <= 0 || N <= 0 || K <= 0) return P4Q_ERR_INVALID_ARG;
     if (N % 64 != 0 || K % 128 != 0) return P4Q_ERR_INVALID_ARG;
-    if (K > 16384 || M > (1 << 20) || N > (1 << 20) || (int64_t)M * N > (1LL << 31) ||
-        (int64_t)N * K > (1LL << 31))
+    if (K > 16384 || M > (1 << 20) || N > (1 << 20) || (int64_t)M * N >= (1LL << 31) ||
+        (int64_t)N * K >= (1LL << 31))
         return P4Q_ERR_UNSUPPORTED;
     return P4Q_OK;
 }

@@ -7,9 +7,50 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "../../include/p4q.h"
 
 namespace p4q {
+
+// ---- per-device constants -----------------------------------------------------
+// Launch shapes depend on the device's CU count and on how many blocks of a
+// kernel fit on a CU.  Both are fixed for a device, so they are queried once
+// per device ordinal and kept in a cache of atomics: concurrent first calls
+// from several host threads each store the same value, and no other state
+// is shared between calls.
+constexpr int kMaxDevices = 64;
+
+inline int current_device() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+    return dev;
+}
+
+// cached value of query() for the current device; query() returns > 0
+template <class Query>
+inline int per_device_cached(std::atomic<int> (&cache)[kMaxDevices], Query query) {
+    const int dev = current_device();
+    if (dev >= kMaxDevices) return query(dev);
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v <= 0) {
+        v = query(dev);
+        cache[dev].store(v, std::memory_order_relaxed);
+    }
+    return v;
+}
+
+// compute units of the current device (256 on MI355X if the query fails)
+inline int device_cus() {
+    static std::atomic<int> cache[kMaxDevices];
+    return per_device_cached(cache, [](int dev) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+        return cus;
+    });
+}
 
 // ---- quantize + pack (Q4 per row) ------------------------------------------
 hipError_t launch_quant_act(p4q_dtype dt, int M, int K_in, const void *x, int64_t ldx,

@@ -567,17 +567,15 @@ hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const vo
     const size_t lds = (size_t)JMAX * 64 * CH * 4;
     // Rows per wavefront: enough that the whole grid is resident at once
     // (one wave of blocks, no partly filled last wave).
-    static int resident = 0;                      // blocks per CU x CUs, per instantiation
-    if (resident == 0) {
-        int dev = 0, cus = 0, per_cu = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_select_score<CH, JMAX, BF16, CLIP1>, 256,
-                                                         lds) != hipSuccess ||
-            cus <= 0 || per_cu <= 0)
-            per_cu = 1, cus = 256;
-        resident = per_cu * cus;
-    }
+    static std::atomic<int> per_cu_cache[kMaxDevices];   // blocks per CU, per instantiation
+    const int per_cu = per_device_cached(per_cu_cache, [lds](int) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_select_score<CH, JMAX, BF16, CLIP1>, 256,
+                                                         lds) != hipSuccess || n <= 0)
+            n = 1;
+        return n;
+    });
+    const int resident = per_cu * device_cus();
     const int64_t waves = 4LL * resident;
     const int rpw = (int)std::max<int64_t>(1, ((int64_t)B * N + waves - 1) / waves);
     const dim3 grid((N + 4 * rpw - 1) / (4 * rpw), B);

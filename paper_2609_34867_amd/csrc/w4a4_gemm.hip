@@ -900,10 +900,10 @@ __global__ __launch_bounds__(64 * NW) void k_w4a4_gemv(const uint8_t *__restrict
 // nor when N % 4 != 0 (the epilogue writes 4 outputs per thread).
 static int small_m_splits(int M, int N, int K) {
     if (M <= 16 || (M >= 1024 && N >= 1024) || N % 4 != 0) return 1;
-    const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    const int64_t tiles = (((int64_t)M + BM - 1) / BM) * (((int64_t)N + BN - 1) / BN);
     const int kt_all = (K / 2 + KS_ROW - 1) / KS_ROW;
     if (tiles >= 256) return 1;
-    int S = (256 + tiles - 1) / tiles;
+    int S = (int)((256 + tiles - 1) / tiles);
     S = std::min(S, 4);
     S = std::min(S, kt_all / 4);
     return std::max(S, 1);
@@ -921,14 +921,7 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
     const bool bf16 = (out_dt == P4Q_BF16);
     // decode kernel: 32-bit buffer offsets need N * K_in / 2 < 2^31
     if (M <= 16 && K <= G_MAX_KIN && (int64_t)N * (K / 2) < 0x7FFF0000LL) {
-        static int cus = 0;
-        if (cus == 0) {
-            int dev = 0;
-            if (hipGetDevice(&dev) != hipSuccess ||
-                hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-                cus <= 0)
-                cus = 256;
-        }
+        const int cus = device_cus();
         const int groups = (N + G_ROWS - 1) / G_ROWS;
         const int ktiles = (K + 127) / 128;
         auto go = [&](auto kern, int nw, int blocks_per_cu) {

@@ -12,7 +12,7 @@ import torch
 import oracle
 import paper_2609_34867_amd as p4q
 from workload import random_features
-from gpu_util import to_gpu, to_np
+from gpu_util import Guarded, check_canaries, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 D = 128
@@ -30,8 +30,10 @@ def tol(dtype):
 def check(qkv, B, L, H, causal=True, dtype="fp16", samples=None):
     t = to_gpu(qkv, dtype)
     HD = H * D
-    out = p4q.attention_prefill(t[:, :HD], t[:, HD:2 * HD], t[:, 2 * HD:], B, H, causal)
+    go = Guarded((B * L, HD), t.dtype, "out")
+    out = p4q.attention_prefill(t[:, :HD], t[:, HD:2 * HD], t[:, 2 * HD:], B, H, causal, out=go.t)
     torch.cuda.synchronize()
+    check_canaries(go)
     got = oracle.as_f32(to_np(out), dtype).astype(np.float64).reshape(B, L, H, D)
     a, r = tol(dtype)
     for b in (range(B) if samples is None else samples):

@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2609_34867_amd as p4q
 from workload import CONFIGS, random_features, weight, attn_standin
-from gpu_util import to_gpu, to_np, bits, first_mismatch
+from gpu_util import Guarded, bits, check_canaries, first_mismatch, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -28,19 +28,29 @@ def codes_for(M, N, K, seed, extreme=None):
     return oracle.pack_int4(a), sa, oracle.pack_int4(w), sw
 
 
-def run_gpu(ap, sa, wp, sw, out_dtype):
+def run_gpu(ap, sa, wp, sw, out_dtype, with_acc=True, workspace=None):
+    """One call into canary-guarded outputs; with_acc=False runs the y-only
+    kernels (the instantiations the benchmark times)."""
     tdt = torch.float16 if out_dtype == "fp16" else torch.bfloat16
-    y, acc = p4q.w4a4_linear(to_gpu(ap), to_gpu(sa), to_gpu(wp), to_gpu(sw), tdt,
-                             return_acc=True)
+    M, N = ap.shape[0], wp.shape[0]
+    gy = Guarded((M, N), tdt, "y")
+    ga = Guarded((M, N), torch.int32, "acc_out") if with_acc else None
+    p4q.w4a4_linear(to_gpu(ap), to_gpu(sa), to_gpu(wp), to_gpu(sw), y=gy.t,
+                    acc_out=None if ga is None else ga.t, workspace=workspace)
     torch.cuda.synchronize()
-    return to_np(y), to_np(acc)
+    check_canaries(gy, *([ga] if ga else []))
+    return to_np(gy.t), (to_np(ga.t) if ga else None)
 
 
 def check_full(ap, sa, wp, sw, out_dtype):
-    y, acc = run_gpu(ap, sa, wp, sw, out_dtype)
+    """Both instantiations (with and without the int32 store) against the
+    oracle, bit for bit."""
     racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, out_dtype)
+    y, acc = run_gpu(ap, sa, wp, sw, out_dtype)
     assert (m := first_mismatch(acc, racc.astype(np.int32))) is None, m
     assert (m := first_mismatch(bits(y), bits(ry))) is None, m
+    y, _ = run_gpu(ap, sa, wp, sw, out_dtype, with_acc=False)
+    assert (m := first_mismatch(bits(y), bits(ry))) is None, ("y-only", m)
 
 
 @pytest.mark.parametrize("out_dtype", ["fp16", "bf16"])
@@ -95,52 +105,73 @@ def test_quantized_pipeline_tiny():
     assert np.array_equal(bits(to_np(y)), bits(ry))
 
 
-@pytest.mark.slow
-@pytest.mark.parametrize("li", [0, 4, 6])
-def test_llava_next_b16_linears_sampled(li):
-    """q_proj (4096x4096), gate_proj (11008x4096) and down_proj (4096x11008) at
-    M = 11264 in one launch each; rows 0..63, the last 64 rows and 1024 random
-    entries are checked against the oracle."""
-    cfg = CONFIGS["next7b_b16"]
-    lin = cfg.linears[li]
-    rng = np.random.default_rng(li)
-    ap = rng.integers(0, 256, size=(cfg.M, lin.k_in // 2), dtype=np.uint8)
-    sa = rng.uniform(1e-3, 4, size=cfg.M).astype(np.float32)
-    wp, sw = oracle.quant_act(weight(cfg, li))
-    y, acc = run_gpu(ap, sa, wp, sw, "bf16")
-    for rows in (slice(0, 64), slice(cfg.M - 64, cfg.M)):
+def check_sampled(ap, sa, wp, sw, y, acc, rng, edge_rows=32, entries=1024):
+    """First and last rows in full plus random entries, against the oracle
+    (acc may be None: the y-only kernels)."""
+    M = ap.shape[0]
+    for rows in (slice(0, edge_rows), slice(M - edge_rows, M)):
         racc, ry = oracle.w4a4_linear(ap[rows], sa[rows], wp, sw, "bf16")
-        assert (m := first_mismatch(acc[rows], racc.astype(np.int32))) is None, m
+        if acc is not None:
+            assert (m := first_mismatch(acc[rows], racc.astype(np.int32))) is None, m
         assert (m := first_mismatch(bits(y[rows]), bits(ry))) is None, m
-    for _ in range(1024):
-        m, n = int(rng.integers(cfg.M)), int(rng.integers(lin.n_out))
+    yb = bits(y)
+    for _ in range(entries):
+        m, n = int(rng.integers(M)), int(rng.integers(wp.shape[0]))
         racc, ry = oracle.w4a4_linear_entry(ap, sa, wp, sw, m, n, "bf16")
-        assert acc[m, n] == racc and bits(y)[m, n] == ry
+        assert yb[m, n] == ry, (m, n)
+        if acc is not None:
+            assert acc[m, n] == racc, (m, n)
+
+
+def launch_weights(cfg, members):
+    """Row-concatenated quantized weights of one launch of the layer, from the
+    config's weight recipe (quantized by the oracle)."""
+    parts = [oracle.quant_act(weight(cfg, li)) for li in members]
+    return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("members", [(0, 1, 2), (4, 5)])
-def test_llava_next_b16_fused_projections_sampled(members):
-    """The fused launches the benchmark runs: q|k|v (12288 x 4096) and
-    gate|up (22016 x 4096) on row-concatenated weights at M = 11264; the first
-    and last 32 rows and 1024 random entries are checked against the oracle."""
+@pytest.mark.parametrize("members", [(0, 1, 2), (3,), (4, 5), (6,)],
+                         ids=["qkv", "o_proj", "gate_up", "down_proj"])
+def test_llava_next_b16_launches_sampled(members):
+    """The four launches one benchmark step times at M = 11264 (q|k|v 12288 x
+    4096 and gate|up 22016 x 4096 on row-concatenated weights, o_proj 4096 x
+    4096, down_proj 4096 x 11008), in the y-only instantiation the benchmark
+    runs and in the one that also stores the int32 accumulators; the first and
+    last 32 rows and 1024 random entries of each are checked against the
+    oracle."""
     cfg = CONFIGS["next7b_b16"]
     k_in = cfg.linears[members[0]].k_in
-    rng = np.random.default_rng(sum(members))
+    rng = np.random.default_rng(sum(members) + 17 * len(members))
     ap = rng.integers(0, 256, size=(cfg.M, k_in // 2), dtype=np.uint8)
     sa = rng.uniform(1e-3, 4, size=cfg.M).astype(np.float32)
-    parts = [oracle.quant_act(weight(cfg, li)) for li in members]
-    wp = np.concatenate([p[0] for p in parts])
-    sw = np.concatenate([p[1] for p in parts])
-    y, acc = run_gpu(ap, sa, wp, sw, "bf16")
-    for rows in (slice(0, 32), slice(cfg.M - 32, cfg.M)):
-        racc, ry = oracle.w4a4_linear(ap[rows], sa[rows], wp, sw, "bf16")
-        assert (m := first_mismatch(acc[rows], racc.astype(np.int32))) is None, m
-        assert (m := first_mismatch(bits(y[rows]), bits(ry))) is None, m
-    for _ in range(1024):
-        m, n = int(rng.integers(cfg.M)), int(rng.integers(wp.shape[0]))
-        racc, ry = oracle.w4a4_linear_entry(ap, sa, wp, sw, m, n, "bf16")
-        assert acc[m, n] == racc and bits(y)[m, n] == ry
+    wp, sw = launch_weights(cfg, members)
+    y, _ = run_gpu(ap, sa, wp, sw, "bf16", with_acc=False)
+    check_sampled(ap, sa, wp, sw, y, None, rng)
+    y2, acc = run_gpu(ap, sa, wp, sw, "bf16")
+    assert np.array_equal(bits(y), bits(y2)), "y differs between the two instantiations"
+    check_sampled(ap, sa, wp, sw, y2, acc, rng, entries=256)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("NK", [(15360, 5120), (5120, 5120), (27648, 5120), (5120, 13824)],
+                         ids=["qkv", "o_proj", "gate_up", "down_proj"])
+def test_stress13b_prefill_launches_sampled(NK):
+    """The 13B-shape prefill launches at M = 5632 (batch 8 x (640 + 64)):
+    h = 5120, f = 13824, random codes and scales, y-only (the timed kernel)
+    and with the accumulators, sampled against the oracle."""
+    N, K = NK
+    M = CONFIGS["stress13b_b8"].M
+    rng = np.random.default_rng(N + K)
+    ap = rng.integers(0, 256, size=(M, K // 2), dtype=np.uint8)
+    wp = rng.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+    sa = rng.uniform(1e-3, 4, size=M).astype(np.float32)
+    sw = rng.uniform(1e-4, 3e-2, size=N).astype(np.float32)
+    y, _ = run_gpu(ap, sa, wp, sw, "bf16", with_acc=False)
+    check_sampled(ap, sa, wp, sw, y, None, rng, entries=512)
+    y2, acc = run_gpu(ap, sa, wp, sw, "bf16")
+    assert np.array_equal(bits(y), bits(y2))
+    check_sampled(ap, sa, wp, sw, y2, acc, rng, edge_rows=16, entries=256)
 
 
 @pytest.mark.parametrize("M", [1, 2, 4, 7, 16])
@@ -240,8 +271,26 @@ def test_small_m_split_k(shape):
     dev = torch.device("cuda:0")
     empty = torch.empty(0, dtype=torch.uint8, device=dev)      # zero bytes: the unsplit path
     for ws in (None, empty):
-        y, acc = p4q.w4a4_linear(to_gpu(ap), to_gpu(sa), to_gpu(wp), to_gpu(sw), torch.bfloat16,
-                                 return_acc=True, workspace=ws)
-        torch.cuda.synchronize()
-        assert (m := first_mismatch(to_np(acc), racc.astype(np.int32))) is None, m
-        assert (m := first_mismatch(bits(to_np(y)), bits(ry))) is None, m
+        for with_acc in (True, False):        # the split epilogue with and without acc_out
+            y, acc = run_gpu(ap, sa, wp, sw, "bf16", with_acc=with_acc,
+                             workspace=ws if ws is not None else
+                             p4q.w4a4_linear_workspace(M, N, K, dev))
+            if with_acc:
+                assert (m := first_mismatch(acc, racc.astype(np.int32))) is None, m
+            assert (m := first_mismatch(bits(y), bits(ry))) is None, (with_acc, m)
+
+
+@pytest.mark.parametrize("cfg_name", ["next7b_b1_k320", "next7b_b1_k640", "llava15_7b"])
+def test_batch1_layer_launches(cfg_name):
+    """The four launches of a batch-1 decoder layer (M = 384 / 704 / 256) as
+    the benchmark runs them (y only, split-K workspace given), in full against
+    the oracle on random codes."""
+    cfg = CONFIGS[cfg_name]
+    dev = torch.device("cuda:0")
+    h, f = cfg.d, cfg.linears[4].n_out
+    for N, K in ((3 * h, h), (h, h), (2 * f, h), (h, f)):
+        ap, sa, wp, sw = codes_for(cfg.M, N, K, seed=N + K + cfg.M)
+        racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
+        y, _ = run_gpu(ap, sa, wp, sw, "bf16", with_acc=False,
+                       workspace=p4q.w4a4_linear_workspace(cfg.M, N, K, dev))
+        assert (m := first_mismatch(bits(y), bits(ry))) is None, ((N, K), m)

@@ -8,7 +8,7 @@ import torch
 import oracle
 import paper_2609_34867_amd as p4q
 from workload import CONFIGS, random_features, selector_inputs
-from gpu_util import first_mismatch, to_gpu, to_np
+from gpu_util import Guarded, check_canaries, first_mismatch, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -31,8 +31,10 @@ def check(x, g, dtype="fp16", eps=1e-5, clip=1.0, ldx=None, rows=None):
         xs = pad
     xt = to_gpu(xs, dtype)[:, :d]
     gt = to_gpu(g, dtype)
-    codes, scales = p4q.rmsnorm_quant(xt, gt, eps, clip)
+    gc, gs = Guarded((M, d // 2), torch.uint8, "codes"), Guarded((M,), torch.float32, "scales")
+    codes, scales = p4q.rmsnorm_quant(xt, gt, eps, clip, codes=gc.t, scales=gs.t)
     torch.cuda.synchronize()
+    check_canaries(gc, gs)
     codes, scales = to_np(codes), to_np(scales)
     sel = np.arange(M) if rows is None else np.asarray(rows)
     rc, rs = oracle.rmsnorm_quant(x[sel], g, eps, dtype, clip)

@@ -7,7 +7,7 @@ import torch
 import oracle
 import paper_2609_34867_amd as p4q
 from workload import CONFIGS, random_features, mlp_standin, attn_standin, f32_to_bf16_bits
-from gpu_util import to_gpu, to_np, first_mismatch
+from gpu_util import Guarded, check_canaries, first_mismatch, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -20,8 +20,10 @@ def check(x, dtype, clip=1.0, ldx=None):
         xt = to_gpu(wide, dtype)[:, :K]
     else:
         xt = to_gpu(x, dtype)
-    codes, scales = p4q.quant_act(xt, clip)
+    gc, gs = Guarded((M, K // 2), torch.uint8, "codes"), Guarded((M,), torch.float32, "scales")
+    codes, scales = p4q.quant_act(xt, clip, codes=gc.t, scales=gs.t)
     torch.cuda.synchronize()
+    check_canaries(gc, gs)
     ref_codes, ref_scales = oracle.quant_act(x, dtype, clip)
     got_c, got_s = to_np(codes), to_np(scales)
     assert (m := first_mismatch(got_s.view(np.uint32), ref_scales.view(np.uint32))) is None, m

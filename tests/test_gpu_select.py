@@ -7,7 +7,7 @@ import torch
 import oracle
 import paper_2609_34867_amd as p4q
 from workload import CONFIGS, selector_inputs, random_features
-from gpu_util import to_gpu, to_np, bits, first_mismatch
+from gpu_util import Guarded, bits, check_canaries, first_mismatch, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -17,9 +17,13 @@ def run_gpu(vis, con, text, K, dtype, clip=1.0):
     J = con.shape[1]
     vt, ct = to_gpu(vis, dtype), to_gpu(con, dtype)
     tt = None if text is None else to_gpu(text, dtype)
+    T = 0 if text is None else text.shape[1]
     ws = p4q.select_workspace(B, N, d, J, vt.device)
-    idx, tok = p4q.select(vt, ct, tt, K, clip, workspace=ws)
+    gi = Guarded((B, K), torch.int32, "idx_out")
+    gt = Guarded((B, K + T, d), vt.dtype, "tokens_out")
+    idx, tok = p4q.select(vt, ct, tt, K, clip, idx_out=gi.t, tokens_out=gt.t, workspace=ws)
     torch.cuda.synchronize()
+    check_canaries(gi, gt)
     stats = to_np(ws[: B * N * (J + 1) * 4].view(torch.int32)).reshape(B, N, J + 1)
     return to_np(idx), to_np(tok), stats
 

@@ -9,7 +9,7 @@ import torch
 import oracle
 import paper_2609_34867_amd as p4q
 from workload import CONFIGS, cls_attention, random_features, selector_inputs
-from gpu_util import bits, first_mismatch, to_gpu, to_np
+from gpu_util import Guarded, bits, check_canaries, first_mismatch, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -19,8 +19,13 @@ def run_gpu(vis, con, cls, text, K, kq, ks, dtype, clip=1.0):
     vt, ct = to_gpu(vis, dtype), to_gpu(con, dtype)
     at = torch.from_numpy(np.ascontiguousarray(cls, dtype=np.float32)).cuda()
     tt = None if text is None else to_gpu(text, dtype)
-    idx, tok, stages = p4q.select_full(vt, ct, at, tt, K, kq, ks, clip, return_stages=True)
+    T = 0 if text is None else text.shape[1]
+    gi, gs = Guarded((B, K), torch.int32, "idx_out"), Guarded((B, K), torch.int32, "stages_out")
+    gt = Guarded((B, K + T, d), vt.dtype, "tokens_out")
+    idx, tok, stages = p4q.select_full(vt, ct, at, tt, K, kq, ks, clip, idx_out=gi.t,
+                                       stages_out=gs.t, tokens_out=gt.t, return_stages=True)
     torch.cuda.synchronize()
+    check_canaries(gi, gs, gt)
     return to_np(idx), to_np(tok), to_np(stages)
 
 

@@ -236,3 +236,50 @@ def test_bf16_operands_close(dtype):
         ref = np.abs(a[key]).max()
         assert np.abs(a[key] - b[key]).max() <= 2 ** -6 * ref
     assert b["grad_clip_a"] == pytest.approx(a["grad_clip_a"], rel=2 ** -6)
+
+
+@pytest.mark.parametrize("dtype,M,N,K,clip_a", [("fp16", 40, 64, 256, 0.9),
+                                                ("bf16", 96, 192, 512, 0.7),
+                                                ("fp16", 130, 128, 1024, 1.0)])
+def test_bound_covers_rounded_operands(dtype, M, N, K, clip_a):
+    """The propagated bound around the float64 result (bounds=True) covers
+    an evaluation that rounds the contraction operands to bf16 (the oracle's
+    bf16-operand mode, computed independently of the bound), and it is not
+    vacuous: it stays a small fraction of each component's own magnitude
+    scale (the operand rounding is 2^-8 relative)."""
+    p = calib_problem(M * 3 + N + K, M, N, K, dtype, clip_a=clip_a)
+    r64 = oracle.calib_linear(p.x, p.w, p.target, p.sigma, p.clip_a, p.clip_w, dtype, "fp64",
+                              bounds=True)
+    r16 = oracle.calib_linear(p.x, p.w, p.target, p.sigma, p.clip_a, p.clip_w, dtype, "bf16")
+    for key in ("grad_sigma", "grad_clip_w", "grad_clip_a", "loss"):
+        err = np.abs(np.asarray(r16[key]) - np.asarray(r64[key]))
+        assert np.all(err <= np.asarray(r64["bound_" + key])), key
+    # not vacuous: for most components the bound is well below the value
+    # itself (sigma's components are differences of larger activation- and
+    # weight-side sums, so their bound is the larger fraction)
+    rel = lambda k: np.median(r64["bound_" + k] / np.maximum(np.abs(r64[k]), 1e-30))
+    assert rel("grad_clip_w") < 0.25 and rel("grad_sigma") < 0.6
+    assert r64["bound_loss"] < 1e-2 * r64["loss"]
+
+
+def test_bound_fails_for_a_wrong_gradient():
+    """A planted mistake (the weight-side argmax share dropped) moves the
+    gradient by far more than the propagated bound, so a GPU step carrying
+    that mistake could not pass the float64 comparison."""
+    p = calib_problem(5, 48, 64, 256, "fp16", clip_a=0.9)
+    r64 = oracle.calib_linear(p.x, p.w, p.target, p.sigma, p.clip_a, p.clip_w, "fp16", "fp64",
+                              bounds=True)
+    orig = oracle.p4q_oracle.fq_row_backward
+
+    def dropped(zp, s, clip, codes, absmax, kstar, g, absolute=False):
+        dz, dc = orig(zp, s, clip, codes, absmax, kstar, g, absolute)
+        if not absolute and zp.shape[0] == p.w.shape[1] and s != 0:
+            dz = g * (np.abs(np.rint(zp / np.float32(s))) <= 8)
+        return dz, dc
+    oracle.p4q_oracle.fq_row_backward = dropped
+    try:
+        bad = oracle.calib_linear(p.x, p.w, p.target, p.sigma, p.clip_a, p.clip_w, "fp16", "fp64")
+    finally:
+        oracle.p4q_oracle.fq_row_backward = orig
+    err = np.abs(bad["grad_sigma"] - r64["grad_sigma"])
+    assert np.any(err > r64["bound_grad_sigma"])
