@@ -14,10 +14,19 @@ Four copies of the layer's weights rotate across steps so that successive
 steps read weights like successive decoder layers would (101 MB per layer at
 7B, i.e. not resident in the 256 MB MALL across the rotation).
 
+Timing: W untimed steps, then K timed steps between two synchronizations and
+a start / end event pair on the launch stream; inside them each step records
+three events only (after the selector, the quantize calls and the GEMMs), from
+which the per-phase mean, median, p10 and p90 are reported.
+
 Prints ONE JSON line.  value = W4A4 linear ops of the step / step time (TOPS);
-the selector's token rate and the GEMM-only rate are reported beside it, and,
-outside the timed steps, the fused RMSNorm + quantize prologue, the attention
-prefill, the three-stage selector (selector_full) and the decode-step GEMV.
+roofline = the GEMM phase against the int8 MFMA peak (published, and measured
+by a microbenchmark of this device); the selector's token rate and HBM
+fraction beside it.  Also reported, outside the timed steps: the same step at
+batch 1 (LLaVA-NeXT-7B, K = 320 / 640) and at the 13B stress shape, the hot-
+cache GEMM rate, the fused RMSNorm + quantize prologue, the attention prefill,
+the calibration step, the three-stage selector and the decode-step GEMV, and
+the oracle's rate on the host's cores (all of them and one).
 """
 from __future__ import annotations
 
@@ -56,6 +65,12 @@ def parse():
                     help="skip the three-stage selector measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (HBM counter calibration)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the batch-1 and 13B-shape configurations")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the MFMA and HBM microbenchmarks")
+    ap.add_argument("--step-only", action="store_true",
+                    help="only the timed steps of --config (for profiling them alone)")
     return ap.parse_args()
 
 
@@ -94,6 +109,11 @@ def setup(cfg, dev):
     st["weights"] = [[(wc.clone(), ws.clone()) for (wc, ws) in weights]
                      for _ in range(N_WEIGHT_SETS)]
     st["y"] = [torch.empty((M, wc.shape[0]), dtype=out_dt, device=dev) for (wc, _) in weights]
+    # split-K workspaces of the small-M launches (none at large M), allocated
+    # once so that no allocation happens inside the timed steps
+    k_in = {"x": cfg.d, "attn": cfg.d, "mlp": f}
+    st["gemm_ws"] = [p4q.w4a4_linear_workspace(M, wc.shape[0], k_in[src], dev)
+                     for (wc, _), (_, _, src) in zip(weights, launch_groups(cfg))]
     del weights
     torch.cuda.synchronize()
     return st
@@ -120,82 +140,214 @@ def launch_groups(cfg):
     return groups
 
 
-def step(cfg, st, layer, ev=None):
-    """One hot-path pass.  With `ev`, records an event pair around each call."""
+PHASES = ("select", "quant_act", "gemm")
+
+
+def step(cfg, st, layer, marks=None):
+    """One hot-path pass: the selector, the three quantize calls, the four
+    GEMM launches, in that order on the current stream.  `marks`, when given,
+    holds three pre-created events recorded after the selector, after the
+    quantize calls and after the GEMMs (the phase boundaries; the step's
+    start is the previous step's last mark), so a timed step records three
+    events and nothing else."""
     import paper_2609_34867_amd as p4q
 
-    def rec(name, fn):
-        if ev is None:
-            return fn()
-        e0, e1 = ev.pair(name)
-        e0.record()
-        r = fn()
-        e1.record()
-        return r
-
-    rec("select", lambda: p4q.select(st["vis"], st["con"], st["text"], cfg.K,
-                                     idx_out=st["idx"], tokens_out=st["tok"],
-                                     workspace=st["ws"]))
+    p4q.select(st["vis"], st["con"], st["text"], cfg.K, idx_out=st["idx"], tokens_out=st["tok"],
+               workspace=st["ws"])
+    if marks:
+        marks[0].record()
     x = st["tok"].view(cfg.M, cfg.d)
-    rec("quant_act", lambda: p4q.quant_act(x, codes=st["xq"][0], scales=st["xq"][1]))
-    rec("quant_act", lambda: p4q.quant_act(st["attn"], codes=st["aq"][0], scales=st["aq"][1]))
-    rec("quant_act", lambda: p4q.quant_act(st["mlp"], codes=st["mq"][0], scales=st["mq"][1]))
+    p4q.quant_act(x, codes=st["xq"][0], scales=st["xq"][1])
+    p4q.quant_act(st["attn"], codes=st["aq"][0], scales=st["aq"][1])
+    p4q.quant_act(st["mlp"], codes=st["mq"][0], scales=st["mq"][1])
+    if marks:
+        marks[1].record()
     W = st["weights"][layer % N_WEIGHT_SETS]
     src = {"x": st["xq"], "attn": st["aq"], "mlp": st["mq"]}
     for gi, (gname, members, source) in enumerate(launch_groups(cfg)):
         a = src[source]
-        rec("gemm", lambda: p4q.w4a4_linear(a[0], a[1], W[gi][0], W[gi][1],
-                                            y=st["y"][gi]))
+        p4q.w4a4_linear(a[0], a[1], W[gi][0], W[gi][1], y=st["y"][gi],
+                        workspace=st["gemm_ws"][gi])
+    if marks:
+        marks[2].record()
 
 
-class Events:
-    def __init__(self):
-        self.pairs = []
+def timed_steps(cfg, st, steps, warmup):
+    """`warmup` untimed steps, then `steps` timed ones bracketed by
+    synchronizations and a start / end event pair on the launch stream (the
+    stream the binding passes to every call).  Returns the mean ms per step
+    and the per-step duration of each phase (ms, from the phase marks)."""
+    import torch
 
-    def pair(self, name):
-        import torch
-        e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-        self.pairs.append((name, e))
-        return e
+    for i in range(warmup):
+        step(cfg, st, i)
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    marks = [[mk(), mk(), mk()] for _ in range(steps)]
+    start, end = mk(), mk()
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        step(cfg, st, i, marks[i])
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    phases = {p: [] for p in PHASES}
+    prev = start
+    for m in marks:
+        phases["select"].append(prev.elapsed_time(m[0]))
+        phases["quant_act"].append(m[0].elapsed_time(m[1]))
+        phases["gemm"].append(m[1].elapsed_time(m[2]))
+        prev = m[2]
+    return ms, phases
 
-    def totals_ms(self):
-        out = {}
-        for name, (a, b) in self.pairs:
-            out[name] = out.get(name, 0.0) + a.elapsed_time(b)
-        return out
+
+def dist(v):
+    """mean, median, p10 and p90 of per-step durations (ms)."""
+    a = np.asarray(v, dtype=np.float64)
+    return {"mean": round(float(a.mean()), 5), "median": round(float(np.median(a)), 5),
+            "p10": round(float(np.percentile(a, 10)), 5),
+            "p90": round(float(np.percentile(a, 90)), 5)}
+
+
+def selector_bytes(cfg):
+    """Algorithmic HBM bytes of one selector call: the features once, the kept
+    rows again, the text rows, the pruned sequence written."""
+    return (cfg.B * cfg.N * cfg.d * 2 + cfg.B * cfg.K * cfg.d * 2 + cfg.B * cfg.T * cfg.d * 2
+            + cfg.M * cfg.d * 2)
+
+
+def gemm_hot(cfg, st, reps=10):
+    """The step's four GEMM launches on one weight copy, repeated: operands
+    stay in the 256 MB MALL as far as they fit (the hot-cache number beside
+    the rotated, cold one of the timed steps)."""
+    import torch
+    import paper_2609_34867_amd as p4q
+
+    W = st["weights"][0]
+    src = {"x": st["xq"], "attn": st["aq"], "mlp": st["mq"]}
+
+    def run():
+        for gi, (gname, members, source) in enumerate(launch_groups(cfg)):
+            a = src[source]
+            p4q.w4a4_linear(a[0], a[1], W[gi][0], W[gi][1], y=st["y"][gi],
+                            workspace=st["gemm_ws"][gi])
+    run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def config_result(cfg, ms, phases, peak_meas=None):
+    """Per-configuration figures of the timed steps."""
+    ops = cfg.linear_ops()
+    g, s = dist(phases["gemm"]), dist(phases["select"])
+    tops = ops / (g["mean"] * 1e-3) / 1e12
+    sel_gbs = selector_bytes(cfg) / (s["mean"] * 1e-3) / 1e9
+    out = {"workload": workload_name(cfg), "ms_per_step": round(ms, 4),
+           "gemm_tops": round(tops, 2), "gemm_frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
+           "gemm_floor_ms": round(ops / (INT8_PEAK_TOPS * 1e12) * 1e3, 4),
+           "selector_us": round(s["mean"] * 1e3, 2),
+           "selector_tokens_per_s": round(cfg.B * cfg.N / (s["mean"] * 1e-3), 1),
+           "selector_gbs": round(sel_gbs, 1), "selector_hbm_frac": round(sel_gbs / HBM_PEAK_GBS, 4),
+           "selector_floor_us": round(selector_bytes(cfg) / (HBM_PEAK_GBS * 1e9) * 1e6, 2),
+           "phase_ms": {k: dist(v) for k, v in phases.items()}}
+    if peak_meas:
+        out["gemm_frac_measured_mfma_peak"] = round(tops / peak_meas, 4)
+    return out
+
+
+def workload_name(cfg):
+    return (f"{cfg.name}: select K={cfg.K} of N={cfg.N} tokens x d={cfg.d} fp16 for B={cfg.B} "
+            f"image(s) + T={cfg.T} text, then 7 W4A4 linears (h={cfg.d}, "
+            f"f={cfg.linears[4].n_out}) at M={cfg.M} as 4 launches (q|k|v, o, gate|up, down), "
+            f"{cfg.out_dtype} out")
+
+
+def peaks(dev):
+    """Measured ceilings of this device: the int8 MFMA microbenchmark (random
+    operands, 2 work-groups of 4 wavefronts per CU) and a streaming read of
+    2 GiB (2 work-groups of 4 wavefronts per CU, the fastest of 2 to 64 per
+    CU in a sweep on this MI355X: 6.98 TB/s against 5.6-6.0 with more)."""
+    import torch
+    import paper_2609_34867_amd as p4q
+
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    out = torch.empty(4 * cus * 256 * 8, dtype=torch.int32, device=dev)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            work = fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return work, e0.elapsed_time(e1) / reps
+    ops, ms = timed(lambda: p4q.diag_mfma_i8(2 * cus, 4096, out), 5)
+    src = torch.empty(1 << 31, dtype=torch.uint8, device=dev)
+    src.fill_(1)
+    nb, ms_r = timed(lambda: p4q.diag_stream_read(src, 2 * cus, out), 5)
+    del src
+    return {"mfma_i8_tops": round(ops / (ms * 1e-3) / 1e12, 1),
+            "hbm_read_gbs": round(nb / (ms_r * 1e-3) / 1e9, 1),
+            "cus": cus,
+            "note": "int8 MFMA: 2 x 4 wavefronts per CU each issuing 16 independent "
+                    "v_mfma_i32_16x16x64_i8 per round on pseudo-random operands; HBM: one "
+                    "streaming read of 2 GiB, 16-byte non-temporal loads, 2 work-groups per CU"}
 
 
 def cpu_baseline(cfg):
     """The oracle on a bounded sample of the same workload, scaled to the step:
     every image through the selector and 8192 of the pruned rows through
-    every quantize + linear (weights quantized beforehand, untimed)."""
+    every quantize + linear (weights quantized beforehand, untimed), with the
+    BLAS threads of the host (the oracle's selector and quantizer loops are
+    single-threaded Python / NumPy); then the same on one image and 1024 rows
+    with one BLAS thread."""
     import oracle
+    from threadpoolctl import threadpool_limits
     from workload import selector_inputs, weight, attn_standin, mlp_standin
 
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    n_img = cfg.B
-    si = selector_inputs(cfg, samples=list(range(n_img)))
-    toks = []
-    t0 = time.perf_counter()
-    for b in range(n_img):
-        toks.append(oracle.select(si.vis[b], si.concepts[b], si.text[b], cfg.K)[1])
-    t_sel = (time.perf_counter() - t0) / n_img
-    rows = min(8192, n_img * (cfg.K + cfg.T))
-    xs = {"x": np.concatenate(toks)[:rows],
-          "attn": attn_standin(cfg, rows), "mlp": mlp_standin(cfg, rows)}
-    t_lin = 0.0
-    for li, lin in enumerate(cfg.linears):
-        wp, sw = oracle.quant_act(weight(cfg, li))        # offline, untimed
+    si = selector_inputs(cfg, samples=list(range(cfg.B)))
+    wq = [oracle.quant_act(weight(cfg, li)) for li in range(len(cfg.linears))]   # offline, untimed
+
+    def run(n_img, rows):
+        toks = []
         t0 = time.perf_counter()
-        ap, sa = oracle.quant_act(xs[lin.source])
-        oracle.w4a4_linear(ap, sa, wp, sw, cfg.out_dtype)
-        t_lin += time.perf_counter() - t0
-    t_full = cfg.B * t_sel + (cfg.M / rows) * t_lin
+        for b in range(n_img):
+            toks.append(oracle.select(si.vis[b], si.concepts[b], si.text[b], cfg.K)[1])
+        t_sel = (time.perf_counter() - t0) / n_img
+        xs = {"x": np.concatenate(toks)[:rows],
+              "attn": attn_standin(cfg, rows), "mlp": mlp_standin(cfg, rows)}
+        t_lin = 0.0
+        for li, lin in enumerate(cfg.linears):
+            t0 = time.perf_counter()
+            ap, sa = oracle.quant_act(xs[lin.source])
+            oracle.w4a4_linear(ap, sa, wq[li][0], wq[li][1], cfg.out_dtype)
+            t_lin += time.perf_counter() - t0
+        return t_sel, t_lin, cfg.B * t_sel + (cfg.M / rows) * t_lin
+
+    rows = min(8192, cfg.B * (cfg.K + cfg.T))
+    t_sel, t_lin, t_full = run(cfg.B, rows)
+    with threadpool_limits(limits=1):
+        rows1 = min(1024, cfg.K + cfg.T)
+        t_sel1, t_lin1, t_full1 = run(1, rows1)
     return {"value": round(cfg.linear_ops() / t_full / 1e12, 6), "unit": "TOPS",
             "cores": threads, "kind": "oracle",
-            "sample": (f"{n_img} of {cfg.B} images through the selector ({n_img * t_sel:.1f}s) and "
+            "scaled_from_sample": True,
+            "sample": (f"{cfg.B} of {cfg.B} images through the selector ({cfg.B * t_sel:.1f}s) and "
                        f"{rows} of {cfg.M} rows through quantize + all 7 linears ({t_lin:.1f}s), "
-                       f"scaled to the full step ({t_full:.0f}s)")}
+                       f"scaled to the full step ({t_full:.0f}s)"),
+            "value_1thread": round(cfg.linear_ops() / t_full1 / 1e12, 6),
+            "sample_1thread": (f"1 image through the selector ({t_sel1:.1f}s) and {rows1} rows "
+                               f"through quantize + all 7 linears ({t_lin1:.1f}s) with one BLAS "
+                               f"thread, scaled to the full step ({t_full1:.0f}s)")}
 
 
 def decode_gemv(dev, steps=20):
@@ -481,33 +633,16 @@ def main():
         print(json.dumps({"decode_gemv": decode_gemv(dev)}), flush=True)
         return
     st = setup(cfg, dev)
-    for i in range(args.warmup):
-        step(cfg, st, i)
-    torch.cuda.synchronize()
-
-    # HIP events on the launch stream (torch's current stream, which the
-    # binding passes to every call): one pair around the K steps, one pair
-    # around every call inside them
-    ev = Events()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for i in range(args.steps):
-        step(cfg, st, i, ev)
-    end.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
-    tot = {k: v / args.steps for k, v in ev.totals_ms().items()}
+    ms, phases = timed_steps(cfg, st, args.steps, args.warmup)
+    if args.step_only:
+        print(json.dumps(config_result(cfg, ms, phases)), flush=True)
+        return
+    pk = None if args.no_peaks else peaks(dev)
+    main_cfg = config_result(cfg, ms, phases, pk and pk["mfma_i8_tops"])
 
     ops = cfg.linear_ops()
-    gemm_ms = tot["gemm"]
-    gemm_tops = ops / (gemm_ms * 1e-3) / 1e12
-    sel_tokens = cfg.B * cfg.N
-    sel_bytes = (cfg.B * cfg.N * cfg.d * 2                      # read features once
-                 + cfg.B * cfg.K * cfg.d * 2                    # re-read kept rows
-                 + cfg.B * cfg.T * cfg.d * 2                    # text rows
-                 + cfg.M * cfg.d * 2)                           # write pruned sequence
-    sel_gbs = sel_bytes / (tot["select"] * 1e-3) / 1e9
+    gemm_ms = main_cfg["phase_ms"]["gemm"]["mean"]
+    gemm_tops = main_cfg["gemm_tops"]
     res = {
         "metric": "W4A4 GEMM TOPS (% int8 MFMA peak) + selector tokens/s, LLaVA-NeXT-7B shape",
         "value": round(ops / (ms * 1e-3) / 1e12, 3),
@@ -516,32 +651,51 @@ def main():
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int4 (int8 MFMA, int32 acc)", "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: select K={cfg.K} of N={cfg.N} tokens x d={cfg.d} "
-                               f"fp16 for B={cfg.B} images + T={cfg.T} text, then 7 W4A4 "
-                               f"linears (h={cfg.d}, f={cfg.linears[4].n_out}) at M={cfg.M} as 4 "
-                               f"launches (q|k|v, o, gate|up, down), {cfg.out_dtype} out",
+        "config": {"workload": workload_name(cfg),
                    "B": cfg.B, "N": cfg.N, "d": cfg.d, "K": cfg.K, "T": cfg.T, "J": cfg.J,
                    "M": cfg.M, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
                      "unit": "TOPS", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
                      "traffic": traffic_from_profile(), "kernel": "k_w4a4_gemm_2cu",
-                     "per_launch": "2*M*n_out*k_in int ops, averaged over the 4 launches of a step; "
-                                   "traffic in HBM bytes per launch"},
+                     "per_launch": "2*M*n_out*k_in int ops, averaged over the 4 launches of a step "
+                                   "(HIP events around the step's GEMM phase); traffic in HBM "
+                                   "bytes per launch"},
         "gemm_tops": round(gemm_tops, 2),
-        "selector_tokens_per_s": round(sel_tokens / (tot["select"] * 1e-3), 1),
-        "selector_gbs": round(sel_gbs, 1),
-        "selector_hbm_frac": round(sel_gbs / HBM_PEAK_GBS, 4),
-        "breakdown_ms": {k: round(v, 4) for k, v in tot.items()},
+        "selector_tokens_per_s": main_cfg["selector_tokens_per_s"],
+        "selector_gbs": main_cfg["selector_gbs"],
+        "selector_hbm_frac": main_cfg["selector_hbm_frac"],
+        "phase_ms": main_cfg["phase_ms"],
         "lib": p4q.version(),
     }
+    if pk:
+        res["measured_peaks"] = pk
+        res["roofline"]["peak_measured"] = pk["mfma_i8_tops"]
+        res["roofline"]["frac_measured"] = round(gemm_tops / pk["mfma_i8_tops"], 4)
+        res["selector_frac_measured_read_peak"] = round(main_cfg["selector_gbs"] / pk["hbm_read_gbs"], 4)
+    hot_ms = gemm_hot(cfg, st)
+    res["gemm_hot_cache"] = {"ms": round(hot_ms, 4),
+                             "tops": round(ops / (hot_ms * 1e-3) / 1e12, 2),
+                             "note": "the 4 launches on one weight copy, repeated (the timed "
+                                     "steps rotate 4 copies: cold weights)"}
     res["prologue_rmsnorm_quant"] = prologue(cfg, st, dev)
+    del st
+    torch.cuda.empty_cache()
+    if not args.no_configs:
+        others = {}
+        for name in ("next7b_b1_k320", "next7b_b1_k640", "stress13b_b8"):
+            c = CONFIGS[name]
+            sc = setup(c, dev)
+            cms, cph = timed_steps(c, sc, 20, 5)
+            others[name] = config_result(c, cms, cph, pk and pk["mfma_i8_tops"])
+            del sc
+            torch.cuda.empty_cache()
+        res["configs"] = others
     res["attention_prefill"] = attention(cfg, dev)
     if not args.no_calib:
         res["calibration_step"] = calibration(dev)
     if not args.no_select_full:
         res["selector_full"] = selector_full(cfg, dev)
     if not args.no_decode:
-        del st
         torch.cuda.empty_cache()
         res["decode_gemv"] = decode_gemv(dev)
     if not args.no_cpu_baseline:

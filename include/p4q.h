@@ -307,6 +307,26 @@ int p4q_w4a4_linear(int M, int N_out, int K_in,
                     p4q_dtype out_dt, void *y, int64_t ldy, int32_t *acc_out,
                     void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Diagnostics: microbenchmarks of the device's own ceilings, against which
+ * the kernels above are reported beside the published peaks.  They are not
+ * part of the method.
+ *
+ * p4q_diag_mfma_i8: `blocks` work-groups of 256 threads; every wavefront
+ *   issues iters x 16 independent v_mfma_i32_16x16x64_i8 on pseudo-random
+ *   operands, i.e. blocks * 4 * iters * 16 * 32768 integer operations.
+ *   out int32 [blocks * 256] receives a checksum per thread.
+ * p4q_diag_stream_read: reads the `bytes` (a multiple of 16) at src with
+ *   `blocks` work-groups of 256 threads, 16 bytes per load;
+ *   out uint32 [blocks * 256] receives a checksum per thread.
+ * Limits: blocks in [1, 2^20], iters in [1, 2^20]; src 16-byte aligned,
+ *   out 4-byte aligned.
+ * ---------------------------------------------------------------------- */
+int p4q_diag_mfma_i8(int blocks, int iters, int32_t *out, hipStream_t stream);
+
+int p4q_diag_stream_read(const void *src, size_t bytes, int blocks, uint32_t *out,
+                         hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -48,6 +48,8 @@ SIGNATURES = {
     "p4q_w4a4_linear_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int]),
     "p4q_w4a4_linear": (_c_int, [_c_int, _c_int, _c_int, _vp, _vp, _vp, _vp, _c_int, _vp,
                                  _c_i64, _vp, _vp, _c_size, _vp]),
+    "p4q_diag_mfma_i8": (_c_int, [_c_int, _c_int, _vp, _vp]),
+    "p4q_diag_stream_read": (_c_int, [_vp, _c_size, _c_int, _vp, _vp]),
 }
 
 _lib = None

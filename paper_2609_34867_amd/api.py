@@ -398,3 +398,29 @@ def w4a4_linear(a_codes: torch.Tensor, a_scales: torch.Tensor, w_codes: torch.Te
                                _ptr(acc_out), _ptr(workspace), ws_bytes, _stream(dev))
     check(st)
     return (y, acc_out) if return_acc else y
+
+
+# --------------------------------------------------------------------------- diagnostics
+def diag_mfma_i8(blocks: int, iters: int, out: torch.Tensor) -> int:
+    """Enqueue the int8 MFMA microbenchmark (p4q_diag_mfma_i8) writing its
+    checksums to out (int32, >= blocks * 256 entries); returns the integer
+    operations it performs."""
+    _check(out, "out", None, torch.int32)
+    if out.numel() < blocks * 256:
+        raise ValueError(f"out needs {blocks * 256} entries")
+    _need_gpu(out)
+    check(lib().p4q_diag_mfma_i8(blocks, iters, _ptr(out), _stream(out.device)))
+    return blocks * 4 * iters * 16 * 2 * 16 * 16 * 64
+
+
+def diag_stream_read(src: torch.Tensor, blocks: int, out: torch.Tensor) -> int:
+    """Enqueue the HBM read microbenchmark (p4q_diag_stream_read) over the
+    bytes of src; returns the bytes read."""
+    _check(src, "src", None, None)
+    _check(out, "out", None, torch.int32)
+    if out.numel() < blocks * 256:
+        raise ValueError(f"out needs {blocks * 256} entries")
+    nbytes = src.numel() * src.element_size()
+    _need_gpu(src, out)
+    check(lib().p4q_diag_stream_read(_ptr(src), nbytes, blocks, _ptr(out), _stream(src.device)))
+    return nbytes

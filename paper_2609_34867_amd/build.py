@@ -20,7 +20,7 @@ BUILD_DIR = os.path.join(REPO, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "libp4q.so")
 
 SOURCES = ["p4q_api.hip", "quant_act.hip", "prologue.hip", "select.hip", "diversity.hip", "calib.hip",
-           "w4a4_gemm.hip", "attention.hip"]
+           "w4a4_gemm.hip", "attention.hip", "diag.hip"]
 
 ARCH = "gfx950"
 HIPCC_FLAGS = [

@@ -67,27 +67,39 @@ size_t p4q_select_workspace_bytes(int B, int N, int d, int J) {
     return p4q::select_workspace_bytes(B, N, d, J);
 }
 
+// Checks of p4q_select's arguments, everything but the
+// workspace.  Returns P4Q_OK or the failing status (message recorded).
+static int check_select_args(const char *who, p4q_dtype dt, int B, int N, int d,
+                             const void *vis, const void *concepts, int J, const void *text,
+                             int T, int K, float clip, const int32_t *idx_out,
+                             const void *tokens_out) {
+    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "%s: dtype %d", who, (int)dt);
+    if (B <= 0 || N <= 0 || d <= 0 || J <= 0 || K <= 0 || T < 0)
+        return fail(P4Q_ERR_INVALID_ARG, "%s: sizes must be positive (B=%d N=%d d=%d J=%d K=%d T=%d)",
+                    who, B, N, d, J, K, T);
+    if (K > N) return fail(P4Q_ERR_INVALID_ARG, "%s: K=%d > N=%d", who, K, N);
+    if (!vis || !concepts || !idx_out || !tokens_out)
+        return fail(P4Q_ERR_INVALID_ARG, "%s: null pointer", who);
+    if ((T > 0) != (text != nullptr))
+        return fail(P4Q_ERR_INVALID_ARG, "%s: text must be given iff T > 0", who);
+    if (!valid_clip(clip)) return fail(P4Q_ERR_INVALID_ARG, "%s: clip %g outside [2^-16, 1]", who, clip);
+    if (d % 32 != 0) return fail(P4Q_ERR_INVALID_ARG, "%s: d=%d not a multiple of 32", who, d);
+    if (!aligned(vis, 16) || !aligned(concepts, 16) || !aligned(tokens_out, 16) ||
+        (text && !aligned(text, 16)) || !aligned(idx_out, 4))
+        return fail(P4Q_ERR_INVALID_ARG, "%s: misaligned pointer", who);
+    if (N > 8192) return fail(P4Q_ERR_UNSUPPORTED, "%s: N=%d > 8192", who, N);
+    if (J > 8) return fail(P4Q_ERR_UNSUPPORTED, "%s: J=%d > 8", who, J);
+    if (d > 16384) return fail(P4Q_ERR_UNSUPPORTED, "%s: d=%d > 16384", who, d);
+    if (J > 4 && d > 8192) return fail(P4Q_ERR_UNSUPPORTED, "%s: J > 4 needs d <= 8192", who);
+    return P4Q_OK;
+}
+
 int p4q_select(p4q_dtype dt, int B, int N, int d, const void *vis, const void *concepts, int J,
                const void *text, int T, int K, float clip, int32_t *idx_out, void *tokens_out,
                void *ws, size_t ws_bytes, hipStream_t stream) {
-    if (!valid_dtype(dt)) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: dtype %d", (int)dt);
-    if (B <= 0 || N <= 0 || d <= 0 || J <= 0 || K <= 0 || T < 0)
-        return fail(P4Q_ERR_INVALID_ARG, "p4q_select: sizes must be positive (B=%d N=%d d=%d J=%d K=%d T=%d)",
-                    B, N, d, J, K, T);
-    if (K > N) return fail(P4Q_ERR_INVALID_ARG, "p4q_select: K=%d > N=%d", K, N);
-    if (!vis || !concepts || !idx_out || !tokens_out)
-        return fail(P4Q_ERR_INVALID_ARG, "p4q_select: null pointer");
-    if ((T > 0) != (text != nullptr))
-        return fail(P4Q_ERR_INVALID_ARG, "p4q_select: text must be given iff T > 0");
-    if (!valid_clip(clip)) return fail(P4Q_ERR_INVALID_ARG, "p4q_select: clip %g outside [2^-16, 1]", clip);
-    if (d % 32 != 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_select: d=%d not a multiple of 32", d);
-    if (!aligned(vis, 16) || !aligned(concepts, 16) || !aligned(tokens_out, 16) ||
-        (text && !aligned(text, 16)) || !aligned(idx_out, 4))
-        return fail(P4Q_ERR_INVALID_ARG, "p4q_select: misaligned pointer");
-    if (N > 8192) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: N=%d > 8192", N);
-    if (J > 8) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: J=%d > 8", J);
-    if (d > 16384) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: d=%d > 16384", d);
-    if (J > 4 && d > 8192) return fail(P4Q_ERR_UNSUPPORTED, "p4q_select: J > 4 needs d <= 8192");
+    if (const int st = check_select_args("p4q_select", dt, B, N, d, vis, concepts, J, text, T, K,
+                                         clip, idx_out, tokens_out))
+        return st;
     const size_t need = p4q::select_workspace_bytes(B, N, d, J);
     if (!ws || ws_bytes < need)
         return fail(P4Q_ERR_WORKSPACE, "p4q_select: workspace %zu < %zu bytes", ws_bytes, need);
@@ -291,6 +303,22 @@ int p4q_calib_linear_grad(p4q_dtype dt, int M, int N, int K, const void *x, int6
                                                clip_w, loss, grad_sigma, grad_clip_a, grad_clip_w, ws,
                                                stream),
                       "p4q_calib_linear_grad");
+}
+
+int p4q_diag_mfma_i8(int blocks, int iters, int32_t *out, hipStream_t stream) {
+    if (blocks < 1 || blocks > (1 << 20) || iters < 1 || iters > (1 << 20))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_diag_mfma_i8: blocks=%d iters=%d", blocks, iters);
+    if (!out || !aligned(out, 4)) return fail(P4Q_ERR_INVALID_ARG, "p4q_diag_mfma_i8: out");
+    return hip_status(p4q::launch_diag_mfma_i8(blocks, iters, out, stream), "p4q_diag_mfma_i8");
+}
+
+int p4q_diag_stream_read(const void *src, size_t bytes, int blocks, uint32_t *out,
+                         hipStream_t stream) {
+    if (blocks < 1 || blocks > (1 << 20) || bytes % 16 != 0 || bytes == 0)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_diag_stream_read: blocks=%d bytes=%zu", blocks, bytes);
+    if (!src || !out || !aligned(src, 16) || !aligned(out, 4))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_diag_stream_read: pointer");
+    return hip_status(p4q::launch_diag_read(src, bytes, blocks, out, stream), "p4q_diag_stream_read");
 }
 
 }  // extern "C"

@@ -130,4 +130,9 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
                             int64_t ldy, int32_t *acc_out, void *ws, size_t ws_bytes,
                             hipStream_t stream);
 
+// ---- diagnostics (diag.hip) ----------------------------------------------------
+hipError_t launch_diag_mfma_i8(int blocks, int iters, int32_t *out, hipStream_t stream);
+hipError_t launch_diag_read(const void *src, size_t bytes, int blocks, uint32_t *out,
+                            hipStream_t stream);
+
 }  // namespace p4q
