@@ -107,6 +107,31 @@ int p4q_select(p4q_dtype dt, int B, int N, int d,
                void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * p4q_select without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  It computes exactly what p4q_select
+ * computes, with the same arguments, checks and results, and calls no
+ * allocating routine.
+ *
+ * Its workspace is a static device array of P4Q_SELECT_SCRATCH_BYTES (8 MiB)
+ * that every device the library runs on holds until the process ends.  A
+ * call needs p4q_select_workspace_bytes(B, N, d, J) bytes of it (2.7 MB for
+ * 16 images of 2880 tokens, d = 4096, J = 4); a larger request returns
+ * P4Q_ERR_WORKSPACE and enqueues nothing.  No part of the array is read
+ * before the same call has written it, so nothing needs clearing between
+ * calls.  Calls on one device share the array: calls that overlap in time on
+ * one device (concurrent streams, or host threads) race and must not be
+ * issued.  The first call on a device looks up the array's device address
+ * (with the stream's device current) and may fail with P4Q_ERR_HIP.
+ * ---------------------------------------------------------------------- */
+#define P4Q_SELECT_SCRATCH_BYTES (8u << 20)
+
+int p4q_select_noalloc(p4q_dtype dt, int B, int N, int d,
+                       const void *vis, const void *concepts, int J,
+                       const void *text, int T, int K, float clip,
+                       int32_t *idx_out, void *tokens_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * The three-stage quantization-aware selector (Sec. 3.2, Eq.
  * p4q_progressive_selection: Query Relevance, Visual Saliency, Visual
  * Diversity, with budgets kq + ks + kd = K).

@@ -28,6 +28,8 @@ SIGNATURES = {
     "p4q_select_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
     "p4q_select": (_c_int, [_c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _vp, _c_int,
                             _c_int, _c_float, _vp, _vp, _vp, _c_size, _vp]),
+    "p4q_select_noalloc": (_c_int, [_c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _vp, _c_int,
+                                    _c_int, _c_float, _vp, _vp, _vp]),
     "p4q_select_full_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "p4q_select_budgets": (_c_int, [_c_int, ctypes.POINTER(_c_int), ctypes.POINTER(_c_int),
                                     ctypes.POINTER(_c_int)]),

@@ -131,6 +131,28 @@ def select(vis: torch.Tensor, concepts: torch.Tensor, text: Optional[torch.Tenso
     return idx_out, tokens_out
 
 
+def select_noalloc(vis: torch.Tensor, concepts: torch.Tensor, text: Optional[torch.Tensor],
+                   K: int, clip: float = 1.0, idx_out: Optional[torch.Tensor] = None,
+                   tokens_out: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """select() without a workspace (p4q_select_noalloc): the library's
+    per-device scratch array serves instead, so with idx_out and tokens_out
+    given nothing is allocated.  Calls that overlap on one device race."""
+    B, N, d, J, T = _selector_shapes(vis, concepts, text)
+    _check(idx_out, "idx_out", (B, K), torch.int32)
+    _check(tokens_out, "tokens_out", (B, K + T, d), vis.dtype)
+    _need_gpu(vis, concepts, text, idx_out, tokens_out)
+    dev = vis.device
+    if idx_out is None:
+        idx_out = torch.empty((B, K), dtype=torch.int32, device=dev)
+    if tokens_out is None:
+        tokens_out = torch.empty((B, K + T, d), dtype=vis.dtype, device=dev)
+    st = lib().p4q_select_noalloc(_dtype_code(vis.dtype), B, N, d, _ptr(vis), _ptr(concepts), J,
+                                  _ptr(text) if T > 0 else None, T, K, ctypes.c_float(clip),
+                                  _ptr(idx_out), _ptr(tokens_out), _stream(dev))
+    check(st)
+    return idx_out, tokens_out
+
+
 def select_budgets(K: int) -> Tuple[int, int, int]:
     """The default (Query Relevance, Visual Saliency, Visual Diversity) token
     budgets for K kept tokens (p4q_select_budgets)."""

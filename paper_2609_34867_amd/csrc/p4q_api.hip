@@ -67,7 +67,7 @@ size_t p4q_select_workspace_bytes(int B, int N, int d, int J) {
     return p4q::select_workspace_bytes(B, N, d, J);
 }
 
-// Checks of p4q_select's arguments, everything but the
+// Checks shared by p4q_select and p4q_select_noalloc: everything but the
 // workspace.  Returns P4Q_OK or the failing status (message recorded).
 static int check_select_args(const char *who, p4q_dtype dt, int B, int N, int d,
                              const void *vis, const void *concepts, int J, const void *text,
@@ -108,6 +108,76 @@ int p4q_select(p4q_dtype dt, int B, int N, int d, const void *vis, const void *c
     return hip_status(p4q::launch_select(dt, B, N, d, vis, concepts, J, text, T, K, clip, idx_out,
                                          tokens_out, w, stream),
                       "p4q_select");
+}
+
+}  // extern "C"
+
+// ---- the selector without a caller-supplied workspace ------------------------
+// Its workspace lives in `scratch`, one array per device in the library's
+// device image.  In host code the name `scratch` is only a stand-in for the
+// symbol: its device address is looked up (hipGetSymbolAddress) once per
+// device, with that device current, and only that address is ever passed on.
+static __device__ __align__(256) uint8_t scratch[P4Q_SELECT_SCRATCH_BYTES];
+
+namespace {
+
+std::atomic<uintptr_t> g_scratch_addr[p4q::kMaxDevices];
+
+// Device address of `scratch` on the device `stream` belongs to (the
+// caller's current device for the null stream).  Returns P4Q_OK or an error
+// status with the message recorded.
+int scratch_address(hipStream_t stream, void **addr, const char *who) {
+    int dev = 0, cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e == hipSuccess) {
+        dev = cur;
+        if (stream) e = hipStreamGetDevice(stream, &dev);
+    }
+    if (e != hipSuccess) return fail(P4Q_ERR_HIP, "%s: device of the stream: %s", who, hipGetErrorString(e));
+    if (dev < 0 || dev >= p4q::kMaxDevices)
+        return fail(P4Q_ERR_UNSUPPORTED, "%s: device %d beyond the %d supported", who, dev, p4q::kMaxDevices);
+    uintptr_t a = g_scratch_addr[dev].load(std::memory_order_acquire);
+    if (a == 0) {
+        // with that device current: each device holds its own copy of the array
+        if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess)
+            return fail(P4Q_ERR_HIP, "%s: hipSetDevice(%d): %s", who, dev, hipGetErrorString(e));
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        const hipError_t e2 = (dev != cur) ? hipSetDevice(cur) : hipSuccess;
+        if (e != hipSuccess || p == nullptr)
+            return fail(P4Q_ERR_HIP, "%s: hipGetSymbolAddress(scratch): %s", who,
+                        hipGetErrorString(e != hipSuccess ? e : hipErrorInvalidSymbol));
+        if (e2 != hipSuccess)
+            return fail(P4Q_ERR_HIP, "%s: hipSetDevice(%d): %s", who, cur, hipGetErrorString(e2));
+        a = reinterpret_cast<uintptr_t>(p);
+        g_scratch_addr[dev].store(a, std::memory_order_release);   // racing first calls store the same
+    }
+    *addr = reinterpret_cast<void *>(a);
+    return P4Q_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int p4q_select_noalloc(p4q_dtype dt, int B, int N, int d, const void *vis, const void *concepts,
+                       int J, const void *text, int T, int K, float clip, int32_t *idx_out,
+                       void *tokens_out, hipStream_t stream) {
+    if (const int st = check_select_args("p4q_select_noalloc", dt, B, N, d, vis, concepts, J, text,
+                                         T, K, clip, idx_out, tokens_out))
+        return st;
+    const size_t need = p4q::select_workspace_bytes(B, N, d, J);
+    if (need > (size_t)P4Q_SELECT_SCRATCH_BYTES)
+        return fail(P4Q_ERR_WORKSPACE,
+                    "p4q_select_noalloc: B=%d N=%d d=%d J=%d needs %zu bytes of scratch, more than "
+                    "the %zu the library holds per device (use p4q_select with a workspace)",
+                    B, N, d, J, need, (size_t)P4Q_SELECT_SCRATCH_BYTES);
+    void *ws = nullptr;
+    if (const int st = scratch_address(stream, &ws, "p4q_select_noalloc")) return st;
+    const p4q::SelectWorkspace w = p4q::select_workspace_carve(ws, B, N, d, J);
+    return hip_status(p4q::launch_select(dt, B, N, d, vis, concepts, J, text, T, K, clip, idx_out,
+                                         tokens_out, w, stream),
+                      "p4q_select_noalloc");
 }
 
 size_t p4q_select_full_workspace_bytes(int B, int N, int d, int J, int K) {
