@@ -672,3 +672,243 @@ def calib_linear(x: np.ndarray, w: np.ndarray, target: np.ndarray, sigma: np.nda
         eR = 3.0 * u * (absY + absR)
         out["bound_loss"] = float(np.sum(2.0 * absR * eR + eR * eR)) / (M * N) + gam(M * N) * loss
     return out
+
+
+# --------------------------------------------------------------------------
+# O8: pruning-aware calibration of a whole decoder block (Sec. 3.3, Eq.
+#     p4q_pruning_aware_calibration: the per-sample MSE between the W4A4
+#     fake-quantized block and the full-precision block on the pruned
+#     sequence; Appendix B.3: block by block, diagonal scales and weight /
+#     activation clipping factors learned, K and V kept in FP16)
+# --------------------------------------------------------------------------
+BLOCK_GROUPS = ("qkv", "o", "gu", "down")     # the block's four fake-quantized linear groups
+
+
+def _r16(v: np.ndarray, dtype: str) -> np.ndarray:
+    """Round real values to the block's storage dtype (nearest, ties to
+    even); returned as float64 holding the 16-bit values exactly."""
+    if dtype == "fp16":
+        return np.asarray(v, dtype=np.float64).astype(np.float16).astype(np.float64)
+    return as_f32(f32_to_bf16_rne(np.asarray(v, dtype=np.float64).astype(np.float32)),
+                  "bf16").astype(np.float64)
+
+
+def _store16(v64: np.ndarray, dtype: str) -> np.ndarray:
+    """float64 values that are exact 16-bit numbers -> storage array."""
+    if dtype == "fp16":
+        return v64.astype(np.float16)
+    return f32_to_bf16_rne(v64.astype(np.float32))
+
+
+def _rope_tables(M: int, D: int, base: float):
+    """cos / sin of position p times theta_i = base^(-2i/D), i < D/2,
+    positions 0..M-1 (the pruned sequence re-indexed consecutively)."""
+    i = np.arange(D // 2, dtype=np.float64)
+    theta = base ** (-2.0 * i / D)
+    ang = np.arange(M, dtype=np.float64)[:, None] * theta[None, :]
+    return np.cos(ang), np.sin(ang)
+
+
+def _rope(z: np.ndarray, cos: np.ndarray, sin: np.ndarray, inverse: bool = False) -> np.ndarray:
+    """Rotary embedding of z [M, H, D] (rotate-half pairing of channel i
+    with i + D/2); inverse=True applies the transposed rotation (its
+    backward)."""
+    h = z.shape[2] // 2
+    a, b = z[:, :, :h], z[:, :, h:]
+    c, s = cos[:, None, :], sin[:, None, :]
+    if inverse:
+        s = -s
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=2)
+
+
+def _rmsnorm(x: np.ndarray, g: np.ndarray, eps: float):
+    """n = x * gamma / sqrt(mean(x^2) + eps) in real arithmetic; returns (n,
+    r = 1/rms per row)."""
+    r = 1.0 / np.sqrt(np.mean(x * x, axis=1) + eps)
+    return x * r[:, None] * g[None, :], r
+
+
+def _rmsnorm_backward(x, g, r, dn):
+    """dL/dx of n = x gamma r(x):  r gamma dn - x r^3 / d sum_j x_j gamma_j dn_j."""
+    d = x.shape[1]
+    s = np.sum(x * g[None, :] * dn, axis=1)
+    return r[:, None] * g[None, :] * dn - x * (r ** 3 * s / d)[:, None]
+
+
+def _attention(q, k, v):
+    """Causal softmax attention per head in real arithmetic: q, k, v [M, H,
+    D] -> (O [M, H, D], P [H, M, M])."""
+    M, H, D = q.shape
+    causal = np.tril(np.ones((M, M), dtype=bool))
+    P = np.empty((H, M, M), dtype=np.float64)
+    O = np.empty((M, H, D), dtype=np.float64)
+    for hh in range(H):
+        S = np.where(causal, (q[:, hh, :] @ k[:, hh, :].T) / np.sqrt(D), -np.inf)
+        E = np.exp(S - S.max(axis=1, keepdims=True))
+        P[hh] = E / E.sum(axis=1, keepdims=True)
+        O[:, hh, :] = P[hh] @ v[:, hh, :]
+    return O, P
+
+
+def _attention_backward(q, k, v, P, dO):
+    """(dq, dk, dv) of O = P v, P = softmax(q k^T / sqrt(D)):
+    dv = P^T dO, dP = dO v^T, dS = P (dP - rowsum(P dP)), dq = dS k / sqrt(D),
+    dk = dS^T q / sqrt(D)."""
+    M, H, D = q.shape
+    dq, dk, dv = (np.empty((M, H, D)) for _ in range(3))
+    for hh in range(H):
+        dv[:, hh, :] = P[hh].T @ dO[:, hh, :]
+        dP = dO[:, hh, :] @ v[:, hh, :].T
+        dS = P[hh] * (dP - np.sum(P[hh] * dP, axis=1, keepdims=True))
+        dq[:, hh, :] = dS @ k[:, hh, :] / np.sqrt(D)
+        dk[:, hh, :] = dS.T @ q[:, hh, :] / np.sqrt(D)
+    return dq, dk, dv
+
+
+def _silu_mul_backward(g, u, da):
+    """(dg, du) of a = SiLU(g) u = g sig(g) u, sig the logistic function:
+    dSiLU/dg = sig(g) (1 + g (1 - sig(g)))."""
+    sg = 1.0 / (1.0 + np.exp(-g))
+    return da * u * sg * (1.0 + g * (1.0 - sg)), da * g * sg
+
+
+def _fq_linear(X16, W16, sigma, clip_a, clip_w, dtype):
+    """The W4A4 fake-quantized linear of calib_linear, applied in a block:
+    X' = X / sigma and W' = W * sigma quantized per row (clip_a, clip_w[n]),
+    Y = out_rne(fl32(fl32(acc sA) sW)) in the storage dtype (the epilogue of
+    the W4A4 linear).  Returns (Y as float64 values, the quantizer state)."""
+    cA, sA, aA, kA, xp = quant_rows_scaled(X16, sigma, True, np.float32(clip_a), dtype)
+    cW, sW, aW, kW, wp = quant_rows_scaled(W16, sigma, False, clip_w, dtype)
+    acc = int_gemm(cA, cW)
+    y = as_f32(epilogue(acc, sA, sW, dtype), dtype).astype(np.float64)
+    q = {"a_codes": cA, "a_scales": sA, "a_absmax": aA, "a_kstar": kA, "xp": xp,
+         "clip_a": np.float32(clip_a), "w_codes": cW, "w_scales": sW, "w_absmax": aW,
+         "w_kstar": kW, "wp": wp, "clip_w": np.asarray(clip_w, dtype=np.float32),
+         "sigma": np.asarray(sigma, dtype=np.float32),
+         "x64": as_f32(X16, dtype).astype(np.float64), "w64": as_f32(W16, dtype).astype(np.float64)}
+    return y, q
+
+
+def _fq_linear_backward(q, G):
+    """Gradients of a fake-quantized linear from G = dL/dY (rounding of the
+    output passed straight through): (dL/dX [M, K], dL/dsigma [K],
+    dL/dclip_a, dL/dclip_w [N]).  Per row as fq_row_backward; X' = X / sigma
+    gives dX = dX' / sigma."""
+    cA, cW = q["a_codes"].astype(np.float64), q["w_codes"].astype(np.float64)
+    sA, sW = q["a_scales"].astype(np.float64), q["w_scales"].astype(np.float64)
+    gA = G @ (sW[:, None] * cW)                      # dL/d(sA cA)  [M, K]
+    gW = G.T @ (sA[:, None] * cA)                    # dL/d(sW cW)  [N, K]
+    M, N = G.shape
+    dxp = np.zeros(q["xp"].shape, dtype=np.float64)
+    dwp = np.zeros(q["wp"].shape, dtype=np.float64)
+    dclip_a = 0.0
+    dclip_w = np.zeros(N, dtype=np.float64)
+    for m in range(M):
+        dxp[m], dc = fq_row_backward(q["xp"][m], q["a_scales"][m], q["clip_a"], q["a_codes"][m],
+                                     q["a_absmax"][m], q["a_kstar"][m], gA[m])
+        dclip_a += dc
+    for n in range(N):
+        dwp[n], dclip_w[n] = fq_row_backward(q["wp"][n], q["w_scales"][n], q["clip_w"][n],
+                                             q["w_codes"][n], q["w_absmax"][n], q["w_kstar"][n],
+                                             gW[n])
+    s64 = q["sigma"].astype(np.float64)
+    dsigma = (np.sum(dxp * (-q["x64"] / (s64 * s64)[None, :]), axis=0)
+              + np.sum(dwp * q["w64"], axis=0))
+    return dxp / s64[None, :], dsigma, dclip_a, dclip_w
+
+
+def calib_block(x: np.ndarray, weights: dict, gamma1: np.ndarray, gamma2: np.ndarray,
+                H: int, target: np.ndarray = None, sigma: dict = None, clip_a: dict = None,
+                clip_w: dict = None, eps: float = 1e-5, rope_base: float = 10000.0,
+                dtype: str = "fp16", quantize: bool = True) -> dict:
+    """One decoder block on one pruned sequence, full precision or W4A4
+    fake-quantized, and for the latter the calibration loss and gradients.
+
+    x [M, d] is the block input (storage dtype); weights holds "qkv" [3d, d]
+    (q, k, v rows concatenated), "o" [d, d], "gu" [2f, d] (gate then up) and
+    "down" [d, f]; gamma1, gamma2 [d] the RMSNorm weights; H heads of D =
+    d / H.  The block (LLaMA-family decoder, intermediates held in the
+    storage dtype between operations, each rounded once, nearest even):
+        n1 = RMSNorm(x) gamma1;  q|k|v = L_qkv(n1);  q, k <- RoPE(q), RoPE(k)
+        O = softmax(q k^T / sqrt(D), causal) v   (per head, real arithmetic)
+        h = x + L_o(O);  n2 = RMSNorm(h) gamma2;  g|u = L_gu(n2)
+        a = SiLU(g) u;   out = h + L_down(a)
+    With quantize=False every L is the plain linear (X W^T, rounded): the
+    full-precision block whose output is the calibration target.  With
+    quantize=True every L is the W4A4 fake-quantized linear of calib_linear
+    with its group's diagonal scales sigma[g] (dividing the input channels,
+    multiplying the weights' input channels), activation clipping factor
+    clip_a[g] and per-output-channel weight clipping factors clip_w[g];
+    loss = ||out - target||^2 / (M d) (the per-sample term of the calibration
+    objective), and its gradients with respect to every sigma, clip_a and
+    clip_w (rounding of codes and of intermediates passed straight through,
+    clamp and row maxima as in fq_row_backward), by the chain rule through
+    the full-precision attention, RMSNorm and SiLU-gated MLP.
+
+    Returns {"out": out (storage dtype)} and, with quantize and target,
+    "loss", "grad_sigma"[g], "grad_clip_a"[g], "grad_clip_w"[g] (float64)."""
+    r16 = lambda v: _r16(v, dtype)
+    X = as_f32(x, dtype).astype(np.float64)
+    M, d = X.shape
+    D = d // H
+    g1 = as_f32(gamma1, dtype).astype(np.float64)
+    g2 = as_f32(gamma2, dtype).astype(np.float64)
+
+    def lin(name, A16):
+        if not quantize:
+            W = as_f32(weights[name], dtype).astype(np.float64)
+            return r16(A16 @ W.T), None
+        return _fq_linear(_store16(A16, dtype), weights[name], sigma[name], clip_a[name],
+                          clip_w[name], dtype)
+
+    # ---- forward
+    n1f, r1 = _rmsnorm(X, g1, eps)
+    n1 = r16(n1f)
+    qkv, c_qkv = lin("qkv", n1)
+    cos, sin = _rope_tables(M, D, rope_base)
+    q = r16(_rope(qkv[:, :d].reshape(M, H, D), cos, sin))
+    k = r16(_rope(qkv[:, d:2 * d].reshape(M, H, D), cos, sin))
+    v = qkv[:, 2 * d:].reshape(M, H, D)
+    O, P = _attention(q, k, v)
+    O = r16(O).reshape(M, d)
+    o, c_o = lin("o", O)
+    h = r16(X + o)
+    n2f, r2 = _rmsnorm(h, g2, eps)
+    n2 = r16(n2f)
+    gu, c_gu = lin("gu", n2)
+    f = gu.shape[1] // 2
+    gg, uu = gu[:, :f], gu[:, f:]
+    sig_g = 1.0 / (1.0 + np.exp(-gg))
+    a = r16(gg * sig_g * uu)
+    y, c_down = lin("down", a)
+    out = r16(h + y)
+    res = {"out": _store16(out, dtype)}
+    if not quantize or target is None:
+        return res
+
+    # ---- loss and backward (straight through every rounding)
+    T = np.asarray(target, dtype=np.float64)
+    R = out - T
+    res["loss"] = float(np.sum(R * R)) / (M * d)
+    dout = 2.0 * R / (M * d)
+    grads = {}
+
+    def back(name, cache, G):
+        dX, ds, dca, dcw = _fq_linear_backward(cache, G)
+        grads[name] = (ds, dca, dcw)
+        return dX
+
+    da = back("down", c_down, dout)
+    dg, du = _silu_mul_backward(gg, uu, da)
+    dn2 = back("gu", c_gu, np.concatenate([dg, du], axis=1))
+    dh = dout + _rmsnorm_backward(h, g2, r2, dn2)
+    dO = back("o", c_o, dh).reshape(M, H, D)
+    dq, dk, dv = _attention_backward(q, k, v, P, dO)
+    dq = _rope(dq, cos, sin, inverse=True)
+    dk = _rope(dk, cos, sin, inverse=True)
+    back("qkv", c_qkv, np.concatenate([dq.reshape(M, d), dk.reshape(M, d), dv.reshape(M, d)],
+                                      axis=1))
+    res["grad_sigma"] = {g: grads[g][0] for g in BLOCK_GROUPS}
+    res["grad_clip_a"] = {g: grads[g][1] for g in BLOCK_GROUPS}
+    res["grad_clip_w"] = {g: grads[g][2] for g in BLOCK_GROUPS}
+    return res

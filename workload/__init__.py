@@ -308,3 +308,52 @@ def calib_problem(seed: int, M: int, N: int, K: int, dtype: str = "fp16",
     xf, wf = to_f32(x, dtype).astype(np.float64), to_f32(w, dtype).astype(np.float64)
     target = (xf @ wf.T).astype(np.float32)
     return CalibProblem(x, w, target, sigma.astype(np.float32), float(clip_a), clip_w, dtype)
+
+
+@dataclass
+class CalibBlockProblem:
+    x: np.ndarray          # [M, d] block input (storage dtype)
+    weights: dict          # "qkv" [3d, d], "o" [d, d], "gu" [2f, d], "down" [d, f]
+    gamma1: np.ndarray     # [d]
+    gamma2: np.ndarray     # [d]
+    sigma: dict            # per group: fp32 [input width]
+    clip_a: dict           # per group: float
+    clip_w: dict           # per group: fp32 [output width]
+    H: int
+    dtype: str
+
+
+def calib_block_problem(seed: int, M: int, d: int, f: int, H: int,
+                        dtype: str = "fp16") -> CalibBlockProblem:
+    """Seeded stand-in for one block-level calibration step (Sec. 3.3,
+    Appendix B.3) on a pruned sequence of M tokens: a decoder block of
+    hidden size d, MLP width f and H heads.
+
+    * x: the activation recipe (N(0, 1), 8 outlier channels x20);
+    * weights: N(0, 0.02^2) for q|k|v, o, gate|up, down;
+    * gamma1, gamma2: 1 + 0.1 N(0, 1) (RMSNorm weights);
+    * sigma: exp(0.3 N(0, 1)) per input channel of each linear group, times
+      20^0.3 on x's outlier channels for the q|k|v group (whose input keeps
+      the block input's outlier channels through the RMSNorm);
+    * clip_a: 0.9, 0.95, 0.85, 0.9 (q|k|v, o, gate|up, down); clip_w:
+      U(0.75, 1) per output channel.
+    The target (the full-precision block's output) is not drawn: it is the
+    block computed without quantization.  No block arithmetic happens here."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([SEED, 3000, seed])))
+    x32 = g.standard_normal((M, d), dtype=np.float32)
+    ch = g.choice(d, size=min(N_OUTLIER, d), replace=False)
+    x32[:, ch] *= np.float32(OUTLIER_SCALE)
+    shapes = {"qkv": (3 * d, d), "o": (d, d), "gu": (2 * f, d), "down": (d, f)}
+    weights = {k: encode(g.standard_normal(s, dtype=np.float32) * np.float32(WEIGHT_STD), dtype)
+               for k, s in shapes.items()}
+    gam = [encode((1.0 + 0.1 * g.standard_normal(d)).astype(np.float32), dtype) for _ in range(2)]
+    sigma, clip_w = {}, {}
+    for k, (n_out, k_in) in shapes.items():
+        s_ = np.exp(np.float32(0.3) * g.standard_normal(k_in, dtype=np.float32)).astype(np.float32)
+        if k == "qkv":
+            s_[ch] *= np.float32(OUTLIER_SCALE ** 0.3)
+        sigma[k] = s_
+        clip_w[k] = g.uniform(0.75, 1.0, n_out).astype(np.float32)
+    clip_a = {"qkv": 0.9, "o": 0.95, "gu": 0.85, "down": 0.9}
+    return CalibBlockProblem(encode(x32, dtype), weights, gam[0], gam[1], sigma, clip_a, clip_w,
+                             H, dtype)
