@@ -305,6 +305,61 @@ int p4q_calib_linear_grad(p4q_dtype dt, int M, int N, int K,
                           hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Pruning-aware calibration step of a whole decoder block (Sec. 3.3, Eq.
+ * p4q_pruning_aware_calibration: calibration proceeds block by block, each
+ * block's W4A4 fake-quantized output reconstructing the full-precision
+ * block's output on the pruned sequence by mean squared error; Appendix
+ * B.3: diagonal scales and weight / activation clipping factors learned,
+ * keys and values in FP16).
+ *
+ * The block (LLaMA-family decoder, intermediates rounded once to fp16,
+ * nearest even, between operations; H heads of D = d / H):
+ *   n1 = RMSNorm(x) gamma1 (eps);   q|k|v = L_qkv(n1);
+ *   q, k <- RoPE (channel i < D/2 paired with i + D/2, angle p theta_i,
+ *           theta_i = rope_base^(-2i/D), p = the token's position 0..M-1);
+ *   O = softmax(q k^T / sqrt(D), causal) v per head (fp32 arithmetic);
+ *   h = x + L_o(O);  n2 = RMSNorm(h) gamma2;  g|u = L_gu(n2);
+ *   a = SiLU(g) u;   out = h + L_down(a);
+ *   loss = sum (out - target)^2 / (M d),
+ * where every L is the W4A4 fake-quantized linear of p4q_calib_linear_grad
+ * with its group's diagonal scales (dividing the input channels,
+ * multiplying the weights' input channels), activation clipping factor and
+ * per-output-channel weight clipping factors; its output is the W4A4
+ * epilogue's out_rne(fl32(fl32(acc sA) sW)).  Returns the loss and its
+ * gradients with respect to every group's sigma, clip_a and clip_w (rounding
+ * of codes and of intermediates passed straight through, the clamp and the
+ * row maxima as in p4q_calib_linear_grad), chained through the
+ * full-precision attention, RMSNorm and SiLU-gated MLP; each group's
+ * backward contractions take bf16 operands with fp32 accumulation.
+ *
+ * Groups, in this order: q|k|v (N = 3d, input width d), o (d, d), gate|up
+ * (2f, d), down (d, f).
+ * Layouts: x fp16 [M, d] (the block input on the pruned sequence); target
+ *   fp32 [M, ldt] (the full-precision block's output); w_qkv fp16 [3d, d]
+ *   (q, k, v rows), w_o [d, d], w_gu [2f, d] (gate rows, then up rows),
+ *   w_down [d, f]; gamma1, gamma2 fp16 [d];
+ *   sigma fp32 [3d + f] = [qkv: d | o: d | gate|up: d | down: f];
+ *   clip_a: HOST array of 4 floats in (0, 1], one per group;
+ *   clip_w fp32 [5d + 2f] = [qkv: 3d | o: d | gate|up: 2f | down: d];
+ *   outputs loss fp32 [1], grad_sigma [3d + f], grad_clip_a [4] and
+ *   grad_clip_w [5d + 2f] in the same layouts (device).
+ * Workspace: p4q_calib_block_workspace_bytes(M, d, f, H) bytes, 256-byte
+ *   aligned; nothing of it is read before being written.
+ * Limits: dt == P4Q_FP16; 1 <= M <= 4096; d, f multiples of 128, <= 16384;
+ *   d % H == 0 with D = d / H even; M * 2f < 2^31 and 3d * d, 2f * d < 2^31;
+ *   ldt >= d; eps in [0, 1]; rope_base > 1; pointers 16-byte aligned.
+ * ---------------------------------------------------------------------- */
+size_t p4q_calib_block_workspace_bytes(int M, int d, int f, int H);
+
+int p4q_calib_block_grad(p4q_dtype dt, int M, int d, int f, int H, const void *x,
+                         const float *target, int64_t ldt, const void *w_qkv,
+                         const void *w_o, const void *w_gu, const void *w_down,
+                         const void *gamma1, const void *gamma2, float eps, float rope_base,
+                         const float *sigma, const float *clip_a, const float *clip_w,
+                         float *loss, float *grad_sigma, float *grad_clip_a,
+                         float *grad_clip_w, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * W4A4 linear (Appendix B.3: RTN int4 weights and activations for W4A4
  * inference): an integer GEMM on the codes and a dequant epilogue.
  *

@@ -721,10 +721,14 @@ def _rope(z: np.ndarray, cos: np.ndarray, sin: np.ndarray, inverse: bool = False
     return np.concatenate([a * c - b * s, b * c + a * s], axis=2)
 
 
-def _rmsnorm(x: np.ndarray, g: np.ndarray, eps: float):
+def _rmsnorm(x: np.ndarray, g: np.ndarray, eps: float, fp32: bool = False):
     """n = x * gamma / sqrt(mean(x^2) + eps) in real arithmetic; returns (n,
-    r = 1/rms per row)."""
+    r = 1/rms per row).  fp32: r and the two products rounded to fp32."""
     r = 1.0 / np.sqrt(np.mean(x * x, axis=1) + eps)
+    if fp32:
+        r = r.astype(np.float32)
+        n = (x.astype(np.float32) * r[:, None]).astype(np.float32) * g.astype(np.float32)[None, :]
+        return n.astype(np.float64), r.astype(np.float64)
     return x * r[:, None] * g[None, :], r
 
 
@@ -735,18 +739,22 @@ def _rmsnorm_backward(x, g, r, dn):
     return r[:, None] * g[None, :] * dn - x * (r ** 3 * s / d)[:, None]
 
 
-def _attention(q, k, v):
+def _attention(q, k, v, fp32: bool = False):
     """Causal softmax attention per head in real arithmetic: q, k, v [M, H,
-    D] -> (O [M, H, D], P [H, M, M])."""
+    D] -> (O [M, H, D], P [H, M, M]).  fp32: scores, weights and products
+    in fp32."""
     M, H, D = q.shape
     causal = np.tril(np.ones((M, M), dtype=bool))
     P = np.empty((H, M, M), dtype=np.float64)
     O = np.empty((M, H, D), dtype=np.float64)
+    t = np.float32 if fp32 else np.float64
     for hh in range(H):
-        S = np.where(causal, (q[:, hh, :] @ k[:, hh, :].T) / np.sqrt(D), -np.inf)
-        E = np.exp(S - S.max(axis=1, keepdims=True))
-        P[hh] = E / E.sum(axis=1, keepdims=True)
-        O[:, hh, :] = P[hh] @ v[:, hh, :]
+        S = (q[:, hh, :].astype(t) @ k[:, hh, :].T.astype(t)) * t(1.0 / np.sqrt(D))
+        S = np.where(causal, S, -np.inf).astype(t)
+        E = np.exp(S - S.max(axis=1, keepdims=True)).astype(t)
+        Ph = (E / E.sum(axis=1, keepdims=True)).astype(t)
+        P[hh] = Ph
+        O[:, hh, :] = Ph @ v[:, hh, :].astype(t)
     return O, P
 
 
@@ -803,10 +811,12 @@ def _fq_linear_backward(q, G):
     dwp = np.zeros(q["wp"].shape, dtype=np.float64)
     dclip_a = 0.0
     dclip_w = np.zeros(N, dtype=np.float64)
+    q["a_dclip_rows"] = np.zeros(M, dtype=np.float64)
     for m in range(M):
         dxp[m], dc = fq_row_backward(q["xp"][m], q["a_scales"][m], q["clip_a"], q["a_codes"][m],
                                      q["a_absmax"][m], q["a_kstar"][m], gA[m])
         dclip_a += dc
+        q["a_dclip_rows"][m] = dc
     for n in range(N):
         dwp[n], dclip_w[n] = fq_row_backward(q["wp"][n], q["w_scales"][n], q["clip_w"][n],
                                              q["w_codes"][n], q["w_absmax"][n], q["w_kstar"][n],
@@ -820,7 +830,8 @@ def _fq_linear_backward(q, G):
 def calib_block(x: np.ndarray, weights: dict, gamma1: np.ndarray, gamma2: np.ndarray,
                 H: int, target: np.ndarray = None, sigma: dict = None, clip_a: dict = None,
                 clip_w: dict = None, eps: float = 1e-5, rope_base: float = 10000.0,
-                dtype: str = "fp16", quantize: bool = True) -> dict:
+                dtype: str = "fp16", quantize: bool = True, bounds: bool = False,
+                fp32_ops: bool = False) -> dict:
     """One decoder block on one pruned sequence, full precision or W4A4
     fake-quantized, and for the latter the calibration loss and gradients.
 
@@ -846,7 +857,19 @@ def calib_block(x: np.ndarray, weights: dict, gamma1: np.ndarray, gamma2: np.nda
     the full-precision attention, RMSNorm and SiLU-gated MLP.
 
     Returns {"out": out (storage dtype)} and, with quantize and target,
-    "loss", "grad_sigma"[g], "grad_clip_a"[g], "grad_clip_w"[g] (float64)."""
+    "loss", "grad_sigma"[g], "grad_clip_a"[g], "grad_clip_w"[g] (float64) and
+    "state"[g], each group's quantizer state (codes, scales, row maxima and
+    their indices, transformed rows) for inspection.  With bounds, also
+    "mag_grad_sigma"[g], "mag_grad_clip_a"[g] and "mag_grad_clip_w"[g]: for
+    every gradient component the sum of the magnitudes of its terms given
+    the group's upstream gradient (calib_linear's magnitude form), the scale
+    against which a rounded evaluation of the component is measured.
+
+    fp32_ops=True evaluates RMSNorm, attention and the SiLU-gated product
+    with fp32 arithmetic instead of real arithmetic (every rounding of the
+    definition unchanged).  It is a probe of how sensitive each result is to
+    the precision those operations are evaluated in -- some components are
+    ill-conditioned -- and never the reference, which is fp32_ops=False."""
     r16 = lambda v: _r16(v, dtype)
     X = as_f32(x, dtype).astype(np.float64)
     M, d = X.shape
@@ -862,24 +885,28 @@ def calib_block(x: np.ndarray, weights: dict, gamma1: np.ndarray, gamma2: np.nda
                           clip_w[name], dtype)
 
     # ---- forward
-    n1f, r1 = _rmsnorm(X, g1, eps)
+    n1f, r1 = _rmsnorm(X, g1, eps, fp32_ops)
     n1 = r16(n1f)
     qkv, c_qkv = lin("qkv", n1)
     cos, sin = _rope_tables(M, D, rope_base)
     q = r16(_rope(qkv[:, :d].reshape(M, H, D), cos, sin))
     k = r16(_rope(qkv[:, d:2 * d].reshape(M, H, D), cos, sin))
     v = qkv[:, 2 * d:].reshape(M, H, D)
-    O, P = _attention(q, k, v)
+    O, P = _attention(q, k, v, fp32_ops)
     O = r16(O).reshape(M, d)
     o, c_o = lin("o", O)
     h = r16(X + o)
-    n2f, r2 = _rmsnorm(h, g2, eps)
+    n2f, r2 = _rmsnorm(h, g2, eps, fp32_ops)
     n2 = r16(n2f)
     gu, c_gu = lin("gu", n2)
     f = gu.shape[1] // 2
     gg, uu = gu[:, :f], gu[:, f:]
     sig_g = 1.0 / (1.0 + np.exp(-gg))
-    a = r16(gg * sig_g * uu)
+    if fp32_ops:
+        g32 = gg.astype(np.float32)
+        a = r16(((g32 / (np.float32(1) + np.exp(-g32))) * uu.astype(np.float32)).astype(np.float64))
+    else:
+        a = r16(gg * sig_g * uu)
     y, c_down = lin("down", a)
     out = r16(h + y)
     res = {"out": _store16(out, dtype)}
@@ -893,9 +920,18 @@ def calib_block(x: np.ndarray, weights: dict, gamma1: np.ndarray, gamma2: np.nda
     dout = 2.0 * R / (M * d)
     grads = {}
 
+    mags = {}
+
     def back(name, cache, G):
         dX, ds, dca, dcw = _fq_linear_backward(cache, G)
         grads[name] = (ds, dca, dcw)
+        if bounds:
+            # the sums of magnitudes of each component's terms, given this
+            # group's upstream gradient (the backward pass in magnitude form)
+            aG = np.abs(G)
+            mags[name] = _calib_backward(aG * cache["w_scales"].astype(np.float64)[None, :],
+                                         aG * cache["a_scales"].astype(np.float64)[:, None],
+                                         1.0, cache, absolute=True)
         return dX
 
     da = back("down", c_down, dout)
@@ -908,6 +944,11 @@ def calib_block(x: np.ndarray, weights: dict, gamma1: np.ndarray, gamma2: np.nda
     dk = _rope(dk, cos, sin, inverse=True)
     back("qkv", c_qkv, np.concatenate([dq.reshape(M, d), dk.reshape(M, d), dv.reshape(M, d)],
                                       axis=1))
+    res["state"] = {"qkv": c_qkv, "o": c_o, "gu": c_gu, "down": c_down}
+    if bounds:
+        res["mag_grad_sigma"] = {g: mags[g][0] for g in BLOCK_GROUPS}
+        res["mag_grad_clip_a"] = {g: mags[g][1] for g in BLOCK_GROUPS}
+        res["mag_grad_clip_w"] = {g: mags[g][2] for g in BLOCK_GROUPS}
     res["grad_sigma"] = {g: grads[g][0] for g in BLOCK_GROUPS}
     res["grad_clip_a"] = {g: grads[g][1] for g in BLOCK_GROUPS}
     res["grad_clip_w"] = {g: grads[g][2] for g in BLOCK_GROUPS}

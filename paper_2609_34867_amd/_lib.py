@@ -47,6 +47,11 @@ SIGNATURES = {
     "p4q_calib_linear_grad": (_c_int, [_c_int, _c_int, _c_int, _c_int, _vp, _c_i64, _vp, _c_i64,
                                        _vp, _c_i64, _vp, _c_float, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _c_size, _vp]),
+    "p4q_calib_block_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
+    "p4q_calib_block_grad": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_i64,
+                                      _vp, _vp, _vp, _vp, _vp, _vp, _c_float, _c_float, _vp,
+                                      ctypes.POINTER(_c_float), _vp, _vp, _vp, _vp, _vp, _vp,
+                                      _c_size, _vp]),
     "p4q_w4a4_linear_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int]),
     "p4q_w4a4_linear": (_c_int, [_c_int, _c_int, _c_int, _vp, _vp, _vp, _vp, _c_int, _vp,
                                  _c_i64, _vp, _vp, _c_size, _vp]),

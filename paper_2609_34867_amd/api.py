@@ -376,6 +376,68 @@ def calib_linear_grad(x: torch.Tensor, w: torch.Tensor, target: torch.Tensor,
     return loss, gs, gca, gcw
 
 
+def calib_block_workspace(M: int, d: int, f: int, H: int, device) -> torch.Tensor:
+    n = lib().p4q_calib_block_workspace_bytes(M, d, f, H)
+    if n == 0:
+        raise P4QError(P4Q_ERR_INVALID_ARG, f"unsupported block shape M={M} d={d} f={f} H={H}")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def calib_block_grad(x: torch.Tensor, target: torch.Tensor, w_qkv: torch.Tensor,
+                     w_o: torch.Tensor, w_gu: torch.Tensor, w_down: torch.Tensor,
+                     gamma1: torch.Tensor, gamma2: torch.Tensor, H: int, sigma: torch.Tensor,
+                     clip_a, clip_w: torch.Tensor, eps: float = 1e-5, rope_base: float = 10000.0,
+                     workspace: Optional[torch.Tensor] = None, out=None):
+    """One calibration step of a W4A4 fake-quantized decoder block
+    (p4q_calib_block_grad): x fp16 [M, d], target fp32 [M, d], weights fp16
+    (q|k|v [3d, d], o [d, d], gate|up [2f, d], down [d, f]), RMSNorm weights
+    fp16 [d]; sigma fp32 [3d + f] (groups q|k|v, o, gate|up, down), clip_a
+    four floats (host), clip_w fp32 [5d + 2f].  Returns (loss [1],
+    grad_sigma [3d + f], grad_clip_a [4], grad_clip_w [5d + 2f]) as fp32
+    device tensors; `out` may hold those four to be written in place."""
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [M, d]")
+    M, d = x.shape
+    if w_down.dim() != 2 or w_down.shape[0] != d:
+        raise ValueError("w_down must be [d, f]")
+    f = w_down.shape[1]
+    for t, shape, name in ((x, (M, d), "x"), (w_qkv, (3 * d, d), "w_qkv"), (w_o, (d, d), "w_o"),
+                           (w_gu, (2 * f, d), "w_gu"), (w_down, (d, f), "w_down"),
+                           (gamma1, (d,), "gamma1"), (gamma2, (d,), "gamma2")):
+        _check(t, name, shape, torch.float16)
+    _check(target, "target", (M, d), torch.float32)
+    _check(sigma, "sigma", (3 * d + f,), torch.float32)
+    _check(clip_w, "clip_w", (5 * d + 2 * f,), torch.float32)
+    ca = [float(c) for c in clip_a]
+    if len(ca) != 4:
+        raise ValueError("clip_a must hold four factors (q|k|v, o, gate|up, down)")
+    if out is not None:
+        if len(out) != 4:
+            raise ValueError("out must hold (loss, grad_sigma, grad_clip_a, grad_clip_w)")
+        for t, n, name in zip(out, (1, 3 * d + f, 4, 5 * d + 2 * f),
+                              ("loss", "grad_sigma", "grad_clip_a", "grad_clip_w")):
+            _check(t, name, (n,), torch.float32)
+    _check(workspace, "workspace", None, torch.uint8)
+    _need_gpu(x, target, w_qkv, w_o, w_gu, w_down, gamma1, gamma2, sigma, clip_w, workspace,
+              *(out or ()))
+    dev = x.device
+    if out is None:
+        out = tuple(torch.empty(n, dtype=torch.float32, device=dev)
+                    for n in (1, 3 * d + f, 4, 5 * d + 2 * f))
+    if workspace is None:
+        workspace = calib_block_workspace(M, d, f, H, dev)
+    loss, gs, gca, gcw = out
+    ca_arr = (ctypes.c_float * 4)(*ca)
+    st = lib().p4q_calib_block_grad(P4Q_FP16, M, d, f, H, _ptr(x), _ptr(target), target.stride(0),
+                                    _ptr(w_qkv), _ptr(w_o), _ptr(w_gu), _ptr(w_down),
+                                    _ptr(gamma1), _ptr(gamma2), ctypes.c_float(eps),
+                                    ctypes.c_float(rope_base), _ptr(sigma), ca_arr, _ptr(clip_w),
+                                    _ptr(loss), _ptr(gs), _ptr(gca), _ptr(gcw), _ptr(workspace),
+                                    workspace.numel(), _stream(dev))
+    check(st)
+    return loss, gs, gca, gcw
+
+
 # --------------------------------------------------------------------------- W4A4 linear
 def w4a4_linear_workspace(M: int, N_out: int, K_in: int, device) -> Optional[torch.Tensor]:
     n = lib().p4q_w4a4_linear_workspace_bytes(M, N_out, K_in)

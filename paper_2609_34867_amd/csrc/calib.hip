@@ -408,7 +408,9 @@ __global__ __launch_bounds__(kThreads) void k_calib_residual(
 //    16 rows one fragment read touches hit distinct banks.
 //    grid (Kd / 128, ceil(I / 128), splits); split z covers j in
 //    [z js, min(J, (z + 1) js)).  Outputs: rowpart[(kt splits + z) I + i],
-//    colpart[(it splits + z) Kd + k].
+//    colpart[(it splits + z) Kd + k], and when gpart is given the values
+//    inside ? g : 0 themselves at gpart[(z I + i) Kd + k] (the direct part of
+//    the gradient with respect to the transformed input, per split).
 // ---------------------------------------------------------------------------
 constexpr int BB = 128;
 constexpr int BJ = 64;
@@ -456,7 +458,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
     const float *__restrict__ zprime, const uint8_t *__restrict__ codes,
     const uint8_t *__restrict__ inside, const float *__restrict__ sigma,
     const float *__restrict__ srow, int Kd, float *__restrict__ rowpart,
-    float *__restrict__ colpart) {
+    float *__restrict__ colpart, float *__restrict__ gpart) {
     __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * kStage];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int wi = wave >> 1, wk = wave & 1;
@@ -634,6 +636,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
                 const uint32_t cw = *reinterpret_cast<const uint16_t *>(
                     smem + kOffC + il * kCStride + kb / 2);
                 const uint32_t bw = (uint32_t)smem[kOffB + il * kBStride + kb / 8] >> ish;
+                float gi[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float g = acc[x][y][4 * rg + e] * gm[y];
@@ -643,7 +646,11 @@ __global__ __launch_bounds__(kThreads, 2) void k_calib_bwd(
                     rowv[y] = __builtin_fmaf(g, in ? -f : q, rowv[y]);
                     colv[16 * x + 4 * rg + e] = __builtin_fmaf(in ? g : 0.0f, zp[e],
                                                                colv[16 * x + 4 * rg + e]);
+                    gi[e] = in ? g : 0.0f;
                 }
+                if (gpart != nullptr && i0 + il < I)
+                    *reinterpret_cast<float4 *>(gpart + ((int64_t)split * I + i0 + il) * Kd + k0 + kb) =
+                        make_float4(gi[0], gi[1], gi[2], gi[3]);
             }
         }
     }
@@ -903,11 +910,11 @@ hipError_t calib_typed(int M, int N, int K, const void *x, int64_t ldx, const vo
     hipLaunchKernelGGL((k_calib_bwd<BF16, true>), dim3(K / BB, p.tilesMA, p.nsA),
                        dim3(kThreads), 0, stream, c.P1, (int64_t)N, c.CwT, (int64_t)N, M, N,
                        p.jsA, static_cast<const uint16_t *>(x), ldx, c.xprime, c.codesA, c.insA,
-                       sigma, c.sA, K, c.rowA, c.colA);
+                       sigma, c.sA, K, c.rowA, c.colA, nullptr);
     hipLaunchKernelGGL((k_calib_bwd<BF16, false>), dim3(K / BB, p.tilesNW, p.nsW),
                        dim3(kThreads), 0, stream, c.P2T, (int64_t)p.Mp, c.CaT, (int64_t)p.Mp, N,
                        p.Mp, p.jsW, static_cast<const uint16_t *>(w), ldw, c.xprime, c.codesW,
-                       c.insW, sigma, c.sW, K, c.rowW, c.colW);
+                       c.insW, sigma, c.sW, K, c.rowW, c.colW, nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // 6-7. finish
     const double scale = 2.0 / ((double)M * (double)N);
@@ -921,6 +928,568 @@ hipError_t calib_typed(int M, int N, int K, const void *x, int64_t ldx, const vo
                        c.corr + K, sigma, K, scale, grad_sigma, c.loss_part, p.nloss,
                        1.0 / ((double)M * (double)N), loss, c.dclipa_part, p.nbA, grad_clip_a);
     return hipGetLastError();
+}
+
+
+// ===========================================================================
+// Block-level calibration: one decoder block on a pruned sequence (Sec. 3.3,
+// Eq. p4q_pruning_aware_calibration; Appendix B.3).  The four linear groups
+// (q|k|v, o, gate|up, down) run as above (transformed quantizers, int8 MFMA
+// forward, bf16 backward contractions with fused reductions); between them
+// the block's full-precision operations run in fp32 on 16-bit intermediates:
+//   n1 = RMSNorm(x) g1; q|k|v = L(n1); RoPE(q), RoPE(k); O = attention;
+//   h = x + L(O); n2 = RMSNorm(h) g2; g|u = L(n2); a = SiLU(g) u;
+//   out = h + L(a); loss = ||out - T||^2 / (M d)
+// and the backward pass chains the groups' input gradients through them.
+// Every intermediate is rounded once to fp16 (nearest even) as the FP16
+// model holds it; rounding passes gradients straight through.
+// ===========================================================================
+__device__ __forceinline__ float f16v(uint16_t h) { return half_to_f32<false>(h); }
+__device__ __forceinline__ uint16_t to_f16(float v) {
+    return __builtin_bit_cast(uint16_t, (_Float16)v);
+}
+
+// sum over the 256 threads of a block (fp32 partials summed in double)
+__device__ __forceinline__ double block_sum_f(double v, double *red) {
+    const double s = block_sum(v, red);
+    __syncthreads();
+    return s;
+}
+
+// RMSNorm of row m: out = fp16(x r gamma), r = 1 / sqrt(mean(x^2) + eps)
+__global__ __launch_bounds__(kThreads) void k_blk_rmsnorm(const uint16_t *__restrict__ x, int d,
+                                                         const uint16_t *__restrict__ gamma,
+                                                         float eps, uint16_t *__restrict__ out,
+                                                         float *__restrict__ rinv) {
+    __shared__ double red[kThreads / 64];
+    const int m = blockIdx.x, t = threadIdx.x;
+    const uint16_t *xr = x + (int64_t)m * d;
+    double ss = 0.0;
+    for (int k = t; k < d; k += kThreads) {
+        const float v = f16v(xr[k]);
+        ss += (double)v * v;
+    }
+    ss = block_sum_f(ss, red);
+    const float r = (float)(1.0 / sqrt(ss / d + (double)eps));
+    if (t == 0) rinv[m] = r;
+    for (int k = t; k < d; k += kThreads)
+        out[(int64_t)m * d + k] = to_f16(__fmul_rn(__fmul_rn(f16v(xr[k]), r), f16v(gamma[k])));
+}
+
+// dL/dx of n = x r gamma plus the residual path's gradient dres:
+//   dx = dres + r gamma dn - x r^3 / d sum_j x_j gamma_j dn_j
+__global__ __launch_bounds__(kThreads) void k_blk_rmsnorm_bwd(
+    const uint16_t *__restrict__ x, const uint16_t *__restrict__ gamma,
+    const float *__restrict__ rinv, const float *__restrict__ dn, const float *__restrict__ dres,
+    int d, float *__restrict__ dx) {
+    __shared__ double red[kThreads / 64];
+    const int m = blockIdx.x, t = threadIdx.x;
+    const int64_t o = (int64_t)m * d;
+    double s = 0.0;
+    for (int k = t; k < d; k += kThreads) s += (double)f16v(x[o + k]) * f16v(gamma[k]) * dn[o + k];
+    s = block_sum_f(s, red);
+    const double r = rinv[m];
+    const float c = (float)(r * r * r * s / d);
+    for (int k = t; k < d; k += kThreads)
+        dx[o + k] = dres[o + k] + (float)r * f16v(gamma[k]) * dn[o + k] - f16v(x[o + k]) * c;
+}
+
+// Rotary embedding of q and k (columns [0, 2 d) of the fused q|k|v rows):
+// channel i < D/2 of a head pairs with i + D/2, angle p theta_i, theta_i =
+// base^(-2i/D), p the token position; angles and their cosines in double.
+// forward: in place on the fp16 values; backward (BWD): the transposed
+// rotation in place on the fp32 gradients.
+template <bool BWD, typename T>
+__global__ __launch_bounds__(kThreads) void k_blk_rope(T *__restrict__ z, int64_t ld, int M,
+                                                      int H, int D, double base) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int half = D / 2;
+    const int64_t total = (int64_t)M * 2 * H * half;
+    if (idx >= total) return;
+    const int i = (int)(idx % half);
+    const int hh = (int)((idx / half) % (2 * H));           // q heads, then k heads
+    const int m = (int)(idx / ((int64_t)half * 2 * H));
+    const double ang = (double)m * pow(base, -2.0 * i / D);
+    const float c = (float)cos(ang), s = (float)sin(ang);
+    T *row = z + (int64_t)m * ld + (int64_t)hh * D;
+    if constexpr (BWD) {
+        const float a = row[i], b = row[i + half];
+        row[i] = a * c + b * s;
+        row[i + half] = b * c - a * s;
+    } else {
+        const float a = f16v(row[i]), b = f16v(row[i + half]);
+        row[i] = to_f16(__fmul_rn(a, c) - __fmul_rn(b, s));
+        row[i + half] = to_f16(__fmul_rn(b, c) + __fmul_rn(a, s));
+    }
+}
+
+template <typename T> __device__ __forceinline__ float ldv(const T *p, int64_t i);
+template <> __device__ __forceinline__ float ldv<float>(const float *p, int64_t i) { return p[i]; }
+template <> __device__ __forceinline__ float ldv<uint16_t>(const uint16_t *p, int64_t i) {
+    return f16v(p[i]);
+}
+
+// Batched strided GEMM with fp32 accumulation (the attention products of
+// one block): C[b](i, j) = alpha sum_k A[b](i, k) B[b](k, j); A element
+// (i, k) at A + b sAb + i sAi + k sAk, B (k, j) at B + b sBb + k sBk + j sBj,
+// C (i, j) at C + b sCb + i sCi + j.  64 x 64 tiles, 16 k per stage, 256
+// threads with 4 x 4 outputs each.  band: 0 all k; 1 only k <= i (A is
+// lower triangular: P or dS); 2 only k >= i (A is upper triangular: P^T or
+// dS^T); 3 full k, tiles strictly above the diagonal (j > i everywhere)
+// skipped (their entries are never read).
+constexpr int GB = 64, GK = 16;
+template <typename TA, typename TB, bool C16>
+__global__ __launch_bounds__(kThreads) void k_blk_bgemm(
+    const TA *__restrict__ A, int64_t sAb, int64_t sAi, int64_t sAk, const TB *__restrict__ B,
+    int64_t sBb, int64_t sBk, int64_t sBj, void *__restrict__ Cv, int64_t sCb, int64_t sCi, int I,
+    int J, int K, float alpha, int band) {
+    __shared__ float As[GK][GB + 1];
+    __shared__ float Bs[GK][GB + 1];
+    const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+    const int i0 = blockIdx.y * GB, j0 = blockIdx.x * GB, b = blockIdx.z;
+    if (band == 3 && j0 > i0 + GB - 1) return;
+    A += b * sAb;
+    B += b * sBb;
+    int kbeg = 0, kend = K;
+    if (band == 1) kend = min(K, i0 + GB);
+    if (band == 2) kbeg = i0;
+    float acc[4][4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[r][c] = 0.0f;
+    const bool a_kfast = (sAk == 1), b_jfast = (sBj == 1);
+    for (int k0 = kbeg; k0 < kend; k0 += GK) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = t + kThreads * q;
+            const int kk = a_kfast ? (e & 15) : (e >> 6), ii = a_kfast ? (e >> 4) : (e & 63);
+            const int i = i0 + ii, k = k0 + kk;
+            As[kk][ii] = (i < I && k < kend) ? ldv<TA>(A, (int64_t)i * sAi + (int64_t)k * sAk) : 0.0f;
+            const int kb = b_jfast ? (e >> 6) : (e & 15), jj = b_jfast ? (e & 63) : (e >> 4);
+            const int j = j0 + jj, kq = k0 + kb;
+            Bs[kb][jj] = (j < J && kq < kend) ? ldv<TB>(B, (int64_t)kq * sBk + (int64_t)j * sBj) : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < GK; ++kk) {
+            float a[4], bv[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) a[r] = As[kk][ty + 16 * r];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) bv[c] = Bs[kk][tx + 16 * c];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) acc[r][c] = __builtin_fmaf(a[r], bv[c], acc[r][c]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = i0 + ty + 16 * r;
+        if (i >= I) continue;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int j = j0 + tx + 16 * c;
+            if (j >= J) continue;
+            const int64_t o = b * sCb + (int64_t)i * sCi + j;
+            if constexpr (C16) static_cast<uint16_t *>(Cv)[o] = to_f16(alpha * acc[r][c]);
+            else static_cast<float *>(Cv)[o] = alpha * acc[r][c];
+        }
+    }
+}
+
+// Causal softmax of every row of S [H][M][M] (already scaled) in place: P
+// over j <= i, zeros beyond.  One wavefront per row.
+__global__ __launch_bounds__(kThreads) void k_blk_softmax(float *__restrict__ S, int M, int rows) {
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    const int i = row % M;
+    float *p = S + (int64_t)row * M;
+    float mx = -INFINITY;
+    for (int j = lane; j <= i; j += 64) mx = fmaxf(mx, p[j]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    double sum = 0.0;
+    for (int j = lane; j <= i; j += 64) sum += (double)expf(p[j] - mx);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+    const float inv = (float)(1.0 / sum);
+    for (int j = lane; j < M; j += 64) p[j] = (j <= i) ? expf(p[j] - mx) * inv : 0.0f;
+}
+
+// dS = P (dP - sum_l P dP) over j <= i, zeros beyond; dP [H][M][M] in place
+__global__ __launch_bounds__(kThreads) void k_blk_softmax_bwd(const float *__restrict__ P,
+                                                             float *__restrict__ dP, int M,
+                                                             int rows) {
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    const int i = row % M;
+    const float *p = P + (int64_t)row * M;
+    float *g = dP + (int64_t)row * M;
+    double s = 0.0;
+    for (int j = lane; j <= i; j += 64) s += (double)p[j] * g[j];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    const float sf = (float)s;
+    for (int j = lane; j < M; j += 64) g[j] = (j <= i) ? p[j] * (g[j] - sf) : 0.0f;
+}
+
+// out = fp16(a + b), elementwise
+__global__ __launch_bounds__(kThreads) void k_blk_add16(const uint16_t *__restrict__ a,
+                                                       const uint16_t *__restrict__ b,
+                                                       uint16_t *__restrict__ out, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) out[i] = to_f16(f16v(a[i]) + f16v(b[i]));
+}
+
+// a = fp16(SiLU(g) u) from the fused gate|up rows [M][2f]
+__global__ __launch_bounds__(kThreads) void k_blk_silu_mul(const uint16_t *__restrict__ gu, int M,
+                                                          int f, uint16_t *__restrict__ a) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= (int64_t)M * f) return;
+    const int64_t m = idx / f, k = idx % f;
+    const float g = f16v(gu[m * 2 * f + k]), u = f16v(gu[m * 2 * f + f + k]);
+    a[idx] = to_f16(__fmul_rn(g / (1.0f + expf(-g)), u));
+}
+
+// (dg, du) of a = g sig(g) u: dg = da u sig (1 + g (1 - sig)), du = da g sig
+__global__ __launch_bounds__(kThreads) void k_blk_silu_mul_bwd(const float *__restrict__ da,
+                                                              const uint16_t *__restrict__ gu,
+                                                              int M, int f,
+                                                              float *__restrict__ dgu) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= (int64_t)M * f) return;
+    const int64_t m = idx / f, k = idx % f;
+    const float g = f16v(gu[m * 2 * f + k]), u = f16v(gu[m * 2 * f + f + k]);
+    const float sg = 1.0f / (1.0f + expf(-g));
+    const float d = da[idx];
+    dgu[m * 2 * f + k] = d * u * sg * (1.0f + g * (1.0f - sg));
+    dgu[m * 2 * f + f + k] = d * g * sg;
+}
+
+// block output out = fp16(h + y), residual against the fp32 target, the
+// upstream gradient 2 (out - T) / (M d) and per-block partial sums of the
+// squared residual
+__global__ __launch_bounds__(kThreads) void k_blk_out(const uint16_t *__restrict__ h,
+                                                     const uint16_t *__restrict__ y,
+                                                     const float *__restrict__ T, int64_t ldt,
+                                                     int M, int d, float g_scale,
+                                                     float *__restrict__ dout,
+                                                     double *__restrict__ loss_part) {
+    __shared__ double red[kThreads / 64];
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    double l2 = 0.0;
+    if (idx < (int64_t)M * d) {
+        const int64_t m = idx / d, k = idx % d;
+        const float out = f16v(to_f16(f16v(h[idx]) + f16v(y[idx])));
+        const float r = out - T[m * ldt + k];
+        l2 = (double)r * r;
+        dout[idx] = r * g_scale;
+    }
+    const double s = block_sum(l2, red);
+    if (threadIdx.x == 0) loss_part[blockIdx.x] = s;
+}
+
+// The bf16 contraction operands of a linear group's backward pass from its
+// upstream gradient G [M][N] (fp32): P1 = bf16(G sW[n]) [M][N], P2^T =
+// bf16(G sA[m]) [N][Mp] (rows m >= M zero).  64 x 64 tiles, grid (N / 64,
+// Mp / 64); the grid also clears the float64 scatter targets.
+__global__ __launch_bounds__(kThreads) void k_blk_upstream(
+    const float *__restrict__ G, int64_t ldg, const float *__restrict__ sa,
+    const float *__restrict__ sw, int M, int N, int Mp, uint16_t *__restrict__ P1,
+    uint16_t *__restrict__ P2T, double *__restrict__ corr, int ncorr) {
+    __shared__ __attribute__((aligned(16))) uint16_t tr[64 * 72];
+    const int t = threadIdx.x;
+    const int n0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
+    const int bid = blockIdx.y * gridDim.x + blockIdx.x;
+    const int nb = gridDim.x * gridDim.y;
+    for (int i = bid * kThreads + t; i < ncorr; i += nb * kThreads) corr[i] = 0.0;
+    const int cn = 4 * (t & 15);
+    const float4 swv = *reinterpret_cast<const float4 *>(sw + n0 + cn);
+    const float swa[4] = {swv.x, swv.y, swv.z, swv.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int ml = (t >> 4) + 16 * i, m = m0 + ml;
+        if (m < M) {
+            const float4 gv = *reinterpret_cast<const float4 *>(G + (int64_t)m * ldg + n0 + cn);
+            const float ga[4] = {gv.x, gv.y, gv.z, gv.w};
+            const float s = sa[m];
+            uint32_t p[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                p[e] = bf16_rne(__fmul_rn(ga[e], swa[e]));
+                tr[(cn + e) * 72 + ml] = (uint16_t)bf16_rne(__fmul_rn(ga[e], s));
+            }
+            *reinterpret_cast<uint2 *>(P1 + (int64_t)m * N + n0 + cn) =
+                make_uint2(p[0] | (p[1] << 16), p[2] | (p[3] << 16));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) tr[(cn + e) * 72 + ml] = 0;
+        }
+    }
+    __syncthreads();
+    const int nl = t >> 2, c = t & 3;
+    const uint4 *sp = reinterpret_cast<const uint4 *>(tr + nl * 72 + 16 * c);
+    uint4 *dp = reinterpret_cast<uint4 *>(P2T + (int64_t)(n0 + nl) * Mp + m0 + 16 * c);
+    dp[0] = sp[0];
+    dp[1] = sp[1];
+}
+
+// The gradient with respect to a linear group's input X (X' = X / sigma):
+//   dX[m][k] = (sum_z gpart[z][m][k] + [k = kstar_m] g_s[m] clip / 7
+//               sign(X'[m][k])) / sigma_k,
+// g_s[m] = the row's slot sums (its share through the scale).  One block
+// per row.
+__global__ __launch_bounds__(kThreads) void k_blk_input_grad(
+    const float *__restrict__ gpart, int ns, const float *__restrict__ rowpart, int nslots,
+    const float *__restrict__ xprime, const int32_t *__restrict__ kstar,
+    const float *__restrict__ scales, float clip, const float *__restrict__ sigma, int M, int K,
+    float *__restrict__ dX) {
+    __shared__ double red[kThreads / 64];
+    const int m = blockIdx.x, t = threadIdx.x;
+    double gs = 0.0;
+    for (int s = t; s < nslots; s += kThreads) gs += (double)rowpart[(int64_t)s * M + m];
+    gs = block_sum_f(gs, red);
+    const int ks = kstar[m];
+    const bool live = scales[m] != 0.0f;
+    for (int k = t; k < K; k += kThreads) {
+        double v = 0.0;
+        for (int z = 0; z < ns; ++z) v += (double)gpart[((int64_t)z * M + m) * K + k];
+        if (live && k == ks) {
+            const float xp = xprime[(int64_t)m * K + k];
+            v += gs * (double)clip / 7.0 * (xp > 0.0f ? 1.0 : (xp < 0.0f ? -1.0 : 0.0));
+        }
+        dX[(int64_t)m * K + k] = (float)(v / (double)sigma[k]);
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// Block-level calibration, host side
+// ---------------------------------------------------------------------------
+enum { kGQkv = 0, kGO = 1, kGGu = 2, kGDown = 3 };
+
+struct BlockGroup {
+    int N, K;
+    bool dx;                // the chain needs the gradient with respect to its input
+    CalibPlan p;
+    CalibWs c;
+    float *gpart;
+};
+
+struct BlockWs {
+    BlockGroup g[4];
+    uint16_t *n1, *qkv, *O, *o_out, *h, *n2, *gu, *a, *y;
+    float *r1, *r2, *P, *dP, *dout, *da, *dgu, *dn2, *dh, *dO, *dqkv, *dummy;
+    double *loss_part;
+    int nloss;
+};
+
+void block_groups(int d, int f, BlockGroup *g) {
+    const int N[4] = {3 * d, d, 2 * f, d}, K[4] = {d, d, d, f};
+    for (int i = 0; i < 4; ++i) {
+        g[i].N = N[i];
+        g[i].K = K[i];
+        g[i].dx = (i != kGQkv);
+    }
+}
+
+size_t block_carve(int M, int d, int f, int H, uint8_t *base, BlockWs *w) {
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        uint8_t *q = base ? base + off : nullptr;
+        off += up256(bytes);
+        return q;
+    };
+    BlockWs b;
+    block_groups(d, f, b.g);
+    for (int i = 0; i < 4; ++i) {
+        BlockGroup &g = b.g[i];
+        g.p = calib_plan(M, g.N, g.K);
+        const size_t cb = calib_carve(g.p, M, g.N, g.K, nullptr, nullptr);
+        uint8_t *cbase = take(cb);
+        calib_carve(g.p, M, g.N, g.K, cbase, &g.c);
+        g.gpart = g.dx ? reinterpret_cast<float *>(take((size_t)g.p.nsA * M * g.K * 4)) : nullptr;
+    }
+    const size_t Md = (size_t)M * d, Mf = (size_t)M * f, HMM = (size_t)H * M * M;
+    auto h16 = [&](size_t n) { return reinterpret_cast<uint16_t *>(take(n * 2)); };
+    auto f32 = [&](size_t n) { return reinterpret_cast<float *>(take(n * 4)); };
+    b.n1 = h16(Md); b.qkv = h16(3 * Md); b.O = h16(Md); b.o_out = h16(Md); b.h = h16(Md);
+    b.n2 = h16(Md); b.gu = h16(2 * Mf); b.a = h16(Mf); b.y = h16(Md);
+    b.r1 = f32(M); b.r2 = f32(M); b.P = f32(HMM); b.dP = f32(HMM); b.dout = f32(Md);
+    b.da = f32(Mf); b.dgu = f32(2 * Mf); b.dn2 = f32(Md); b.dh = f32(Md); b.dO = f32(Md);
+    b.dqkv = f32(3 * Md); b.dummy = f32(64);
+    b.nloss = (int)((Md + kThreads - 1) / kThreads);
+    b.loss_part = reinterpret_cast<double *>(take((size_t)b.nloss * 8));
+    if (w) *w = b;
+    return off;
+}
+
+// forward of one fake-quantized group: quantizers, transposed codes, the
+// W4A4 GEMM into y (fp16, row stride ldy)
+hipError_t group_forward(BlockGroup &g, int M, const uint16_t *X, const void *W,
+                         const float *sigma, float clip_a, const float *clip_w, uint16_t *y,
+                         int64_t ldy, hipStream_t stream) {
+    CalibWs &c = g.c;
+    const int N = g.N, K = g.K;
+    hipError_t e;
+    if ((e = launch_qs_typed<false, true>(M, K, X, K, sigma, clip_a, nullptr, c.codesA, c.sA, c.aA,
+                                          c.kA, stream, c.xprime, c.insA)) != hipSuccess)
+        return e;
+    if ((e = launch_qs_typed<false, false>(N, K, W, K, sigma, 1.0f, clip_w, c.codesW, c.sW, c.aW,
+                                           c.kW, stream, nullptr, c.insW)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_codes_bf16t, dim3(g.p.Mp / 64, K / 128), dim3(kThreads), 0, stream,
+                       c.codesA, M, K / 2, c.CaT, (int64_t)g.p.Mp);
+    if (N >= 2048)
+        hipLaunchKernelGGL(k_codes_bf16t_wide, dim3((N + kTWide - 1) / kTWide, K / 128),
+                           dim3(kThreads), 0, stream, c.codesW, N, K / 2, c.CwT, (int64_t)N);
+    else
+        hipLaunchKernelGGL(k_codes_bf16t, dim3(N / 64, K / 128), dim3(kThreads), 0, stream,
+                           c.codesW, N, K / 2, c.CwT, (int64_t)N);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return launch_w4a4_gemm(M, N, K, c.codesA, c.sA, c.codesW, c.sW, P4Q_FP16, y, ldy, nullptr,
+                            nullptr, 0, stream);
+}
+
+// backward of one group from its upstream gradient G [M][N] (fp32, row
+// stride ldg): sigma / clip gradients into the given slices and, when the
+// group has one, the gradient with respect to its input into dX [M][K]
+hipError_t group_backward(BlockGroup &g, int M, const float *G, int64_t ldg, const uint16_t *X,
+                          const void *W, const float *sigma, float clip_a, const float *clip_w,
+                          float *grad_sigma, float *grad_clip_a, float *grad_clip_w, float *dX,
+                          const double *loss_part, int nloss, double inv_md, float *loss,
+                          hipStream_t stream) {
+    CalibWs &c = g.c;
+    const CalibPlan &p = g.p;
+    const int N = g.N, K = g.K;
+    hipLaunchKernelGGL(k_blk_upstream, dim3(N / 64, p.Mp / 64), dim3(kThreads), 0, stream, G, ldg,
+                       c.sA, c.sW, M, N, p.Mp, c.P1, c.P2T, c.corr, 2 * K);
+    hipLaunchKernelGGL((k_calib_bwd<false, true>), dim3(K / BB, p.tilesMA, p.nsA),
+                       dim3(kThreads), 0, stream, c.P1, (int64_t)N, c.CwT, (int64_t)N, M, N, p.jsA,
+                       X, (int64_t)K, c.xprime, c.codesA, c.insA, sigma, c.sA, K, c.rowA, c.colA,
+                       dX ? g.gpart : nullptr);
+    hipLaunchKernelGGL((k_calib_bwd<false, false>), dim3(K / BB, p.tilesNW, p.nsW),
+                       dim3(kThreads), 0, stream, c.P2T, (int64_t)p.Mp, c.CaT, (int64_t)p.Mp, N,
+                       p.Mp, p.jsW, static_cast<const uint16_t *>(W), (int64_t)K, c.xprime,
+                       c.codesW, c.insW, sigma, c.sW, K, c.rowW, c.colW, nullptr);
+    const int nbW = (N + kRowsW - 1) / kRowsW;
+    hipLaunchKernelGGL(k_calib_rows, dim3(p.nbA + nbW), dim3(kThreads), 0, stream, c.rowA,
+                       (K / BB) * p.nsA, M, c.sA, c.aA, c.kA, clip_a, c.rowW, (K / BB) * p.nsW, N,
+                       c.sW, c.aW, c.kW, clip_w, p.nbA, 1.0, c.corr, c.corr + K, c.dclipa_part,
+                       grad_clip_w);
+    hipLaunchKernelGGL(k_calib_cols, dim3(K / kRowsW), dim3(kThreads), 0, stream, c.colA,
+                       p.tilesMA * p.nsA, c.colW, p.tilesNW * p.nsW, c.corr, c.corr + K, sigma, K,
+                       1.0, grad_sigma, loss_part, nloss, inv_md, loss, c.dclipa_part, p.nbA,
+                       grad_clip_a);
+    if (dX)
+        hipLaunchKernelGGL(k_blk_input_grad, dim3(M), dim3(kThreads), 0, stream, g.gpart, p.nsA,
+                           c.rowA, (K / BB) * p.nsA, c.xprime, c.kA, c.sA, clip_a, sigma, M, K,
+                           dX);
+    return hipGetLastError();
+}
+
+// C[b] = alpha A[b] B[b] over a grid of 64 x 64 tiles (see k_blk_bgemm)
+template <typename TA, typename TB, bool C16>
+void bgemm(const TA *A, int64_t sAb, int64_t sAi, int64_t sAk, const TB *B, int64_t sBb,
+           int64_t sBk, int64_t sBj, void *C, int64_t sCb, int64_t sCi, int I, int J, int K,
+           int batch, float alpha, int band, hipStream_t stream) {
+    hipLaunchKernelGGL((k_blk_bgemm<TA, TB, C16>), dim3((J + GB - 1) / GB, (I + GB - 1) / GB, batch),
+                       dim3(kThreads), 0, stream, A, sAb, sAi, sAk, B, sBb, sBk, sBj, C, sCb, sCi,
+                       I, J, K, alpha, band);
+}
+
+hipError_t calib_block_run(int M, int d, int f, int H, const uint16_t *x, const float *target,
+                           int64_t ldt, const void *const w[4], const uint16_t *gamma1,
+                           const uint16_t *gamma2, float eps, float rope_base,
+                           const float *sigma, const float clip_a[4], const float *clip_w,
+                           float *loss, float *grad_sigma, float *grad_clip_a,
+                           float *grad_clip_w, void *ws, hipStream_t stream) {
+    BlockWs b;
+    block_carve(M, d, f, H, static_cast<uint8_t *>(ws), &b);
+    const int D = d / H;
+    const int64_t ld3 = 3 * (int64_t)d;
+    const float isd = (float)(1.0 / sqrt((double)D));
+    // parameter slices: sigma [qkv d | o d | gu d | down f], clip_w [3d | d | 2f | d]
+    const float *sg[4] = {sigma, sigma + d, sigma + 2 * d, sigma + 3 * d};
+    float *gsg[4] = {grad_sigma, grad_sigma + d, grad_sigma + 2 * d, grad_sigma + 3 * d};
+    const int64_t cwo[4] = {0, 3 * (int64_t)d, 4 * (int64_t)d, 4 * (int64_t)d + 2 * (int64_t)f};
+    hipError_t e;
+    const int64_t Md = (int64_t)M * d, Mf = (int64_t)M * f;
+    const unsigned ebl = (unsigned)((Md + kThreads - 1) / kThreads);
+    const int rows = H * M;
+
+    // ---- forward
+    hipLaunchKernelGGL(k_blk_rmsnorm, dim3(M), dim3(kThreads), 0, stream, x, d, gamma1, eps, b.n1,
+                       b.r1);
+    if ((e = group_forward(b.g[kGQkv], M, b.n1, w[kGQkv], sg[kGQkv], clip_a[kGQkv],
+                           clip_w + cwo[kGQkv], b.qkv, ld3, stream)) != hipSuccess)
+        return e;
+    const int64_t nrope = (int64_t)M * 2 * H * (D / 2);
+    hipLaunchKernelGGL((k_blk_rope<false, uint16_t>), dim3((unsigned)((nrope + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, stream, b.qkv, ld3, M, H, D, (double)rope_base);
+    // S = q k^T / sqrt(D) (causal tiles only), P = softmax, O = P v
+    bgemm<uint16_t, uint16_t, false>(b.qkv, D, ld3, 1, b.qkv + d, D, 1, ld3, b.P, (int64_t)M * M, M,
+                                     M, M, D, H, isd, 3, stream);
+    hipLaunchKernelGGL(k_blk_softmax, dim3((rows + 3) / 4), dim3(kThreads), 0, stream, b.P, M, rows);
+    bgemm<float, uint16_t, true>(b.P, (int64_t)M * M, M, 1, b.qkv + 2 * d, D, ld3, 1, b.O, D, d, M,
+                                 D, M, H, 1.0f, 1, stream);
+    if ((e = group_forward(b.g[kGO], M, b.O, w[kGO], sg[kGO], clip_a[kGO], clip_w + cwo[kGO],
+                           b.o_out, d, stream)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_blk_add16, dim3(ebl), dim3(kThreads), 0, stream, x, b.o_out, b.h, Md);
+    hipLaunchKernelGGL(k_blk_rmsnorm, dim3(M), dim3(kThreads), 0, stream, b.h, d, gamma2, eps, b.n2,
+                       b.r2);
+    if ((e = group_forward(b.g[kGGu], M, b.n2, w[kGGu], sg[kGGu], clip_a[kGGu],
+                           clip_w + cwo[kGGu], b.gu, 2 * (int64_t)f, stream)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_blk_silu_mul, dim3((unsigned)((Mf + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, stream, b.gu, M, f, b.a);
+    if ((e = group_forward(b.g[kGDown], M, b.a, w[kGDown], sg[kGDown], clip_a[kGDown],
+                           clip_w + cwo[kGDown], b.y, d, stream)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_blk_out, dim3(ebl), dim3(kThreads), 0, stream, b.h, b.y, target, ldt, M, d,
+                       (float)(2.0 / ((double)M * d)), b.dout, b.loss_part);
+
+    // ---- backward (the down group also reduces the loss)
+    const double inv_md = 1.0 / ((double)M * d);
+    if ((e = group_backward(b.g[kGDown], M, b.dout, d, b.a, w[kGDown], sg[kGDown], clip_a[kGDown],
+                            clip_w + cwo[kGDown], gsg[kGDown], grad_clip_a + kGDown,
+                            grad_clip_w + cwo[kGDown],
+                            b.da, b.loss_part, b.nloss, inv_md, loss, stream)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_blk_silu_mul_bwd, dim3((unsigned)((Mf + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, stream, b.da, b.gu, M, f, b.dgu);
+    if ((e = group_backward(b.g[kGGu], M, b.dgu, 2 * (int64_t)f, b.n2, w[kGGu], sg[kGGu],
+                            clip_a[kGGu], clip_w + cwo[kGGu], gsg[kGGu], grad_clip_a + kGGu,
+                            grad_clip_w + cwo[kGGu], b.dn2, nullptr, 0, 0.0, b.dummy, stream)) !=
+        hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_blk_rmsnorm_bwd, dim3(M), dim3(kThreads), 0, stream, b.h, gamma2, b.r2,
+                       b.dn2, b.dout, d, b.dh);
+    if ((e = group_backward(b.g[kGO], M, b.dh, d, b.O, w[kGO], sg[kGO], clip_a[kGO],
+                            clip_w + cwo[kGO], gsg[kGO], grad_clip_a + kGO, grad_clip_w + cwo[kGO],
+                            b.dO, nullptr, 0, 0.0, b.dummy, stream)) != hipSuccess)
+        return e;
+    // dP = dO v^T (causal tiles), dS = P (dP - rowsum(P dP)); dq = dS k / sqrt(D),
+    // dk = dS^T q / sqrt(D), dv = P^T dO, into the fused d(q|k|v) rows
+    bgemm<float, uint16_t, false>(b.dO, D, d, 1, b.qkv + 2 * d, D, 1, ld3, b.dP, (int64_t)M * M, M,
+                                  M, M, D, H, 1.0f, 3, stream);
+    hipLaunchKernelGGL(k_blk_softmax_bwd, dim3((rows + 3) / 4), dim3(kThreads), 0, stream, b.P,
+                       b.dP, M, rows);
+    bgemm<float, uint16_t, false>(b.dP, (int64_t)M * M, M, 1, b.qkv + d, D, ld3, 1, b.dqkv, D, ld3,
+                                  M, D, M, H, isd, 1, stream);
+    bgemm<float, uint16_t, false>(b.dP, (int64_t)M * M, 1, M, b.qkv, D, ld3, 1, b.dqkv + d, D, ld3,
+                                  M, D, M, H, isd, 2, stream);
+    bgemm<float, float, false>(b.P, (int64_t)M * M, 1, M, b.dO, D, d, 1, b.dqkv + 2 * d, D, ld3, M,
+                               D, M, H, 1.0f, 2, stream);
+    hipLaunchKernelGGL((k_blk_rope<true, float>), dim3((unsigned)((nrope + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, stream, b.dqkv, ld3, M, H, D, (double)rope_base);
+    return group_backward(b.g[kGQkv], M, b.dqkv, ld3, b.n1, w[kGQkv], sg[kGQkv], clip_a[kGQkv],
+                          clip_w + cwo[kGQkv], gsg[kGQkv], grad_clip_a + kGQkv,
+                          grad_clip_w + cwo[kGQkv], nullptr, nullptr, 0, 0.0, b.dummy, stream);
 }
 
 }  // namespace
@@ -954,6 +1523,24 @@ hipError_t launch_calib_linear(p4q_dtype dt, int M, int N, int K, const void *x,
                                  loss, grad_sigma, grad_clip_a, grad_clip_w, ws, stream);
     return calib_typed<false>(M, N, K, x, ldx, w, ldw, target, ldt, sigma, clip_a, clip_w, loss,
                               grad_sigma, grad_clip_a, grad_clip_w, ws, stream);
+}
+
+size_t calib_block_workspace_bytes(int M, int d, int f, int H) {
+    return block_carve(M, d, f, H, nullptr, nullptr);
+}
+
+hipError_t launch_calib_block(int M, int d, int f, int H, const void *x, const float *target,
+                              int64_t ldt, const void *w_qkv, const void *w_o, const void *w_gu,
+                              const void *w_down, const void *gamma1, const void *gamma2,
+                              float eps, float rope_base, const float *sigma, const float *clip_a,
+                              const float *clip_w, float *loss, float *grad_sigma,
+                              float *grad_clip_a, float *grad_clip_w, void *ws,
+                              hipStream_t stream) {
+    const void *const w[4] = {w_qkv, w_o, w_gu, w_down};
+    return calib_block_run(M, d, f, H, static_cast<const uint16_t *>(x), target, ldt, w,
+                           static_cast<const uint16_t *>(gamma1), static_cast<const uint16_t *>(gamma2),
+                           eps, rope_base, sigma, clip_a, clip_w, loss, grad_sigma, grad_clip_a,
+                           grad_clip_w, ws, stream);
 }
 
 }  // namespace p4q

@@ -283,6 +283,56 @@ int p4q_attention_prefill(p4q_dtype dt, int B, int L, int H, int D, const void *
                       "p4q_attention_prefill");
 }
 
+static int calib_block_shape_error(int M, int d, int f, int H) {
+    if (M <= 0 || d <= 0 || f <= 0 || H <= 0) return P4Q_ERR_INVALID_ARG;
+    if (d % 128 != 0 || f % 128 != 0 || d % H != 0 || (d / H) % 2 != 0) return P4Q_ERR_INVALID_ARG;
+    if (M > 4096 || d > 16384 || f > 16384 || (int64_t)M * 2 * f >= (1LL << 31) ||
+        (int64_t)3 * d * d >= (1LL << 31) || (int64_t)2 * f * d >= (1LL << 31))
+        return P4Q_ERR_UNSUPPORTED;
+    return P4Q_OK;
+}
+
+size_t p4q_calib_block_workspace_bytes(int M, int d, int f, int H) {
+    if (calib_block_shape_error(M, d, f, H) != P4Q_OK) return 0;
+    return p4q::calib_block_workspace_bytes(M, d, f, H);
+}
+
+int p4q_calib_block_grad(p4q_dtype dt, int M, int d, int f, int H, const void *x,
+                         const float *target, int64_t ldt, const void *w_qkv, const void *w_o,
+                         const void *w_gu, const void *w_down, const void *gamma1,
+                         const void *gamma2, float eps, float rope_base, const float *sigma,
+                         const float *clip_a, const float *clip_w, float *loss,
+                         float *grad_sigma, float *grad_clip_a, float *grad_clip_w, void *ws,
+                         size_t ws_bytes, hipStream_t stream) {
+    if (dt != P4Q_FP16) return fail(P4Q_ERR_UNSUPPORTED, "p4q_calib_block_grad: only fp16 blocks");
+    if (const int st = calib_block_shape_error(M, d, f, H))
+        return fail(st, "p4q_calib_block_grad: M=%d d=%d f=%d H=%d outside the limits", M, d, f, H);
+    if (ldt < d) return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_block_grad: ldt=%lld < d", (long long)ldt);
+    if (!(eps >= 0.0f && eps <= 1.0f) || !(rope_base > 1.0f))
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_block_grad: eps=%g rope_base=%g", (double)eps,
+                    (double)rope_base);
+    if (!x || !target || !w_qkv || !w_o || !w_gu || !w_down || !gamma1 || !gamma2 || !sigma ||
+        !clip_a || !clip_w || !loss || !grad_sigma || !grad_clip_a || !grad_clip_w)
+        return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_block_grad: null pointer");
+    for (int g = 0; g < 4; ++g)
+        if (!(clip_a[g] > 0.0f && clip_a[g] <= 1.0f))
+            return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_block_grad: clip_a[%d]=%g outside (0, 1]", g,
+                        (double)clip_a[g]);
+    const void *ptrs[] = {x, target, w_qkv, w_o, w_gu, w_down, gamma1, gamma2, sigma, clip_w,
+                          loss, grad_sigma, grad_clip_a, grad_clip_w};
+    for (const void *q : ptrs)
+        if (!aligned(q, 16)) return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_block_grad: misaligned pointer");
+    if (ldt % 4 != 0) return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_block_grad: ldt not a multiple of 4");
+    const size_t need = p4q::calib_block_workspace_bytes(M, d, f, H);
+    if (!ws || ws_bytes < need)
+        return fail(P4Q_ERR_WORKSPACE, "p4q_calib_block_grad: workspace %zu < %zu bytes", ws_bytes, need);
+    if (!aligned(ws, 256)) return fail(P4Q_ERR_INVALID_ARG, "p4q_calib_block_grad: workspace not 256-byte aligned");
+    return hip_status(p4q::launch_calib_block(M, d, f, H, x, target, ldt, w_qkv, w_o, w_gu, w_down,
+                                              gamma1, gamma2, eps, rope_base, sigma, clip_a, clip_w,
+                                              loss, grad_sigma, grad_clip_a, grad_clip_w, ws, stream),
+                      "p4q_calib_block_grad");
+}
+
 size_t p4q_w4a4_linear_workspace_bytes(int M, int N_out, int K_in) {
     if (M <= 0 || N_out <= 0 || K_in <= 0 || K_in % 32 != 0 || K_in > 131072 ||
         (int64_t)M > 65535LL * 128)

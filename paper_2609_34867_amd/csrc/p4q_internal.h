@@ -119,6 +119,15 @@ hipError_t launch_calib_linear(p4q_dtype dt, int M, int N, int K, const void *x,
                                float *loss, float *grad_sigma, float *grad_clip_a,
                                float *grad_clip_w, void *ws, hipStream_t stream);
 
+size_t calib_block_workspace_bytes(int M, int d, int f, int H);
+hipError_t launch_calib_block(int M, int d, int f, int H, const void *x, const float *target,
+                              int64_t ldt, const void *w_qkv, const void *w_o, const void *w_gu,
+                              const void *w_down, const void *gamma1, const void *gamma2,
+                              float eps, float rope_base, const float *sigma, const float *clip_a,
+                              const float *clip_w, float *loss, float *grad_sigma,
+                              float *grad_clip_a, float *grad_clip_w, void *ws,
+                              hipStream_t stream);
+
 // ---- W4A4 GEMM ---------------------------------------------------------------
 // G_b = C_b C_b^T for b < B, C_b = codes + b * n * (k/2) packed [n, k/2];
 // G int32 [B][n][n].
