@@ -44,6 +44,7 @@ if ROOT not in sys.path:
 
 INT8_PEAK_TOPS = 5000.0      # MI355X dense int8 MFMA
 FP16_PEAK_TFLOPS = 2500.0    # MI355X dense fp16 MFMA
+FP32_PEAK_TFLOPS = 157.3     # MI355X dense fp32
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 N_WEIGHT_SETS = 4
 
@@ -580,6 +581,82 @@ def calibration(dev, reps=20, M=384, N=12288, K=4096):
             "mfma_floor_us": round(floor_us, 2), "mfma_frac": round(floor_us / us, 4)}
 
 
+def calibration_block(dev, reps=10, M=384, d=4096, f=11008, H=32):
+    """One pruning-aware calibration step of a whole W4A4 fake-quantized
+    LLaVA-NeXT-7B decoder block (loss + gradients of every linear group's
+    diagonal scales and clipping factors) on one pruned calibration sample
+    (320 kept visual + 64 text tokens).  Synthetic inputs of the block
+    recipe drawn on the GPU; the target, the full-precision block's output,
+    is computed in the untimed set-up with plain torch fp32 operations."""
+    import torch
+    import paper_2609_34867_amd as p4q
+    g = torch.Generator(device=dev).manual_seed(13)
+    rn = lambda *sh: torch.randn(*sh, generator=g, device=dev, dtype=torch.float32)
+    x = rn(M, d)
+    ch = torch.randperm(d, generator=g, device=dev)[:8]
+    x[:, ch] *= 20.0
+    x = x.half()
+    w = {k: (rn(*sh) * 0.02).half() for k, sh in
+         (("qkv", (3 * d, d)), ("o", (d, d)), ("gu", (2 * f, d)), ("down", (d, f)))}
+    g1, g2 = (1.0 + 0.1 * rn(d)).half(), (1.0 + 0.1 * rn(d)).half()
+    sig = torch.exp(0.3 * rn(3 * d + f))
+    sig[ch] *= 20.0 ** 0.3
+    clip_w = 0.75 + 0.25 * torch.rand(5 * d + 2 * f, generator=g, device=dev)
+    clip_a = [0.9, 0.95, 0.85, 0.9]
+    with torch.no_grad():                                  # full-precision target
+        D = d // H
+
+        def rms(v, gm):
+            return (v * torch.rsqrt((v * v).mean(1, keepdim=True) + 1e-5) * gm.float()).half().float()
+        xf = x.float()
+        qkv = (rms(xf, g1) @ w["qkv"].float().T).half().float()
+        i = torch.arange(D // 2, device=dev, dtype=torch.float64)
+        ang = torch.arange(M, device=dev, dtype=torch.float64)[:, None] * 10000.0 ** (-2 * i / D)
+        c, sn = torch.cos(ang).float()[:, None, :], torch.sin(ang).float()[:, None, :]
+
+        def rope(z):
+            a, b = z[..., :D // 2], z[..., D // 2:]
+            return torch.cat([a * c - b * sn, b * c + a * sn], -1).half().float()
+        q = rope(qkv[:, :d].reshape(M, H, D)).transpose(0, 1).contiguous()
+        k = rope(qkv[:, d:2 * d].reshape(M, H, D)).transpose(0, 1).contiguous()
+        v = qkv[:, 2 * d:].reshape(M, H, D).transpose(0, 1).contiguous()
+        S = torch.matmul(q, k.transpose(1, 2).contiguous()) / D ** 0.5
+        S = S.masked_fill(~torch.tril(torch.ones(M, M, device=dev, dtype=torch.bool)), float("-inf"))
+        O = torch.matmul(torch.softmax(S, -1), v).transpose(0, 1).reshape(M, d).half().float()
+        h = (xf + (O @ w["o"].float().T).half().float()).half().float()
+        gu = (rms(h, g2) @ w["gu"].float().T).half().float()
+        a = (torch.nn.functional.silu(gu[:, :f]) * gu[:, f:]).half().float()
+        target = (h + (a @ w["down"].float().T).half().float()).half().float().contiguous()
+        del qkv, q, k, v, S, O, h, gu, a
+    ws = p4q.calib_block_workspace(M, d, f, H, dev)
+    outs = (torch.empty(1, device=dev), torch.empty(3 * d + f, device=dev),
+            torch.empty(4, device=dev), torch.empty(5 * d + 2 * f, device=dev))
+    run = lambda: p4q.calib_block_grad(x, target, w["qkv"], w["o"], w["gu"], w["down"], g1, g2, H,
+                                       sig, clip_a, clip_w, workspace=ws, out=outs)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    mnk = M * (3 * d * d + d * d + 2 * f * d + d * f)
+    attn = 6 * 2 * H * M * M * D            # 6 fp32 products per head (full tiles)
+    # the matrix units' floor: int8 forward GEMMs, two bf16 backward
+    # contractions per group, the attention products at the fp32 peak
+    floor_us = (2 * mnk / (INT8_PEAK_TOPS * 1e6) + 4 * mnk / (FP16_PEAK_TFLOPS * 1e6)
+                + attn / (FP32_PEAK_TFLOPS * 1e6))
+    del ws
+    return {"workload": f"calibration step of one W4A4 LLaVA-NeXT-7B decoder block: M={M} (320 kept "
+                        f"visual + 64 text tokens), d={d}, f={f}, {H} heads, fp16; loss + d sigma, "
+                        f"d clip_a, d clip_w of the 4 linear groups",
+            "us": round(us, 2), "steps_per_s": round(1e6 / us, 1),
+            "mfma_floor_us": round(floor_us, 2), "mfma_frac": round(floor_us / us, 4)}
+
+
 def copy_calibration(dev, nbytes=1 << 30, reps=5):
     """A plain device-to-device copy of known size, run so that the HBM
     counters (FETCH_SIZE, WRITE_SIZE) can be scaled to bytes: the counter
@@ -627,7 +704,8 @@ def main():
         copy_calibration(dev)
         return
     if args.calib_only:
-        print(json.dumps({"calibration_step": calibration(dev)}), flush=True)
+        print(json.dumps({"calibration_step": calibration(dev),
+                          "calibration_block_step": calibration_block(dev)}), flush=True)
         return
     if args.decode_only:
         print(json.dumps({"decode_gemv": decode_gemv(dev)}), flush=True)
@@ -693,6 +771,7 @@ def main():
     res["attention_prefill"] = attention(cfg, dev)
     if not args.no_calib:
         res["calibration_step"] = calibration(dev)
+        res["calibration_block_step"] = calibration_block(dev)
     if not args.no_select_full:
         res["selector_full"] = selector_full(cfg, dev)
     if not args.no_decode:

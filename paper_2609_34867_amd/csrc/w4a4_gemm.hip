@@ -893,13 +893,25 @@ __global__ __launch_bounds__(64 * NW) void k_w4a4_gemv(const uint8_t *__restrict
 
 }  // namespace
 
+// The 256 x 128, two-blocks-per-CU kernel serves every shape with M >= 1024
+// and N >= 1024, and batch-1 shapes (M >= 256) wide enough to give it at
+// least 128 tiles (the fused q|k|v and gate|up launches of one image's
+// pruned sequence: measured 1.3-1.4x faster there than the small-M kernel,
+// which keeps the narrow o / down launches and splits their K).
+static bool use_large_tiles(int M, int N) {
+    if (N < 1024 || M < 256) return false;
+    if (M >= 1024) return true;
+    const int64_t tiles = (((int64_t)M + L_BM - 1) / L_BM) * (((int64_t)N + L_BN - 1) / L_BN);
+    return tiles >= 128;
+}
+
 // Small-M shapes with fewer 128 x 128 tiles than CUs split K across
 // work-groups (exact int32 partials, summed by the epilogue kernel):
 // S = ceil(256 / tiles), at most 4, each slice at least 4 k-tiles of 256.
-// Not for the decode GEMV or the large-M kernel (M >= 1024 and N >= 1024),
-// nor when N % 4 != 0 (the epilogue writes 4 outputs per thread).
+// Not for the decode GEMV or the large-tile kernel, nor when N % 4 != 0
+// (the epilogue writes 4 outputs per thread).
 static int small_m_splits(int M, int N, int K) {
-    if (M <= 16 || (M >= 1024 && N >= 1024) || N % 4 != 0) return 1;
+    if (M <= 16 || use_large_tiles(M, N) || N % 4 != 0) return 1;
     const int64_t tiles = (((int64_t)M + BM - 1) / BM) * (((int64_t)N + BN - 1) / BN);
     const int kt_all = (K / 2 + KS_ROW - 1) / KS_ROW;
     if (tiles >= 256) return 1;
@@ -942,7 +954,7 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
         P4Q_GEMV(7, 16, 1)
 #undef P4Q_GEMV
     }
-    if (M >= 1024 && N >= 1024) {
+    if (use_large_tiles(M, N)) {
         const int tiles_m = (M + L_BM - 1) / L_BM, tiles_n = (N + L_BN - 1) / L_BN;
         const dim3 grid(tiles_m * tiles_n);
         auto go = [&](auto kern) {
