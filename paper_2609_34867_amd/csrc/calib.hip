@@ -994,14 +994,25 @@ __global__ __launch_bounds__(kThreads) void k_blk_rmsnorm_bwd(
         dx[o + k] = dres[o + k] + (float)r * f16v(gamma[k]) * dn[o + k] - f16v(x[o + k]) * c;
 }
 
+// cos / sin of position p times theta_i = base^(-2i/D) for p < M, i < D/2,
+// computed in double and rounded to fp32: tab[p][i] = (cos, sin)
+__global__ __launch_bounds__(kThreads) void k_blk_rope_table(int M, int D, double base,
+                                                            float2 *__restrict__ tab) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int half = D / 2;
+    if (idx >= (int64_t)M * half) return;
+    const int i = (int)(idx % half), m = (int)(idx / half);
+    const double ang = (double)m * pow(base, -2.0 * i / D);
+    tab[idx] = make_float2((float)cos(ang), (float)sin(ang));
+}
+
 // Rotary embedding of q and k (columns [0, 2 d) of the fused q|k|v rows):
-// channel i < D/2 of a head pairs with i + D/2, angle p theta_i, theta_i =
-// base^(-2i/D), p the token position; angles and their cosines in double.
-// forward: in place on the fp16 values; backward (BWD): the transposed
-// rotation in place on the fp32 gradients.
+// channel i < D/2 of a head pairs with i + D/2, angle p theta_i (the table
+// above).  forward: in place on the fp16 values; backward (BWD): the
+// transposed rotation in place on the fp32 gradients.
 template <bool BWD, typename T>
 __global__ __launch_bounds__(kThreads) void k_blk_rope(T *__restrict__ z, int64_t ld, int M,
-                                                      int H, int D, double base) {
+                                                      int H, int D, const float2 *__restrict__ tab) {
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int half = D / 2;
     const int64_t total = (int64_t)M * 2 * H * half;
@@ -1009,8 +1020,8 @@ __global__ __launch_bounds__(kThreads) void k_blk_rope(T *__restrict__ z, int64_
     const int i = (int)(idx % half);
     const int hh = (int)((idx / half) % (2 * H));           // q heads, then k heads
     const int m = (int)(idx / ((int64_t)half * 2 * H));
-    const double ang = (double)m * pow(base, -2.0 * i / D);
-    const float c = (float)cos(ang), s = (float)sin(ang);
+    const float2 cs = tab[(int64_t)m * half + i];
+    const float c = cs.x, s = cs.y;
     T *row = z + (int64_t)m * ld + (int64_t)hh * D;
     if constexpr (BWD) {
         const float a = row[i], b = row[i + half];
@@ -1032,12 +1043,13 @@ template <> __device__ __forceinline__ float ldv<uint16_t>(const uint16_t *p, in
 // Batched strided GEMM with fp32 accumulation (the attention products of
 // one block): C[b](i, j) = alpha sum_k A[b](i, k) B[b](k, j); A element
 // (i, k) at A + b sAb + i sAi + k sAk, B (k, j) at B + b sBb + k sBk + j sBj,
-// C (i, j) at C + b sCb + i sCi + j.  64 x 64 tiles, 16 k per stage, 256
-// threads with 4 x 4 outputs each.  band: 0 all k; 1 only k <= i (A is
-// lower triangular: P or dS); 2 only k >= i (A is upper triangular: P^T or
-// dS^T); 3 full k, tiles strictly above the diagonal (j > i everywhere)
-// skipped (their entries are never read).
-constexpr int GB = 64, GK = 16;
+// C (i, j) at C + b sCb + i sCi + j.  64 x 64 tiles, 32 k per stage, 256
+// threads with 4 x 4 outputs each; the next stage's elements are loaded into
+// registers while the current stage is multiplied.  band: 0 all k; 1 only
+// k <= i (A is lower triangular: P or dS); 2 only k >= i (A is upper
+// triangular: P^T or dS^T); 3 full k, tiles strictly above the diagonal
+// (j > i everywhere) skipped (their entries are never read).
+constexpr int GB = 64, GK = 32;
 template <typename TA, typename TB, bool C16>
 __global__ __launch_bounds__(kThreads) void k_blk_bgemm(
     const TA *__restrict__ A, int64_t sAb, int64_t sAi, int64_t sAk, const TB *__restrict__ B,
@@ -1059,19 +1071,36 @@ __global__ __launch_bounds__(kThreads) void k_blk_bgemm(
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[r][c] = 0.0f;
     const bool a_kfast = (sAk == 1), b_jfast = (sBj == 1);
+    // this thread's 8 elements of each stage: A (kk, ii), B (kb, jj)
+    int akk[8], aii[8], bkk[8], bjj[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const int e = t + kThreads * q;
+        akk[q] = a_kfast ? (e & 31) : (e >> 6);
+        aii[q] = a_kfast ? (e >> 5) : (e & 63);
+        bkk[q] = b_jfast ? (e >> 6) : (e & 31);
+        bjj[q] = b_jfast ? (e & 63) : (e >> 5);
+    }
+    float ra[8], rb[8];
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int i = i0 + aii[q], k = k0 + akk[q];
+            ra[q] = (i < I && k < kend) ? ldv<TA>(A, (int64_t)i * sAi + (int64_t)k * sAk) : 0.0f;
+            const int j = j0 + bjj[q], kq = k0 + bkk[q];
+            rb[q] = (j < J && kq < kend) ? ldv<TB>(B, (int64_t)kq * sBk + (int64_t)j * sBj) : 0.0f;
+        }
+    };
+    if (kbeg < kend) load(kbeg);
     for (int k0 = kbeg; k0 < kend; k0 += GK) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = t + kThreads * q;
-            const int kk = a_kfast ? (e & 15) : (e >> 6), ii = a_kfast ? (e >> 4) : (e & 63);
-            const int i = i0 + ii, k = k0 + kk;
-            As[kk][ii] = (i < I && k < kend) ? ldv<TA>(A, (int64_t)i * sAi + (int64_t)k * sAk) : 0.0f;
-            const int kb = b_jfast ? (e >> 6) : (e & 15), jj = b_jfast ? (e & 63) : (e >> 4);
-            const int j = j0 + jj, kq = k0 + kb;
-            Bs[kb][jj] = (j < J && kq < kend) ? ldv<TB>(B, (int64_t)kq * sBk + (int64_t)j * sBj) : 0.0f;
+        for (int q = 0; q < 8; ++q) {
+            As[akk[q]][aii[q]] = ra[q];
+            Bs[bkk[q]][bjj[q]] = rb[q];
         }
         __syncthreads();
-#pragma unroll
+        if (k0 + GK < kend) load(k0 + GK);          // in flight during this stage
+#pragma unroll 8
         for (int kk = 0; kk < GK; ++kk) {
             float a[4], bv[4];
 #pragma unroll
@@ -1240,31 +1269,37 @@ __global__ __launch_bounds__(kThreads) void k_blk_upstream(
 // The gradient with respect to a linear group's input X (X' = X / sigma):
 //   dX[m][k] = (sum_z gpart[z][m][k] + [k = kstar_m] g_s[m] clip / 7
 //               sign(X'[m][k])) / sigma_k,
-// g_s[m] = the row's slot sums (its share through the scale).  One block
-// per row.
+// g_s[m] = the row's slot sums (its share through the scale).  Grid
+// (ceil(K / 1024), M): each thread handles 4 consecutive k of row m (K % 4
+// == 0) and every block re-sums its row's slots.
 __global__ __launch_bounds__(kThreads) void k_blk_input_grad(
     const float *__restrict__ gpart, int ns, const float *__restrict__ rowpart, int nslots,
     const float *__restrict__ xprime, const int32_t *__restrict__ kstar,
     const float *__restrict__ scales, float clip, const float *__restrict__ sigma, int M, int K,
     float *__restrict__ dX) {
     __shared__ double red[kThreads / 64];
-    const int m = blockIdx.x, t = threadIdx.x;
+    const int m = blockIdx.y, t = threadIdx.x;
     double gs = 0.0;
-    for (int s = t; s < nslots; s += kThreads) gs += (double)rowpart[(int64_t)s * M + m];
+    for (int s2 = t; s2 < nslots; s2 += kThreads) gs += (double)rowpart[(int64_t)s2 * M + m];
     gs = block_sum_f(gs, red);
-    const int ks = kstar[m];
-    const bool live = scales[m] != 0.0f;
-    for (int k = t; k < K; k += kThreads) {
-        double v = 0.0;
-        for (int z = 0; z < ns; ++z) v += (double)gpart[((int64_t)z * M + m) * K + k];
-        if (live && k == ks) {
-            const float xp = xprime[(int64_t)m * K + k];
-            v += gs * (double)clip / 7.0 * (xp > 0.0f ? 1.0 : (xp < 0.0f ? -1.0 : 0.0));
-        }
-        dX[(int64_t)m * K + k] = (float)(v / (double)sigma[k]);
+    const int k = 4 * (blockIdx.x * kThreads + t);
+    if (k >= K) return;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int z = 0; z < ns; ++z) {
+        const float4 g = *reinterpret_cast<const float4 *>(gpart + ((int64_t)z * M + m) * K + k);
+        v.x += g.x; v.y += g.y; v.z += g.z; v.w += g.w;
     }
+    float o[4] = {v.x, v.y, v.z, v.w};
+    const int ks = kstar[m];
+    if (scales[m] != 0.0f && ks >= k && ks < k + 4) {
+        const float xp = xprime[(int64_t)m * K + ks];
+        const double share = gs * (double)clip / 7.0 * (xp > 0.0f ? 1.0 : (xp < 0.0f ? -1.0 : 0.0));
+        o[ks - k] = (float)((double)o[ks - k] + share);
+    }
+    const float4 sg = *reinterpret_cast<const float4 *>(sigma + k);
+    *reinterpret_cast<float4 *>(dX + (int64_t)m * K + k) =
+        make_float4(o[0] / sg.x, o[1] / sg.y, o[2] / sg.z, o[3] / sg.w);
 }
-
 
 // ---------------------------------------------------------------------------
 // Block-level calibration, host side
@@ -1283,8 +1318,11 @@ struct BlockWs {
     BlockGroup g[4];
     uint16_t *n1, *qkv, *O, *o_out, *h, *n2, *gu, *a, *y;
     float *r1, *r2, *P, *dP, *dout, *da, *dgu, *dn2, *dh, *dO, *dqkv, *dummy;
+    float2 *rope;
     double *loss_part;
     int nloss;
+    void *gemm_ws;          // split-K workspace of the forward GEMMs
+    size_t gemm_ws_bytes;
 };
 
 void block_groups(int d, int f, BlockGroup *g) {
@@ -1321,6 +1359,11 @@ size_t block_carve(int M, int d, int f, int H, uint8_t *base, BlockWs *w) {
     b.r1 = f32(M); b.r2 = f32(M); b.P = f32(HMM); b.dP = f32(HMM); b.dout = f32(Md);
     b.da = f32(Mf); b.dgu = f32(2 * Mf); b.dn2 = f32(Md); b.dh = f32(Md); b.dO = f32(Md);
     b.dqkv = f32(3 * Md); b.dummy = f32(64);
+    b.rope = reinterpret_cast<float2 *>(take((size_t)M * (d / H / 2) * 8));
+    b.gemm_ws_bytes = 0;
+    for (int i = 0; i < 4; ++i)
+        b.gemm_ws_bytes = std::max(b.gemm_ws_bytes, gemm_workspace_bytes(M, b.g[i].N, b.g[i].K));
+    b.gemm_ws = b.gemm_ws_bytes ? take(b.gemm_ws_bytes) : nullptr;
     b.nloss = (int)((Md + kThreads - 1) / kThreads);
     b.loss_part = reinterpret_cast<double *>(take((size_t)b.nloss * 8));
     if (w) *w = b;
@@ -1331,7 +1374,7 @@ size_t block_carve(int M, int d, int f, int H, uint8_t *base, BlockWs *w) {
 // W4A4 GEMM into y (fp16, row stride ldy)
 hipError_t group_forward(BlockGroup &g, int M, const uint16_t *X, const void *W,
                          const float *sigma, float clip_a, const float *clip_w, uint16_t *y,
-                         int64_t ldy, hipStream_t stream) {
+                         int64_t ldy, void *gemm_ws, size_t gemm_ws_bytes, hipStream_t stream) {
     CalibWs &c = g.c;
     const int N = g.N, K = g.K;
     hipError_t e;
@@ -1351,7 +1394,7 @@ hipError_t group_forward(BlockGroup &g, int M, const uint16_t *X, const void *W,
                            c.codesW, N, K / 2, c.CwT, (int64_t)N);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_w4a4_gemm(M, N, K, c.codesA, c.sA, c.codesW, c.sW, P4Q_FP16, y, ldy, nullptr,
-                            nullptr, 0, stream);
+                            gemm_ws, gemm_ws_bytes, stream);
 }
 
 // backward of one group from its upstream gradient G [M][N] (fp32, row
@@ -1385,9 +1428,9 @@ hipError_t group_backward(BlockGroup &g, int M, const float *G, int64_t ldg, con
                        1.0, grad_sigma, loss_part, nloss, inv_md, loss, c.dclipa_part, p.nbA,
                        grad_clip_a);
     if (dX)
-        hipLaunchKernelGGL(k_blk_input_grad, dim3(M), dim3(kThreads), 0, stream, g.gpart, p.nsA,
-                           c.rowA, (K / BB) * p.nsA, c.xprime, c.kA, c.sA, clip_a, sigma, M, K,
-                           dX);
+        hipLaunchKernelGGL(k_blk_input_grad, dim3((K + 4 * kThreads - 1) / (4 * kThreads), M),
+                           dim3(kThreads), 0, stream, g.gpart, p.nsA, c.rowA, (K / BB) * p.nsA,
+                           c.xprime, c.kA, c.sA, clip_a, sigma, M, K, dX);
     return hipGetLastError();
 }
 
@@ -1425,11 +1468,14 @@ hipError_t calib_block_run(int M, int d, int f, int H, const uint16_t *x, const 
     hipLaunchKernelGGL(k_blk_rmsnorm, dim3(M), dim3(kThreads), 0, stream, x, d, gamma1, eps, b.n1,
                        b.r1);
     if ((e = group_forward(b.g[kGQkv], M, b.n1, w[kGQkv], sg[kGQkv], clip_a[kGQkv],
-                           clip_w + cwo[kGQkv], b.qkv, ld3, stream)) != hipSuccess)
+                           clip_w + cwo[kGQkv], b.qkv, ld3, b.gemm_ws, b.gemm_ws_bytes, stream)) != hipSuccess)
         return e;
     const int64_t nrope = (int64_t)M * 2 * H * (D / 2);
+    const int64_t ntab = (int64_t)M * (D / 2);
+    hipLaunchKernelGGL(k_blk_rope_table, dim3((unsigned)((ntab + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, stream, M, D, (double)rope_base, b.rope);
     hipLaunchKernelGGL((k_blk_rope<false, uint16_t>), dim3((unsigned)((nrope + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, stream, b.qkv, ld3, M, H, D, (double)rope_base);
+                       dim3(kThreads), 0, stream, b.qkv, ld3, M, H, D, (const float2 *)b.rope);
     // S = q k^T / sqrt(D) (causal tiles only), P = softmax, O = P v
     bgemm<uint16_t, uint16_t, false>(b.qkv, D, ld3, 1, b.qkv + d, D, 1, ld3, b.P, (int64_t)M * M, M,
                                      M, M, D, H, isd, 3, stream);
@@ -1437,18 +1483,19 @@ hipError_t calib_block_run(int M, int d, int f, int H, const uint16_t *x, const 
     bgemm<float, uint16_t, true>(b.P, (int64_t)M * M, M, 1, b.qkv + 2 * d, D, ld3, 1, b.O, D, d, M,
                                  D, M, H, 1.0f, 1, stream);
     if ((e = group_forward(b.g[kGO], M, b.O, w[kGO], sg[kGO], clip_a[kGO], clip_w + cwo[kGO],
-                           b.o_out, d, stream)) != hipSuccess)
+                           b.o_out, d, b.gemm_ws, b.gemm_ws_bytes, stream)) != hipSuccess)
         return e;
     hipLaunchKernelGGL(k_blk_add16, dim3(ebl), dim3(kThreads), 0, stream, x, b.o_out, b.h, Md);
     hipLaunchKernelGGL(k_blk_rmsnorm, dim3(M), dim3(kThreads), 0, stream, b.h, d, gamma2, eps, b.n2,
                        b.r2);
     if ((e = group_forward(b.g[kGGu], M, b.n2, w[kGGu], sg[kGGu], clip_a[kGGu],
-                           clip_w + cwo[kGGu], b.gu, 2 * (int64_t)f, stream)) != hipSuccess)
+                           clip_w + cwo[kGGu], b.gu, 2 * (int64_t)f, b.gemm_ws, b.gemm_ws_bytes,
+                           stream)) != hipSuccess)
         return e;
     hipLaunchKernelGGL(k_blk_silu_mul, dim3((unsigned)((Mf + kThreads - 1) / kThreads)),
                        dim3(kThreads), 0, stream, b.gu, M, f, b.a);
     if ((e = group_forward(b.g[kGDown], M, b.a, w[kGDown], sg[kGDown], clip_a[kGDown],
-                           clip_w + cwo[kGDown], b.y, d, stream)) != hipSuccess)
+                           clip_w + cwo[kGDown], b.y, d, b.gemm_ws, b.gemm_ws_bytes, stream)) != hipSuccess)
         return e;
     hipLaunchKernelGGL(k_blk_out, dim3(ebl), dim3(kThreads), 0, stream, b.h, b.y, target, ldt, M, d,
                        (float)(2.0 / ((double)M * d)), b.dout, b.loss_part);
@@ -1486,7 +1533,7 @@ hipError_t calib_block_run(int M, int d, int f, int H, const uint16_t *x, const 
     bgemm<float, float, false>(b.P, (int64_t)M * M, 1, M, b.dO, D, d, 1, b.dqkv + 2 * d, D, ld3, M,
                                D, M, H, 1.0f, 2, stream);
     hipLaunchKernelGGL((k_blk_rope<true, float>), dim3((unsigned)((nrope + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, stream, b.dqkv, ld3, M, H, D, (double)rope_base);
+                       dim3(kThreads), 0, stream, b.dqkv, ld3, M, H, D, (const float2 *)b.rope);
     return group_backward(b.g[kGQkv], M, b.dqkv, ld3, b.n1, w[kGQkv], sg[kGQkv], clip_a[kGQkv],
                           clip_w + cwo[kGQkv], gsg[kGQkv], grad_clip_a + kGQkv,
                           grad_clip_w + cwo[kGQkv], nullptr, nullptr, 0, 0.0, b.dummy, stream);
