@@ -368,17 +368,18 @@ __global__ __launch_bounds__(256) void k_splitk_epilogue(const int32_t *__restri
 }
 
 // ---------------------------------------------------------------------------
-// Large-M kernel: 256 (m) x 128 (n) block tile, 4 wavefronts of 128 x 64
-// (4 x 8 tiles of v_mfma_i32_16x16x64_i8, 128 accumulator registers), and
-// at most 256 registers per lane, so TWO blocks are resident per CU: one
-// wavefront of each block on every SIMD.  While one block waits on its
+// Two-blocks-per-CU kernel: BMT (m) x 128 (n) block tile, BMT = 256 for the
+// large shapes and 128 for one image's pruned sequence; 4 wavefronts of
+// BMT/2 x 64 (4 x BMT/32 tiles of v_mfma_i32_16x16x64_i8: 128 or 64
+// accumulator registers), and at most 256 registers per lane, so TWO blocks
+// are resident per CU: one wavefront of each block on every SIMD.  While one block waits on its
 // operand DMA, its LDS reads or its epilogue, the other block's wavefront
 // keeps the SIMD's matrix unit busy.
 //  * Packed int4 tiles go straight from HBM to LDS (buffer_load ... lds): no
 //    staging registers and no LDS store instructions.  Out-of-range rows and
 //    k-chunks are zero-filled by the buffer's range check.  A ring of 3 LDS
-//    stages (24 KB each) keeps 2 k-tiles in flight; waits are explicit
-//    (vmcnt + a bare s_barrier).
+//    stages (24 or 16 KB each) keeps 2 k-tiles in flight; waits are
+//    explicit (vmcnt + a bare s_barrier).
 //  * After the LDS read each wave unpacks its fragments to int8 in registers.
 //  * The weight fragment is the MFMA's first operand: lane l then owns four
 //    consecutive output columns n of one row m.
@@ -388,11 +389,15 @@ __global__ __launch_bounds__(256) void k_splitk_epilogue(const int32_t *__restri
 //  * Work-group ids are remapped so that each XCD (ids are dealt round-robin
 //    over 8 XCDs) walks a contiguous, M-grouped range of tiles, sharing A and
 //    W panels in its own L2.
+//  * SPLIT: work-group (tile, z) covers only k-tiles [z kps, (z + 1) kps) of
+//    its tile and stores its exact int32 partial sums to part[z][M][N];
+//    k_splitk_epilogue adds the slices and applies the epilogue.  For the
+//    narrow batch-1 launches, whose tiles alone would leave most CUs idle.
 // ---------------------------------------------------------------------------
 constexpr int L_BM = 256, L_BN = 128;
 constexpr int L_STAGES = 3;
-constexpr int L_STAGE = (L_BM + L_BN) * BKB;       // 24 KB of packed codes
-constexpr int L_SCALE_OFF = L_STAGES * L_STAGE;    // sa[256], sw[128] (fp32)
+template <int BMT> constexpr int l_stage() { return (BMT + L_BN) * BKB; }   // packed codes
+template <int BMT> constexpr int l_scale_off() { return L_STAGES * l_stage<BMT>(); }
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 
@@ -429,11 +434,17 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
     return (uint32_t)(size_t)(lds_ptr_t)p;
 }
 
-__device__ __forceinline__ void tile_coords(int wg, int tiles_m, int tiles_n, int &tm, int &tn) {
-    const int T = tiles_m * tiles_n;
-    const int q = T / kXcds, r = T % kXcds;
+// Work-group id -> logical index such that the ids of one XCD (dealt
+// round-robin) form a contiguous range of [0, total).
+__device__ __forceinline__ int xcd_logical(int wg, int total) {
+    const int q = total / kXcds, r = total % kXcds;
     const int x = wg % kXcds, i = wg / kXcds;
-    const int logical = (x < r) ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+    return (x < r) ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+}
+
+// logical index -> tile, walking groups of kGroupM tile rows column by column
+__device__ __forceinline__ void grouped_tile(int logical, int tiles_m, int tiles_n, int &tm,
+                                             int &tn) {
     const int per_group = kGroupM * tiles_n;
     const int g = logical / per_group;
     const int first_m = g * kGroupM;
@@ -445,7 +456,7 @@ __device__ __forceinline__ void tile_coords(int wg, int tiles_m, int tiles_n, in
 
 // Gram mode (M == N, A == W): only tiles holding an entry on or above the
 // diagonal, i.e. tn >= 2 tm for 256 x 128 tiles; row tm of tiles holds
-// tiles_n - 2 tm of them.  Same XCD-contiguous dealing as tile_coords.
+// tiles_n - 2 tm of them.  Same XCD-contiguous dealing as xcd_logical.
 __device__ __forceinline__ void gram_tile_coords(int wg, int total, int tiles_n, int &tm, int &tn) {
     const int q = total / kXcds, r = total % kXcds;
     const int x = wg % kXcds, i = wg / kXcds;
@@ -470,7 +481,7 @@ __device__ __forceinline__ v4i unpack2(uint32_t w0, uint32_t w1) {
 // holds their count), each entry m < n is stored at [m][n] and at [n][m];
 // blockIdx.y selects one problem of a batch (A, W, acc_out advanced by their
 // strides).
-template <bool BF16OUT, bool ACC, bool YOUT>
+template <int BMT, bool BF16OUT, bool ACC, bool YOUT, bool SPLIT>
 __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restrict__ A,
                                                           const float *__restrict__ sa,
                                                           const uint8_t *__restrict__ W,
@@ -480,32 +491,53 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
                                                           int32_t *__restrict__ acc_out,
                                                           int tiles_m, int tiles_n,
                                                           int64_t a_bstride, int64_t w_bstride,
-                                                          int64_t acc_bstride) {
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[L_STAGES * L_STAGE + 1536];
+                                                          int64_t acc_bstride, int kps,
+                                                          int32_t *__restrict__ part) {
+    static_assert(BMT == 256 || (BMT == 128 && YOUT), "tile height");
+    static_assert(!SPLIT || (YOUT && !ACC), "split-K stores partial sums only");
+    constexpr int L_STAGE = l_stage<BMT>();
+    constexpr int AI = BMT / 64;          // A DMA instructions per wavefront and stage
+    constexpr int AF = BMT / 32;          // A fragments (16 rows) per wavefront
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[l_scale_off<BMT>() + (BMT + L_BN) * 4];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    A += blockIdx.y * a_bstride;
-    W += blockIdx.y * w_bstride;
-    if constexpr (ACC) acc_out += blockIdx.y * acc_bstride;
+    if constexpr (!SPLIT) {               // Gram mode: blockIdx.y selects the problem
+        A += blockIdx.y * a_bstride;
+        W += blockIdx.y * w_bstride;
+        if constexpr (ACC) acc_out += blockIdx.y * acc_bstride;
+    }
     const int wm = wave >> 1, wn = wave & 1;
-    int tm, tn;
-    if constexpr (YOUT) tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
-    else gram_tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * L_BM, n0 = tn * L_BN;
-    const int ktiles = (Kb + BKB - 1) / BKB;
+    int tm, tn, split = 0;
+    if constexpr (YOUT) {
+        const int T = tiles_m * tiles_n;
+        int logical = xcd_logical((int)(blockIdx.x + (SPLIT ? blockIdx.y * gridDim.x : 0u)),
+                                  SPLIT ? T * (int)gridDim.y : T);
+        if constexpr (SPLIT) {
+            split = logical / T;
+            logical -= split * T;
+        }
+        grouped_tile(logical, tiles_m, tiles_n, tm, tn);
+    } else {
+        gram_tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    }
+    const int m0 = tm * BMT, n0 = tn * L_BN;
+    // this block's k-tiles [kbeg, kbeg + ktiles); the launch makes every split non-empty
+    const int ktiles_all = (Kb + BKB - 1) / BKB;
+    const int kbeg = SPLIT ? split * kps : 0;
+    const int ktiles = SPLIT ? min(ktiles_all - kbeg, kps) : ktiles_all;
 
-    const v4i dA = buffer_desc(A + (int64_t)m0 * Kb, (uint32_t)(min(M - m0, L_BM) * Kb));
+    const v4i dA = buffer_desc(A + (int64_t)m0 * Kb, (uint32_t)(min(M - m0, BMT) * Kb));
     const v4i dW = buffer_desc(W + (int64_t)n0 * Kb, (uint32_t)(min(N - n0, L_BN) * Kb));
 
     // DMA: one 1 KB instruction fills 16 rows of 64 bytes; lane L -> row
     // +L/4, slot L%4, which holds k-chunk (L%4) ^ ((row >> 1) & 3).  Wave w
-    // copies A rows [64w, 64w+64) (4 instructions) and W rows [32w, 32w+32)
-    // (2 instructions).
+    // copies A rows [w BMT/4, (w + 1) BMT/4) (AI instructions) and W rows
+    // [32w, 32w+32) (2 instructions).
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    uint32_t voffA[4], voffW[2];
-    int kcA[4], kcW[2];
+    uint32_t voffA[AI], voffW[2];
+    int kcA[AI], kcW[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int row = 64 * wave + 16 * i + (lane >> 2);
+    for (int i = 0; i < AI; ++i) {
+        const int row = (BMT / 4) * wave + 16 * i + (lane >> 2);
         kcA[i] = ((lane & 3) ^ ((row >> 1) & 3)) * 16;
         voffA[i] = (uint32_t)(row * Kb + kcA[i]);
     }
@@ -515,11 +547,11 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         kcW[i] = ((lane & 3) ^ ((row >> 1) & 3)) * 16;
         voffW[i] = (uint32_t)(row * Kb + kcW[i]);
     }
-    const uint32_t ldsA = lds_addr(smem) + wave_u * 4096;
-    const uint32_t ldsW = lds_addr(smem) + L_BM * BKB + wave_u * 2048;
+    const uint32_t ldsA = lds_addr(smem) + wave_u * (BMT / 4) * BKB;
+    const uint32_t ldsW = lds_addr(smem) + BMT * BKB + wave_u * 2048;
     auto issue = [&](int slot, int kt) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < AI; ++i) {
             const uint32_t o = (kt * BKB + kcA[i] < Kb) ? voffA[i] + (uint32_t)(kt * BKB) : 0x80000000u;
             dma16(dA, o, ldsA + slot * L_STAGE + i * 1024);
         }
@@ -530,58 +562,69 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         }
     };
 
-    if constexpr (YOUT) {   // the block's scales -> LDS (zeros past M / N), ahead of the stages
-        const v4i dSa = buffer_desc(sa + m0, (uint32_t)(min(M - m0, L_BM) * 4));
+    if constexpr (YOUT && !SPLIT) {   // the block's scales -> LDS (zeros past M / N), ahead of the stages
+        const v4i dSa = buffer_desc(sa + m0, (uint32_t)(min(M - m0, BMT) * 4));
         const v4i dSw = buffer_desc(sw + n0, (uint32_t)(min(N - n0, L_BN) * 4));
-        const uint32_t sbase = lds_addr(smem) + L_SCALE_OFF;
-        dma4(dSa, (uint32_t)(64 * wave + lane) * 4u, sbase + wave_u * 256);
-        if (wave_u < 2) dma4(dSw, (uint32_t)(64 * wave + lane) * 4u, sbase + 1024 + wave_u * 256);
+        const uint32_t sbase = lds_addr(smem) + l_scale_off<BMT>();
+        if constexpr (BMT == 256) {
+            dma4(dSa, (uint32_t)(64 * wave + lane) * 4u, sbase + wave_u * 256);
+            if (wave_u < 2) dma4(dSw, (uint32_t)(64 * wave + lane) * 4u, sbase + 1024 + wave_u * 256);
+        } else {                      // 128 + 128 scales: waves 0, 1 and 2, 3
+            if (wave_u < 2) dma4(dSa, (uint32_t)(64 * wave + lane) * 4u, sbase + wave_u * 256);
+            else dma4(dSw, (uint32_t)(64 * (wave - 2) + lane) * 4u, sbase + 512 + (wave_u - 2) * 256);
+        }
     }
-    issue(0, 0);
-    if (ktiles > 1) issue(1, 1);
+    issue(0, kbeg);
+    if (ktiles > 1) issue(1, kbeg + 1);
 
-    v4i acc[4][8];
+    v4i acc[4][AF];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+        for (int j = 0; j < AF; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
-    // Fragments: W f = 0..3 (rows wn*64 + 16f), A f = 4..11 (rows
-    // wm*128 + 16(f-4)).  Lane l reads row l%16, chunk l/16 (32 k values;
+    // Fragments: W f = 0..3 (rows wn*64 + 16f), A f = 4..3+AF (rows
+    // wm*BMT/2 + 16(f-4)).  Lane l reads row l%16, chunk l/16 (32 k values;
     // words x,y feed k-step 0 and z,w k-step 1 -- the same placement for A
     // and W, so every k meets its partner exactly once).
     const int r16 = lane & 15, cq = lane >> 4;
     const uint32_t cofs = (uint32_t)((cq ^ ((r16 >> 1) & 3)) << 4);
-    const uint32_t fW = L_BM * BKB + (wn * 64 + r16) * BKB + cofs;
-    const uint32_t fA = (wm * 128 + r16) * BKB + cofs;
-    uint4 P[12];
+    const uint32_t fW = BMT * BKB + (wn * 64 + r16) * BKB + cofs;
+    const uint32_t fA = (wm * (BMT / 2) + r16) * BKB + cofs;
+    constexpr int NF = 4 + AF;
+    uint4 P[NF];
     auto read_tile = [&](int slot) __attribute__((always_inline)) {
         const uint8_t *b = smem + slot * L_STAGE;
 #pragma unroll
-        for (int f = 0; f < 12; ++f) {
+        for (int f = 0; f < NF; ++f) {
             const uint32_t o = (f < 4) ? fW + f * 1024 : fA + (f - 4) * 1024;
             P[f] = *reinterpret_cast<const uint4 *>(b + o);
         }
     };
     auto operands = [&](int s, v4i *u) __attribute__((always_inline)) {
 #pragma unroll
-        for (int f = 0; f < 12; ++f) u[f] = s ? unpack2(P[f].z, P[f].w) : unpack2(P[f].x, P[f].y);
+        for (int f = 0; f < NF; ++f) u[f] = s ? unpack2(P[f].z, P[f].w) : unpack2(P[f].x, P[f].y);
     };
     auto mfma_step = [&](const v4i *u) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
+            for (int j = 0; j < AF; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(u[i], u[4 + j], acc[i][j], 0, 0, 0);
     };
 
-    v4i u0[12], u1[12];
+    v4i u0[NF], u1[NF];
     for (int kt = 0; kt < ktiles; ++kt) {
         // tile kt has landed (from every wave) and every wave is done with
-        // tile kt-1, whose slot the DMA of tile kt+2 now overwrites
-        if (kt + 1 < ktiles) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
-        else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-        if (kt + 2 < ktiles) issue((kt + 2) % L_STAGES, kt + 2);
+        // tile kt-1, whose slot the DMA of tile kt+2 now overwrites; each
+        // wave has AI + 2 DMA instructions per tile in flight
+        if (kt + 1 < ktiles) {
+            if constexpr (BMT == 256) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
+        } else {
+            asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+        }
+        if (kt + 2 < ktiles) issue((kt + 2) % L_STAGES, kbeg + kt + 2);
         read_tile(kt % L_STAGES);
         operands(0, u0);
         __builtin_amdgcn_sched_barrier(0);
@@ -592,7 +635,7 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         operands(1, u1);
         mfma_step(u0);
 #pragma unroll
-        for (int i = 0; i < 24; ++i) {
+        for (int i = 0; i < 2 * NF; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // 1 MFMA
             __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);   // 3 VALU
         }
@@ -602,13 +645,30 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         __builtin_amdgcn_s_setprio(0);
     }
 
+    if constexpr (SPLIT) {      // this slice's exact partial sums: part[split][m][n]
+        int32_t *pz = part + (int64_t)split * M * N;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int nb = n0 + wn * 64 + 16 * i + 4 * cq;         // N % 4 == 0
+#pragma unroll
+            for (int j = 0; j < AF; ++j) {
+                const int m = m0 + wm * (BMT / 2) + 16 * j + r16;
+                if (m < M && nb < N)
+                    *reinterpret_cast<int4 *>(pz + (int64_t)m * N + nb) =
+                        make_int4(acc[i][j][0] >> 8, acc[i][j][1] >> 8, acc[i][j][2] >> 8,
+                                  acc[i][j][3] >> 8);
+            }
+        }
+        return;
+    }
+
     if constexpr (!YOUT) {      // Gram mode: int32 accumulators only
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int nb = n0 + wn * 64 + 16 * i + 4 * cq;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int m = m0 + wm * 128 + 16 * j + r16;
+            for (int j = 0; j < AF; ++j) {
+                const int m = m0 + wm * (BMT / 2) + 16 * j + r16;
                 if (m < M) {
                     int v[4];
 #pragma unroll
@@ -633,23 +693,23 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
     }
 
     // Epilogue.  acc[i][j] lane l, register e holds
-    //   n = n0 + wn*64 + 16 i + 4 (l/16) + e,  m = m0 + wm*128 + 16 j + l%16.
-    // The 256 x 128 tile is assembled in LDS: row m of 256 bytes, 8-byte unit
+    //   n = n0 + wn*64 + 16 i + 4 (l/16) + e,  m = m0 + wm*BMT/2 + 16 j + l%16.
+    // The BMT x 128 tile is assembled in LDS: row m of 256 bytes, 8-byte unit
     // u (4 columns) stored at unit u ^ 2 (m & 15), which keeps both the
     // 8-byte writes and the 16-byte row reads free of bank conflicts.
     __syncthreads();
-    const float *s_sa = reinterpret_cast<const float *>(smem + L_SCALE_OFF);
-    const float *s_sw = s_sa + L_BM;
-    float sam[8];
+    const float *s_sa = reinterpret_cast<const float *>(smem + l_scale_off<BMT>());
+    const float *s_sw = s_sa + BMT;
+    float sam[AF];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) sam[j] = s_sa[wm * 128 + 16 * j + r16];
+    for (int j = 0; j < AF; ++j) sam[j] = s_sa[wm * (BMT / 2) + 16 * j + r16];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int nl = wn * 64 + 16 * i + 4 * cq;
         const float4 swv = *reinterpret_cast<const float4 *>(s_sw + nl);
         const float swe[4] = {swv.x, swv.y, swv.z, swv.w};
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < AF; ++j) {
             int v[4];
             float o[4];
 #pragma unroll
@@ -672,7 +732,7 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
                 }
                 packed = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
             }
-            const int r = wm * 128 + 16 * j + r16;
+            const int r = wm * (BMT / 2) + 16 * j + r16;
             const int u = (nl >> 2) ^ (r16 << 1);
             *reinterpret_cast<uint2 *>(smem + r * 256 + u * 8) = packed;
             if constexpr (ACC) {
@@ -688,12 +748,12 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
     __syncthreads();
     const int rows_left = M - m0, cols_left = N - n0;
     const bool vec16 = ((ldy & 7) == 0) && ((reinterpret_cast<uintptr_t>(y) & 15) == 0);
-    const bool full = vec16 && rows_left >= L_BM && cols_left >= L_BN;
+    const bool full = vec16 && rows_left >= BMT && cols_left >= L_BN;
     const int cch = lane & 15;
     uint16_t *yb = static_cast<uint16_t *>(y) + (int64_t)m0 * ldy + n0 + 8 * cch;
 #pragma unroll 4
-    for (int i = 0; i < 16; ++i) {
-        const int r = 64 * wave + 4 * i + (lane >> 4);
+    for (int i = 0; i < BMT / 16; ++i) {
+        const int r = (BMT / 4) * wave + 4 * i + (lane >> 4);
         const uint4 val = *reinterpret_cast<const uint4 *>(smem + r * 256 + ((cch ^ (r & 15)) << 4));
         uint16_t *dst = yb + (int64_t)r * ldy;
         if (full) {
@@ -893,25 +953,41 @@ __global__ __launch_bounds__(64 * NW) void k_w4a4_gemv(const uint8_t *__restrict
 
 }  // namespace
 
-// The 256 x 128, two-blocks-per-CU kernel serves every shape with M >= 1024
-// and N >= 1024, and batch-1 shapes (M >= 256) wide enough to give it at
-// least 128 tiles (the fused q|k|v and gate|up launches of one image's
-// pruned sequence: measured 1.3-1.4x faster there than the small-M kernel,
-// which keeps the narrow o / down launches and splits their K).
-static bool use_large_tiles(int M, int N) {
-    if (N < 1024 || M < 256) return false;
-    if (M >= 1024) return true;
-    const int64_t tiles = (((int64_t)M + L_BM - 1) / L_BM) * (((int64_t)N + L_BN - 1) / L_BN);
-    return tiles >= 128;
+// Dispatch of the prefill shapes (M > 16):
+//  * M >= 1024 and N >= 1024: the 256 x 128 two-blocks-per-CU kernel;
+//  * M < 1024 and N >= 1024 (one image's pruned sequence): the same kernel
+//    with 128 x 128 tiles; launches with fewer tiles than CUs split K across
+//    work-groups (mid_splits), given the caller's workspace;
+//  * anything narrower: the small-M kernel, split the same way
+//    (small_m_splits).
+static bool use_large_tiles(int M, int N) { return M >= 1024 && N >= 1024; }
+static bool use_mid_tiles(int M, int N) { return M > 16 && M < 1024 && N >= 1024; }
+
+// Mid-tile launches with fewer 128 x 128 tiles than CUs split K into S
+// slices: S = 512 / tiles (two resident work-groups per CU), at most 8, and
+// each slice at least 16 k-tiles of 128: every slice adds M N 4 bytes of
+// partial sums written and read back, which outweighs the extra
+// parallelism below that (measured at M = 384 / 704: o_proj, K = 4096, is
+// fastest at 2 slices; down_proj, K = 11008, at 4-5).  N % 4 == 0
+// (partials are stored 4 at a time).
+static int mid_splits(int M, int N, int K) {
+    if (!use_mid_tiles(M, N) || N % 4 != 0) return 1;
+    const int64_t tiles = (((int64_t)M + 127) / 128) * (((int64_t)N + L_BN - 1) / L_BN);
+    if (tiles >= 256) return 1;
+    const int kt_all = (K / 2 + BKB - 1) / BKB;
+    int S = (int)(512 / tiles);
+    S = std::min(S, 8);
+    S = std::min(S, kt_all / 16);
+    return std::max(S, 1);
 }
 
 // Small-M shapes with fewer 128 x 128 tiles than CUs split K across
 // work-groups (exact int32 partials, summed by the epilogue kernel):
 // S = ceil(256 / tiles), at most 4, each slice at least 4 k-tiles of 256.
-// Not for the decode GEMV or the large-tile kernel, nor when N % 4 != 0
+// Not for the decode GEMV or the tile kernels above, nor when N % 4 != 0
 // (the epilogue writes 4 outputs per thread).
 static int small_m_splits(int M, int N, int K) {
-    if (M <= 16 || use_large_tiles(M, N) || N % 4 != 0) return 1;
+    if (M <= 16 || use_large_tiles(M, N) || use_mid_tiles(M, N) || N % 4 != 0) return 1;
     const int64_t tiles = (((int64_t)M + BM - 1) / BM) * (((int64_t)N + BN - 1) / BN);
     const int kt_all = (K / 2 + KS_ROW - 1) / KS_ROW;
     if (tiles >= 256) return 1;
@@ -922,7 +998,7 @@ static int small_m_splits(int M, int N, int K) {
 }
 
 size_t gemm_workspace_bytes(int M, int N, int K) {
-    const int S = small_m_splits(M, N, K);
+    const int S = use_mid_tiles(M, N) ? mid_splits(M, N, K) : small_m_splits(M, N, K);
     return S > 1 ? (size_t)S * M * N * 4 : 0;
 }
 
@@ -954,26 +1030,51 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
         P4Q_GEMV(7, 16, 1)
 #undef P4Q_GEMV
     }
-    if (use_large_tiles(M, N)) {
-        const int tiles_m = (M + L_BM - 1) / L_BM, tiles_n = (N + L_BN - 1) / L_BN;
-        const dim3 grid(tiles_m * tiles_n);
+    const bool ws_ok = ws && ((uintptr_t)ws & 15) == 0 && ws_bytes >= gemm_workspace_bytes(M, N, K);
+    const unsigned eb = (unsigned)(((int64_t)M * N / 4 + 255) / 256);   // split-K epilogue blocks
+    if (use_large_tiles(M, N) || use_mid_tiles(M, N)) {
+        const bool large = use_large_tiles(M, N);
+        const int bm = large ? L_BM : 128;
+        const int tiles_m = (M + bm - 1) / bm, tiles_n = (N + L_BN - 1) / L_BN;
+        const int T = tiles_m * tiles_n;
+        const int S = large ? 1 : mid_splits(M, N, K);
+        if (S > 1 && ws_ok) {
+            const int kt_all = (K / 2 + BKB - 1) / BKB, kps = (kt_all + S - 1) / S;
+            const int Sr = (kt_all + kps - 1) / kps;          // every slice non-empty
+            int32_t *part = static_cast<int32_t *>(ws);
+            hipLaunchKernelGGL((k_w4a4_gemm_2cu<128, false, false, true, true>), dim3(T, Sr),
+                               dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy, acc_out,
+                               tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0, kps, part);
+            if (bf16)
+                hipLaunchKernelGGL(k_splitk_epilogue<true>, dim3(eb), dim3(256), 0, stream, part, Sr,
+                                   M, N, sa, sw, y, ldy, acc_out);
+            else
+                hipLaunchKernelGGL(k_splitk_epilogue<false>, dim3(eb), dim3(256), 0, stream, part, Sr,
+                                   M, N, sa, sw, y, ldy, acc_out);
+            return hipGetLastError();
+        }
         auto go = [&](auto kern) {
-            hipLaunchKernelGGL(kern, grid, dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy,
-                               acc_out, tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0);
+            hipLaunchKernelGGL(kern, dim3(T), dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy,
+                               acc_out, tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0, 0,
+                               (int32_t *)nullptr);
             return hipGetLastError();
         };
-        if (bf16)
-            return acc_out ? go(k_w4a4_gemm_2cu<true, true, true>) : go(k_w4a4_gemm_2cu<true, false, true>);
-        return acc_out ? go(k_w4a4_gemm_2cu<false, true, true>) : go(k_w4a4_gemm_2cu<false, false, true>);
+#define P4Q_TILES(BMT)                                                                        \
+    if (bf16) return acc_out ? go(k_w4a4_gemm_2cu<BMT, true, true, true, false>)               \
+                             : go(k_w4a4_gemm_2cu<BMT, true, false, true, false>);            \
+    return acc_out ? go(k_w4a4_gemm_2cu<BMT, false, true, true, false>)                        \
+                   : go(k_w4a4_gemm_2cu<BMT, false, false, true, false>);
+        if (large) { P4Q_TILES(256) }
+        P4Q_TILES(128)
+#undef P4Q_TILES
     }
     const dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
     const int S = small_m_splits(M, N, K);
-    if (S > 1 && ws && ((uintptr_t)ws & 15) == 0 && ws_bytes >= gemm_workspace_bytes(M, N, K)) {
+    if (S > 1 && ws_ok) {
         const int kt_all = (K / 2 + KS_ROW - 1) / KS_ROW, kps = (kt_all + S - 1) / S;
         int32_t *part = static_cast<int32_t *>(ws);
         const dim3 gs(grid.x, grid.y, (kt_all + kps - 1) / kps);
         const int Sr = (int)gs.z;
-        const unsigned eb = (unsigned)(((int64_t)M * N / 4 + 255) / 256);
         if (bf16) {
             hipLaunchKernelGGL((k_w4a4_gemm_ks<true, true>), gs, dim3(KS_THREADS), 0, stream, a, sa,
                                w, sw, M, N, K / 2, y, ldy, acc_out, kps, part);
@@ -1005,9 +1106,10 @@ hipError_t launch_code_gram(int B, int n, int k, const uint8_t *codes, int32_t *
         const int tiles_m = (n + L_BM - 1) / L_BM, tiles_n = (n + L_BN - 1) / L_BN;
         int upper = 0;                              // tiles with tn >= 2 tm
         for (int tm = 0; tm < tiles_m; ++tm) upper += std::max(0, tiles_n - 2 * tm);
-        hipLaunchKernelGGL((k_w4a4_gemm_2cu<true, true, false>), dim3(upper, B), dim3(256), 0,
-                           stream, codes, nullptr, codes, nullptr, n, n, kb, nullptr, (int64_t)n, G,
-                           upper, tiles_n, (int64_t)n * kb, (int64_t)n * kb, (int64_t)n * n);
+        hipLaunchKernelGGL((k_w4a4_gemm_2cu<256, true, true, false, false>), dim3(upper, B),
+                           dim3(256), 0, stream, codes, nullptr, codes, nullptr, n, n, kb, nullptr,
+                           (int64_t)n, G, upper, tiles_n, (int64_t)n * kb, (int64_t)n * kb,
+                           (int64_t)n * n, 0, (int32_t *)nullptr);
         return hipGetLastError();
     }
     const dim3 grid((n + BN - 1) / BN, (n + BM - 1) / BM);

@@ -65,9 +65,32 @@ def test_shapes(shape, out_dtype):
 @pytest.mark.parametrize("shape", [(1030, 1100, 512), (1024, 1024, 4128), (1500, 2100, 96),
                                    (2304, 1280, 11008), (1024, 4096, 32)])
 def test_large_tile_shapes(shape):
-    """Shapes served by the 256 x 256 kernel, with ragged M, N and K tails."""
+    """Shapes served by the 256 x 128 two-blocks-per-CU kernel, with ragged
+    M, N and K tails."""
     M, N, K = shape
     check_full(*codes_for(M, N, K, M + N + K), "bf16")
+
+
+@pytest.mark.parametrize("shape", [(17, 1024, 32), (130, 1100, 288), (517, 1030, 4128),
+                                   (1000, 2100, 96), (300, 1024, 8224), (45, 1040, 6016)])
+def test_mid_tile_shapes(shape):
+    """Shapes served by the 128 x 128 tiles of the same kernel (16 < M <
+    1024, N >= 1024), ragged in M, N and K: unsplit (no workspace) and, where
+    the shape has few tiles, with K split across work-groups (the last
+    slice holding the ragged k-tile), each with and without the int32
+    store."""
+    M, N, K = shape
+    ap, sa, wp, sw = codes_for(M, N, K, M + 3 * N + K)
+    check_full(ap, sa, wp, sw, "fp16")
+    nws = p4q.lib().p4q_w4a4_linear_workspace_bytes(M, N, K)
+    if nws:
+        racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
+        ws = p4q.w4a4_linear_workspace(M, N, K, torch.device("cuda:0"))
+        for with_acc in (True, False):
+            y, acc = run_gpu(ap, sa, wp, sw, "bf16", with_acc=with_acc, workspace=ws)
+            if with_acc:
+                assert (m := first_mismatch(acc, racc.astype(np.int32))) is None, m
+            assert (m := first_mismatch(bits(y), bits(ry))) is None, (with_acc, m)
 
 
 @pytest.mark.parametrize("extreme", [-8, 7])
