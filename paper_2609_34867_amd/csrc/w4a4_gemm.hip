@@ -395,9 +395,14 @@ __global__ __launch_bounds__(256) void k_splitk_epilogue(const int32_t *__restri
 //    narrow batch-1 launches, whose tiles alone would leave most CUs idle.
 // ---------------------------------------------------------------------------
 constexpr int L_BM = 256, L_BN = 128;
-constexpr int L_STAGES = 3;
+// Ring depth: 3 stages (24 KB for 256-row tiles, 16 KB for 128-row tiles,
+// so that three 128-row blocks fit on a CU).  Measured at the batch-1
+// shapes: a fourth stage (two blocks per CU) or a fifth (one) made the
+// launches 10-50% slower; the kernel is written for any depth up to 5.
+constexpr int kMidStages = 3;
+template <int BMT> constexpr int l_stages() { return BMT == 256 ? 3 : kMidStages; }
 template <int BMT> constexpr int l_stage() { return (BMT + L_BN) * BKB; }   // packed codes
-template <int BMT> constexpr int l_scale_off() { return L_STAGES * l_stage<BMT>(); }
+template <int BMT> constexpr int l_scale_off() { return l_stages<BMT>() * l_stage<BMT>(); }
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 
@@ -574,8 +579,10 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
             else dma4(dSw, (uint32_t)(64 * (wave - 2) + lane) * 4u, sbase + 512 + (wave_u - 2) * 256);
         }
     }
-    issue(0, kbeg);
-    if (ktiles > 1) issue(1, kbeg + 1);
+    constexpr int NST = l_stages<BMT>();
+#pragma unroll
+    for (int q = 0; q < NST - 1; ++q)
+        if (q < ktiles) issue(q, kbeg + q);
 
     v4i acc[4][AF];
 #pragma unroll
@@ -616,16 +623,22 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
     v4i u0[NF], u1[NF];
     for (int kt = 0; kt < ktiles; ++kt) {
         // tile kt has landed (from every wave) and every wave is done with
-        // tile kt-1, whose slot the DMA of tile kt+2 now overwrites; each
-        // wave has AI + 2 DMA instructions per tile in flight
-        if (kt + 1 < ktiles) {
-            if constexpr (BMT == 256) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
-            else asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
+        // tile kt-1, whose slot the DMA of tile kt+NST-1 now overwrites.  Each
+        // wave issues AI + 2 DMA instructions per tile; the tiles after kt
+        // already issued may stay in flight.
+        const int ahead = min(NST - 2, ktiles - 1 - kt);
+        if constexpr (BMT == 256) {
+            if (ahead >= 1) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
         } else {
-            asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+            static_assert(l_stages<BMT>() <= 5, "wait counts below cover at most 3 tiles ahead");
+            if (ahead >= 3) asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
+            else if (ahead == 2) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+            else if (ahead == 1) asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
         }
-        if (kt + 2 < ktiles) issue((kt + 2) % L_STAGES, kbeg + kt + 2);
-        read_tile(kt % L_STAGES);
+        if (kt + NST - 1 < ktiles) issue((kt + NST - 1) % NST, kbeg + kt + NST - 1);
+        read_tile(kt % NST);
         operands(0, u0);
         __builtin_amdgcn_sched_barrier(0);
         // raised issue priority while this wave streams MFMAs, so the SIMD's
