@@ -476,8 +476,15 @@ __device__ __forceinline__ void gram_tile_coords(int wg, int total, int tiles_n,
     tn = 2 * tm + logical;
 }
 
+// Two adjacent packed words: the low nibbles of both move up by one 64-bit
+// shift (bits crossing from w0 into w1 land in w1's low nibbles, which the
+// mask clears), so the pair takes 5 VALU instructions instead of 6.
 __device__ __forceinline__ v4i unpack2(uint32_t w0, uint32_t w1) {
-    return v4i{(int)nib_lo(w0), (int)nib_hi(w0), (int)nib_lo(w1), (int)nib_hi(w1)};
+    const uint64_t q0 = ((uint64_t)w1 << 32) | w0;
+    uint64_t q;
+    asm("v_lshlrev_b64 %0, 4, %1" : "=v"(q) : "v"(q0));
+    return v4i{(int)((uint32_t)q & 0xF0F0F0F0u), (int)nib_hi(w0),
+               (int)((uint32_t)(q >> 32) & 0xF0F0F0F0u), (int)nib_hi(w1)};
 }
 
 // YOUT = false is the Gram mode (A == W, M == N): only the int32
