@@ -66,10 +66,20 @@ __device__ __forceinline__ uint32_t absmax_chunk(uint32_t m, uint4 v) {
     return absmax2(m, v.w);
 }
 
+// Maximum over the 64 lanes, wave-uniform result.  DPP moves within each
+// row of 16 lanes (quad swaps, half-row and row mirrors) leave every lane
+// holding its row's maximum; the four rows meet through lane reads.  No LDS
+// round trip (a shuffle chain costs six).  Every lane must be active.
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
-    return v;
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));   // quad [1,0,3,2]
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));   // quad [2,3,0,1]
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));  // row_half_mirror
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));  // row_mirror
+    const uint32_t a = max((uint32_t)__builtin_amdgcn_readlane((int)v, 0),
+                           (uint32_t)__builtin_amdgcn_readlane((int)v, 16));
+    const uint32_t b = max((uint32_t)__builtin_amdgcn_readlane((int)v, 32),
+                           (uint32_t)__builtin_amdgcn_readlane((int)v, 48));
+    return max(a, b);
 }
 
 // s = fl32(fl32(c*a)/7); both operations correctly rounded (no fast-math)

@@ -96,26 +96,29 @@ constexpr int kMaxJ = 8;
 
 // Butterfly reduce-scatter of 8 per-lane partial sums: afterwards lane l holds
 // the wavefront total of value ((l>>5)&1)*4 + ((l>>4)&1)*2 + ((l>>3)&1), i.e.
-// value v sits in lanes 8v .. 8v+7.  10 shuffles instead of 48.
+// value v sits in lanes 8v .. 8v+7.  The halves of the wavefront (32 lanes)
+// and of each half (16 lanes) trade values with permlane swaps; within a row
+// of 16, DPP mirrors and quad swaps finish the sums.  No LDS round trip.
 __device__ __forceinline__ int reduce8(const int *v, int lane) {
-    const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+    const bool b3 = lane & 8;
     int w[4], x[2];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int send = b5 ? v[k] : v[k + 4];
-        const int keep = b5 ? v[k + 4] : v[k];
-        w[k] = keep + __shfl_xor(send, 32);
+    for (int k = 0; k < 4; ++k) {          // lanes < 32: value k, lanes >= 32: value k + 4
+        const auto p = __builtin_amdgcn_permlane32_swap(v[k], v[k + 4], false, false);
+        w[k] = p[0] + p[1];
     }
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
-        const int send = b4 ? w[k] : w[k + 2];
-        const int keep = b4 ? w[k + 2] : w[k];
-        x[k] = keep + __shfl_xor(send, 16);
+    for (int k = 0; k < 2; ++k) {          // 16-lane rows 0, 2: w[k]; rows 1, 3: w[k + 2]
+        const auto p = __builtin_amdgcn_permlane16_swap(w[k], w[k + 2], false, false);
+        x[k] = p[0] + p[1];
     }
-    int y = (b3 ? x[1] : x[0]) + __shfl_xor(b3 ? x[0] : x[1], 8);
-    y += __shfl_xor(y, 4);
-    y += __shfl_xor(y, 2);
-    y += __shfl_xor(y, 1);
+    // lane i of a row keeps x[b3] and takes the partner's from lane 15 - i
+    // (which has the other b3); the 8 lanes sharing b3 then cover the row
+    int y = (b3 ? x[1] : x[0]) +
+            __builtin_amdgcn_update_dpp(0, b3 ? x[0] : x[1], 0x140, 0xF, 0xF, false);  // row_mirror
+    y += __builtin_amdgcn_update_dpp(0, y, 0x141, 0xF, 0xF, false);                    // row_half_mirror
+    y += __builtin_amdgcn_update_dpp(0, y, 0x4E, 0xF, 0xF, false);                     // quad [2,3,0,1]
+    y += __builtin_amdgcn_update_dpp(0, y, 0xB1, 0xF, 0xF, false);                     // quad [1,0,3,2]
     return y;
 }
 
@@ -216,10 +219,18 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
         if (s != 0.0f) {
             const bool tiny = !(s >= kTinyScale);
             const float rc = tiny ? 0.0f : 1.0f / s;
+            // Bracketed fast path: with r = fl32(1/s), x r(1 - 2^-20) and
+            // x r(1 + 2^-20) (products rounded once, inside the fma) enclose
+            // fl32(x/s), since r and fl32(x/s) each err by at most 2^-24
+            // relative.  rne is monotone, so where the two bracket ends round
+            // to the same integer, so does fl32(x/s); where they differ a
+            // half-integer lies inside and the exact path decides.  Two fmas
+            // and one bitwise merge per value.
+            const float rhi = __fmul_rn(rc, 1.0f + 0x1p-20f), rlo = __fmul_rn(rc, 1.0f - 0x1p-20f);
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 uint32_t w[8];
-                float fm = 0.0f;      // largest |x r - rne(x r)| of the chunk
+                uint32_t dif = 0u;    // nonzero: a bracket of this chunk straddles a boundary
                 if (!tiny) {
                     const uint32_t x4[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
 #pragma unroll
@@ -227,9 +238,14 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
 #pragma unroll
                         for (int h = 0; h < 2; ++h) {
                             const float x = h ? hi_f32<BF16>(x4[i]) : lo_f32<BF16>(x4[i]);
-                            float tq = __builtin_fmaf(x, rc, kRneMagic);
-                            const float qq = tq - kRneMagic;
-                            fm = __builtin_fmaxf(fm, __builtin_fabsf(__builtin_fmaf(x, rc, -qq)));
+                            float tq = __builtin_fmaf(x, rhi, kRneMagic);
+                            const float tl = __builtin_fmaf(x, rlo, kRneMagic);
+                            // (as asm: left to itself the compiler turns the
+                            // merge into a compare and select per value)
+                            uint32_t tlb = __float_as_uint(tl);
+                            asm("v_xor_b32 %1, %1, %2\n\tv_or_b32 %0, %0, %1"
+                                : "+v"(dif), "+v"(tlb)
+                                : "v"(__float_as_uint(tq)));
                             if constexpr (!CLIP1)
                                 tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
                             w[2 * i + h] = __float_as_uint(tq);
@@ -237,10 +253,10 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
                     }
                 }
                 // wave-uniform and rare: some lane holds a value of this chunk
-                // within 2^-19 of a rounding boundary (exact fp16 ratios such as
-                // x = a/2 land on ties), or the scale is tiny.  Only this chunk
-                // is recomputed by exact division.
-                if (tiny || __any(fm > kNearHalf)) {
+                // next to a rounding boundary (exact fp16 ratios such as x = a/2
+                // land on ties), or the scale is tiny.  Only this chunk is
+                // recomputed by exact division.
+                if (tiny || __any(dif != 0u)) {
                     uint4 vc = v[c];
                     // opaque copy: keeps the exact path's fp16 -> fp32 conversions
                     // from being hoisted into (and paid on) the fast path
