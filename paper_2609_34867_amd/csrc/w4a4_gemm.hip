@@ -793,6 +793,275 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
 
 
 // ---------------------------------------------------------------------------
+// Persistent-tile form of the kernel above (y output, no split): a grid of at
+// most two blocks per CU, each walking a list of tiles, with one DMA ring
+// running on across its tile boundaries.
+//  * Tile list: the work-groups of XCD x (ids x, x + 8, ...) share that XCD's
+//    contiguous range of M-grouped tiles (as in xcd_logical); the i-th of them
+//    takes tiles i, i + nb, i + 2 nb, ... of the range (nb = its work-groups),
+//    so at any time an XCD works on a window of consecutive tiles.
+//  * The ring is indexed by the block's global k-tile count g (tile g / KT,
+//    k-tile g % KT): the DMA of the next tile's first stages (and its scales,
+//    into one of three scale buffers) is issued during the current tile's
+//    last k-tiles, so a new tile starts with its operands in LDS instead of
+//    a full memory round trip, and no block is relaunched per tile.
+//  * The epilogue stores straight from registers (no LDS, no barrier): lane
+//    l holds 4 consecutive columns of one row per fragment, 8 bytes; the 4
+//    fragments along n complete each 128-byte line of a row before the next
+//    store group, which the L2 merges.
+//  * Waits: loads (the DMA) complete in order among themselves, so waiting
+//    until at most 6 instructions (one stage of this wave) are outstanding
+//    guarantees every older stage has landed; epilogue stores in between
+//    can only make such a wait longer, never shorter.
+// ---------------------------------------------------------------------------
+constexpr int kScaleBufs = 3;
+
+template <bool BF16OUT, bool ACC>
+__global__ __launch_bounds__(256, 2) void k_w4a4_gemm_pt(const uint8_t *__restrict__ A,
+                                                         const float *__restrict__ sa,
+                                                         const uint8_t *__restrict__ W,
+                                                         const float *__restrict__ sw, int M,
+                                                         int N, int Kb, void *__restrict__ y,
+                                                         int64_t ldy,
+                                                         int32_t *__restrict__ acc_out,
+                                                         int tiles_m, int tiles_n) {
+    constexpr int BMT = L_BM, NST = 3, AI = BMT / 64, AF = BMT / 32;
+    constexpr int L_STAGE = l_stage<BMT>();
+    constexpr int SCALE_OFF = NST * L_STAGE;
+    constexpr int SCALE_BUF = (BMT + L_BN) * 4;
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[SCALE_OFF + kScaleBufs * SCALE_BUF];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+
+    // this block's tiles: start + i0 + k nb, k < nt
+    const int T = tiles_m * tiles_n;
+    const int xcd = blockIdx.x % kXcds, i0 = blockIdx.x / kXcds;
+    const int nb = ((int)gridDim.x - xcd + kXcds - 1) / kXcds;
+    const int q = T / kXcds, rr = T % kXcds;
+    const int start = (xcd < rr) ? xcd * (q + 1) : rr * (q + 1) + (xcd - rr) * q;
+    const int len = q + (xcd < rr ? 1 : 0);
+    const int nt = (i0 < len) ? (len - i0 + nb - 1) / nb : 0;
+    const int KT = (Kb + BKB - 1) / BKB;
+    const int g_end = nt * KT;
+    auto tile_origin = [&](int k, int &m0, int &n0) __attribute__((always_inline)) {
+        int tm, tn;
+        grouped_tile(start + i0 + k * nb, tiles_m, tiles_n, tm, tn);
+        m0 = tm * BMT;
+        n0 = tn * L_BN;
+    };
+
+    // DMA placement: as in k_w4a4_gemm_2cu (16 rows of 64 bytes per 1 KB
+    // instruction, k-chunk index XORed with (row >> 1) & 3)
+    uint32_t voffA[AI], voffW[2];
+    int kcA[AI], kcW[2];
+#pragma unroll
+    for (int i = 0; i < AI; ++i) {
+        const int row = (BMT / 4) * wave + 16 * i + (lane >> 2);
+        kcA[i] = ((lane & 3) ^ ((row >> 1) & 3)) * 16;
+        voffA[i] = (uint32_t)(row * Kb + kcA[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int row = 32 * wave + 16 * i + (lane >> 2);
+        kcW[i] = ((lane & 3) ^ ((row >> 1) & 3)) * 16;
+        voffW[i] = (uint32_t)(row * Kb + kcW[i]);
+    }
+    const uint32_t ldsA = lds_addr(smem) + wave_u * (BMT / 4) * BKB;
+    const uint32_t ldsW = lds_addr(smem) + BMT * BKB + wave_u * 2048;
+    const uint32_t sbase = lds_addr(smem) + SCALE_OFF;
+
+    // issue side: the tile whose stages are being issued, its descriptors
+    int iss_k = -1, iss_kt = 0;
+    v4i dA, dW;
+    auto issue = [&](int g) __attribute__((always_inline)) {
+        if (iss_kt == 0) {                      // first stage of a new tile
+            ++iss_k;
+            int m0, n0;
+            tile_origin(iss_k, m0, n0);
+            dA = buffer_desc(A + (int64_t)m0 * Kb, (uint32_t)(min(M - m0, BMT) * Kb));
+            dW = buffer_desc(W + (int64_t)n0 * Kb, (uint32_t)(min(N - n0, L_BN) * Kb));
+            // the tile's scales (zeros past M / N) into scale buffer iss_k % 3
+            const v4i dSa = buffer_desc(sa + m0, (uint32_t)(min(M - m0, BMT) * 4));
+            const v4i dSw = buffer_desc(sw + n0, (uint32_t)(min(N - n0, L_BN) * 4));
+            const uint32_t sb = sbase + (uint32_t)((iss_k % kScaleBufs) * SCALE_BUF);
+            dma4(dSa, (uint32_t)(64 * wave + lane) * 4u, sb + wave_u * 256);
+            if (wave_u < 2) dma4(dSw, (uint32_t)(64 * wave + lane) * 4u, sb + BMT * 4 + wave_u * 256);
+        }
+        const int slot = g % NST, kt = iss_kt;
+#pragma unroll
+        for (int i = 0; i < AI; ++i) {
+            const uint32_t o = (kt * BKB + kcA[i] < Kb) ? voffA[i] + (uint32_t)(kt * BKB) : 0x80000000u;
+            dma16(dA, o, ldsA + slot * L_STAGE + i * 1024);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const uint32_t o = (kt * BKB + kcW[i] < Kb) ? voffW[i] + (uint32_t)(kt * BKB) : 0x80000000u;
+            dma16(dW, o, ldsW + slot * L_STAGE + i * 1024);
+        }
+        if (++iss_kt == KT) iss_kt = 0;
+    };
+#pragma unroll
+    for (int g = 0; g < NST - 1; ++g)
+        if (g < g_end) issue(g);
+
+    v4i acc[4][AF];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < AF; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+
+    const int r16 = lane & 15, cq = lane >> 4;
+    const uint32_t cofs = (uint32_t)((cq ^ ((r16 >> 1) & 3)) << 4);
+    const uint32_t fW = BMT * BKB + (wn * 64 + r16) * BKB + cofs;
+    const uint32_t fA = (wm * (BMT / 2) + r16) * BKB + cofs;
+    constexpr int NF = 4 + AF;
+    uint4 P[NF];
+    auto read_tile = [&](int slot) __attribute__((always_inline)) {
+        const uint8_t *b = smem + slot * L_STAGE;
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            const uint32_t o = (f < 4) ? fW + f * 1024 : fA + (f - 4) * 1024;
+            P[f] = *reinterpret_cast<const uint4 *>(b + o);
+        }
+    };
+    auto operands = [&](int s, v4i *u) __attribute__((always_inline)) {
+#pragma unroll
+        for (int f = 0; f < NF; ++f) u[f] = s ? unpack2(P[f].z, P[f].w) : unpack2(P[f].x, P[f].y);
+    };
+    auto mfma_step = [&](const v4i *u) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < AF; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(u[i], u[4 + j], acc[i][j], 0, 0, 0);
+    };
+    const bool vec16 = ((ldy & 7) == 0) && ((reinterpret_cast<uintptr_t>(y) & 15) == 0);
+
+    v4i u0[NF], u1[NF];
+    int ck = 0, ckt = 0;                        // compute side: tile, k-tile
+    for (int g = 0; g < g_end; ++g) {
+        // stage g has landed (every wave) and every wave is done with stage
+        // g-1, whose slot the DMA of stage g+NST-1 now overwrites
+        if (g + 1 < g_end) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
+        else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+        if (g + NST - 1 < g_end) issue(g + NST - 1);
+        read_tile(g % NST);
+        operands(0, u0);
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);
+        operands(1, u1);
+        mfma_step(u0);
+#pragma unroll
+        for (int i = 0; i < 2 * NF; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // 1 MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);   // 3 VALU
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_step(u1);
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(0);
+
+        if (++ckt < KT) continue;
+        // tile ck complete: epilogue from registers, then the next tile
+        ckt = 0;
+        int m0, n0;
+        tile_origin(ck, m0, n0);
+        const float *s_sa = reinterpret_cast<const float *>(smem + SCALE_OFF + (ck % kScaleBufs) * SCALE_BUF);
+        const float *s_sw = s_sa + BMT;
+        // Staging: the ring slot this last k-tile was read from (every wave
+        // has read it after the barrier below; the next tile's two stages sit
+        // in the other slots).  Four passes of 64 rows (16 KB): in pass p
+        // every wave writes its fragments j = 2p, 2p + 1 (rows 32p .. 32p+31
+        // of its half of the tile; 8-byte units XOR-swizzled by the row, as
+        // in k_w4a4_gemm_2cu), then all waves store full 256-byte row
+        // segments, one 16-byte store per lane.  Staging row rs < 32 is tile
+        // row 32p + rs, rs >= 32 is row 128 + 32p + (rs - 32).
+        // lane-derived values made opaque here, so that the epilogue's
+        // address arithmetic stays in the epilogue instead of being hoisted
+        // out of the k-loop into registers the loop needs
+        int r16e = r16, cqe = cq, te = t;
+        asm volatile("" : "+v"(r16e), "+v"(cqe), "+v"(te));
+        uint8_t *stg = smem + (g % NST) * L_STAGE;
+        const int rows_left = M - m0, cols_left = N - n0;
+        const bool full = vec16 && rows_left >= BMT && cols_left >= L_BN;
+        const int cch = te & 15;
+        uint16_t *yb = static_cast<uint16_t *>(y) + (int64_t)m0 * ldy + n0 + 8 * cch;
+#pragma unroll
+        for (int pass = 0; pass < AF / 2; ++pass) {
+            __syncthreads();                    // the slot (or the previous pass) is free
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj) {
+                const int j = 2 * pass + jj;
+                const int rl = wm * (BMT / 2) + 16 * j + r16e;
+                const float sam = s_sa[rl];
+                const int rs = 32 * wm + 16 * jj + r16e;           // staging row
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int nl = wn * 64 + 16 * i + 4 * cqe;
+                    const float4 swv = *reinterpret_cast<const float4 *>(s_sw + nl);
+                    const float swe[4] = {swv.x, swv.y, swv.z, swv.w};
+                    int v[4];
+                    float o[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        v[e] = acc[i][j][e] >> 8;
+                        o[e] = __fmul_rn(__fmul_rn((float)v[e], sam), swe[e]);
+                    }
+                    uint2 packed;
+                    if constexpr (BF16OUT) {
+                        packed.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{o[0], o[1]}, bf2));
+                        packed.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{o[2], o[3]}, bf2));
+                    } else {
+                        uint32_t h[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            float ov = o[e];
+                            asm volatile("" : "+v"(ov));
+                            h[e] = __builtin_bit_cast(uint16_t, (_Float16)ov);
+                        }
+                        packed = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                    }
+                    const int u = (nl >> 2) ^ (r16e << 1);
+                    *reinterpret_cast<uint2 *>(stg + rs * 256 + u * 8) = packed;
+                    if constexpr (ACC) {
+                        const int m = m0 + rl, nb0 = n0 + nl;
+                        if (m < M) {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                if (nb0 + e < N) acc_out[(int64_t)m * N + nb0 + e] = v[e];
+                        }
+                    }
+                    acc[i][j] = v4i{0, 0, 0, 0};
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const int rs = 16 * s4 + (te >> 4);
+                const int r = (rs < 32) ? 32 * pass + rs : BMT / 2 + 32 * pass + (rs - 32);
+                const uint4 val = *reinterpret_cast<const uint4 *>(stg + rs * 256 + ((cch ^ (rs & 15)) << 4));
+                uint16_t *dst = yb + (int64_t)r * ldy;
+                if (full) {
+                    *reinterpret_cast<uint4 *>(dst) = val;
+                } else if (r < rows_left) {
+                    if (vec16 && 8 * cch + 8 <= cols_left) {
+                        *reinterpret_cast<uint4 *>(dst) = val;
+                    } else {
+                        const uint32_t w4[4] = {val.x, val.y, val.z, val.w};
+#pragma unroll
+                        for (int jj = 0; jj < 8; ++jj)
+                            if (8 * cch + jj < cols_left) dst[jj] = (uint16_t)(w4[jj >> 1] >> (16 * (jj & 1)));
+                    }
+                }
+            }
+        }
+        ++ck;
+    }
+}
+
+
+// ---------------------------------------------------------------------------
 // Decode-shaped kernel (M <= 16): the weights are streamed from HBM once, so
 // the kernel is bound by HBM bandwidth and by how many bytes are in flight.
 // A work-group of NW wavefronts (8, or 16 for long rows) computes 16 output
@@ -974,7 +1243,8 @@ __global__ __launch_bounds__(64 * NW) void k_w4a4_gemv(const uint8_t *__restrict
 }  // namespace
 
 // Dispatch of the prefill shapes (M > 16):
-//  * M >= 1024 and N >= 1024: the 256 x 128 two-blocks-per-CU kernel;
+//  * M >= 1024 and N >= 1024: 256 x 128 tiles, two blocks per CU, persistent
+//    over their tiles (k_w4a4_gemm_pt);
 //  * M < 1024 and N >= 1024 (one image's pruned sequence): the same kernel
 //    with 128 x 128 tiles; launches with fewer tiles than CUs split K across
 //    work-groups (mid_splits), given the caller's workspace;
@@ -1084,7 +1354,17 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
                              : go(k_w4a4_gemm_2cu<BMT, true, false, true, false>);            \
     return acc_out ? go(k_w4a4_gemm_2cu<BMT, false, true, true, false>)                        \
                    : go(k_w4a4_gemm_2cu<BMT, false, false, true, false>);
-        if (large) { P4Q_TILES(256) }
+        if (large) {
+            // persistent tiles: at most two resident blocks per CU
+            const unsigned grid = (unsigned)std::min<int64_t>(T, 2LL * device_cus());
+            auto gp = [&](auto kern) {
+                hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2,
+                                   y, ldy, acc_out, tiles_m, tiles_n);
+                return hipGetLastError();
+            };
+            if (bf16) return acc_out ? gp(k_w4a4_gemm_pt<true, true>) : gp(k_w4a4_gemm_pt<true, false>);
+            return acc_out ? gp(k_w4a4_gemm_pt<false, true>) : gp(k_w4a4_gemm_pt<false, false>);
+        }
         P4Q_TILES(128)
 #undef P4Q_TILES
     }
