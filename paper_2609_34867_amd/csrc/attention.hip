@@ -26,6 +26,8 @@
 // 8(r/4) + 4(l/32) + r%4, column l%32.
 #include "p4q_internal.h"
 
+#include <type_traits>
+
 namespace p4q {
 namespace {
 
@@ -146,71 +148,101 @@ __global__ __launch_bounds__(256, 2) void k_attention(const uint16_t *__restrict
 
     const int kend = CAUSAL ? min(L, q0 + kQB) : L;
     const int ntiles = (kend + kKT - 1) / kKT;
-    // one tile of keys from LDS buffer kt & 1
-    auto tile = [&](int kt) __attribute__((always_inline)) {
+    // lanes l and l ^ 32 hold the two halves of a query's keys: their
+    // combination through a permlane swap (no LDS round trip)
+    auto xmax32 = [](float x) __attribute__((always_inline)) {
+        const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        return __builtin_fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+    };
+    auto xsum32 = [](float x) __attribute__((always_inline)) {
+        const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+    };
+    // One tile of 64 keys from LDS buffer kt & 1, both 32-key halves at once:
+    // their S^T products are two independent MFMA chains, and one softmax
+    // update (one max, one rescale decision, one sum) covers the 64 keys.
+    // TWO = false: only the first half has keys at or before this
+    // wavefront's last query (causal diagonal); the second is skipped (its
+    // weights would all be 0, leaving m, lsum and O unchanged).
+    auto tile_keys = [&](int kt, auto two_c) __attribute__((always_inline)) {
+        constexpr bool TWO = decltype(two_c)::value;
+        constexpr int NH = TWO ? 2 : 1;
         const uint8_t *sK = smem + (kt & 1) * (kKBytes + kVBytes);
         const uint8_t *sV = sK + kKBytes;
+        const int k0 = kt * kKT;
+        // S^T = K Q^T: lane holds query c32, keys k0 + 32 hf + 8(r/4) + 4g + r%4
+        v16f st[NH];
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {                    // 32-key halves
-            const int k0 = kt * kKT + 32 * hf;
-            // a half past this wavefront's last query holds only masked
-            // keys (weight 0): skipping it leaves m, lsum and O unchanged
-            if (CAUSAL && k0 > qw0 + kQW - 1) continue;
-            // S^T = K Q^T: lane holds query c32, keys k0 + 8(r/4) + 4g + r%4
-            v16f st = v16f{};
+        for (int hf = 0; hf < NH; ++hf) st[hf] = v16f{};
 #pragma unroll
-            for (int s = 0; s < 8; ++s) {
+        for (int s = 0; s < 8; ++s)
+#pragma unroll
+            for (int hf = 0; hf < NH; ++hf) {
                 const uint4 kf = *reinterpret_cast<const uint4 *>(sK + (32 * hf + c32) * kKStride + 32 * s + 16 * g);
-                st = mfma<BF16>(kf, qf[s], st);
+                st[hf] = mfma<BF16>(kf, qf[s], st[hf]);
             }
-            // mask (only where the half reaches the diagonal or the end)
-            const bool need_mask = (k0 + 32 > L) || (CAUSAL && k0 + 31 > qw0);
-            float tmax = -__builtin_huge_valf();
+        // mask (only where the tile reaches the diagonal or the end)
+        float tmax = -__builtin_huge_valf();
+#pragma unroll
+        for (int hf = 0; hf < NH; ++hf) {
+            const int kh = k0 + 32 * hf;
+            const bool need_mask = (kh + 32 > L) || (CAUSAL && kh + 31 > qw0);
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 if (need_mask) {
-                    const int kk = k0 + 8 * (r >> 2) + 4 * g + (r & 3);
+                    const int kk = kh + 8 * (r >> 2) + 4 * g + (r & 3);
                     const bool ok = kk < L && (!CAUSAL || kk <= tq);
-                    st[r] = ok ? st[r] : -__builtin_huge_valf();
+                    st[hf][r] = ok ? st[hf][r] : -__builtin_huge_valf();
                 }
-                tmax = __builtin_fmaxf(tmax, st[r]);
+                tmax = __builtin_fmaxf(tmax, st[hf][r]);
             }
-            tmax = __builtin_fmaxf(tmax, __shfl_xor(tmax, 32));
-            // raise the running max only past the margin (wave-uniform rescale)
-            const bool raise = (tmax - m) * c2 > kRescale || m == -__builtin_huge_valf();
-            if (__any((int)raise)) {
-                const float mnew = raise ? tmax : m;
-                const float mref = (mnew == -__builtin_huge_valf()) ? 0.0f : mnew;
-                const float alpha = (m == -__builtin_huge_valf()) ? 0.0f : __builtin_amdgcn_exp2f((m - mref) * c2);
-                m = mnew;
-                lsum *= alpha;
+        }
+        tmax = xmax32(tmax);
+        // raise the running max only past the margin (wave-uniform rescale)
+        const bool raise = (tmax - m) * c2 > kRescale || m == -__builtin_huge_valf();
+        if (__any((int)raise)) {
+            const float mnew = raise ? tmax : m;
+            const float mref = (mnew == -__builtin_huge_valf()) ? 0.0f : mnew;
+            const float alpha = (m == -__builtin_huge_valf()) ? 0.0f : __builtin_amdgcn_exp2f((m - mref) * c2);
+            m = mnew;
+            lsum *= alpha;
 #pragma unroll
-                for (int db = 0; db < 4; ++db)
+            for (int db = 0; db < 4; ++db)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
-            }
-            const float mc = (m == -__builtin_huge_valf()) ? 0.0f : m * c2;
-            float psum = 0.0f;
+                for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
+        }
+        const float mc = (m == -__builtin_huge_valf()) ? 0.0f : m * c2;
+        float psum = 0.0f;
+        uint4 pb[NH][2];
+#pragma unroll
+        for (int hf = 0; hf < NH; ++hf) {
             uint32_t pw[8];
 #pragma unroll
             for (int r = 0; r < 16; r += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(st[r], c2, -mc));
-                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(st[r + 1], c2, -mc));
+                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(st[hf][r], c2, -mc));
+                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(st[hf][r + 1], c2, -mc));
                 psum += p0 + p1;
                 pw[r >> 1] = pack2<BF16>(p0, p1);
             }
-            psum += __shfl_xor(psum, 32);
-            lsum += psum;
-            // O^T += V^T P^T (two steps of 16 keys)
-            const uint4 pb0 = make_uint4(pw[0], pw[1], pw[2], pw[3]);
-            const uint4 pb1 = make_uint4(pw[4], pw[5], pw[6], pw[7]);
-#pragma unroll
-            for (int db = 0; db < 4; ++db) {
-                const uint8_t *vrow = sV + (32 * db + c32) * kVStride + 64 * hf + 16 * g;
-                acc[db] = mfma<BF16>(*reinterpret_cast<const uint4 *>(vrow), pb0, acc[db]);
-                acc[db] = mfma<BF16>(*reinterpret_cast<const uint4 *>(vrow + 32), pb1, acc[db]);
-            }
+            pb[hf][0] = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+            pb[hf][1] = make_uint4(pw[4], pw[5], pw[6], pw[7]);
         }
+        lsum += xsum32(psum);
+        // O^T += V^T P^T (two steps of 16 keys per half)
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+            for (int hf = 0; hf < NH; ++hf) {
+                const uint8_t *vrow = sV + (32 * db + c32) * kVStride + 64 * hf + 16 * g;
+                acc[db] = mfma<BF16>(*reinterpret_cast<const uint4 *>(vrow), pb[hf][0], acc[db]);
+                acc[db] = mfma<BF16>(*reinterpret_cast<const uint4 *>(vrow + 32), pb[hf][1], acc[db]);
+            }
+    };
+    auto tile = [&](int kt) __attribute__((always_inline)) {
+        const int k0 = kt * kKT;
+        // halves past this wavefront's last query hold only masked keys
+        if (!CAUSAL || k0 + 32 <= qw0 + kQW - 1) tile_keys(kt, std::true_type{});
+        else if (k0 <= qw0 + kQW - 1) tile_keys(kt, std::false_type{});
     };
     // the next tile's global loads are in flight while this tile computes
     uint4 kr[4], vr[4];
