@@ -734,7 +734,7 @@ def main():
                    "M": cfg.M, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
                      "unit": "TOPS", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
-                     "traffic": traffic_from_profile(), "kernel": "k_w4a4_gemm_2cu",
+                     "traffic": traffic_from_profile(), "kernel": "k_w4a4_gemm_pt",
                      "per_launch": "2*M*n_out*k_in int ops, averaged over the 4 launches of a step "
                                    "(HIP events around the step's GEMM phase); traffic in HBM "
                                    "bytes per launch"},
