@@ -805,10 +805,11 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
 //    into one of three scale buffers) is issued during the current tile's
 //    last k-tiles, so a new tile starts with its operands in LDS instead of
 //    a full memory round trip, and no block is relaunched per tile.
-//  * The epilogue stores straight from registers (no LDS, no barrier): lane
-//    l holds 4 consecutive columns of one row per fragment, 8 bytes; the 4
-//    fragments along n complete each 128-byte line of a row before the next
-//    store group, which the L2 merges.
+//  * Epilogue: one barrier, then each wavefront stages its own 128 x 64
+//    sub-tile through 4 KB of the ring slot just consumed, 32 rows at a
+//    time, and stores full 128-byte row segments.  No other barrier: every
+//    wavefront only reads back what it wrote itself, and the slot is not
+//    refilled before the barrier at the top of the next k-tile.
 //  * Waits: loads (the DMA) complete in order among themselves, so waiting
 //    until at most 6 instructions (one stage of this wave) are outstanding
 //    guarantees every older stage has landed; epilogue stores in between
@@ -969,33 +970,32 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_pt(const uint8_t *__restri
         tile_origin(ck, m0, n0);
         const float *s_sa = reinterpret_cast<const float *>(smem + SCALE_OFF + (ck % kScaleBufs) * SCALE_BUF);
         const float *s_sw = s_sa + BMT;
-        // Staging: the ring slot this last k-tile was read from (every wave
-        // has read it after the barrier below; the next tile's two stages sit
-        // in the other slots).  Four passes of 64 rows (16 KB): in pass p
-        // every wave writes its fragments j = 2p, 2p + 1 (rows 32p .. 32p+31
-        // of its half of the tile; 8-byte units XOR-swizzled by the row, as
-        // in k_w4a4_gemm_2cu), then all waves store full 256-byte row
-        // segments, one 16-byte store per lane.  Staging row rs < 32 is tile
-        // row 32p + rs, rs >= 32 is row 128 + 32p + (rs - 32).
+        // Staging: the ring slot this last k-tile was read from (the next
+        // tile's two stages sit in the other slots), after one barrier that
+        // lets every wave finish its reads of it.  Each wave then works on
+        // its own 4 KB of the slot, no further barrier: four passes over its
+        // fragment pairs j = 2p, 2p + 1 (32 rows x 64 columns of its 128 x 64
+        // sub-tile) -- 8-byte units written in MFMA layout (unit index XORed
+        // with 2 ((row >> 1) & 7): conflict-free), read back as 16-byte
+        // chunks, stored as full 128-byte row segments.
+        __syncthreads();
         // lane-derived values made opaque here, so that the epilogue's
         // address arithmetic stays in the epilogue instead of being hoisted
         // out of the k-loop into registers the loop needs
-        int r16e = r16, cqe = cq, te = t;
-        asm volatile("" : "+v"(r16e), "+v"(cqe), "+v"(te));
-        uint8_t *stg = smem + (g % NST) * L_STAGE;
+        int r16e = r16, cqe = cq, lanee = lane;
+        asm volatile("" : "+v"(r16e), "+v"(cqe), "+v"(lanee));
+        uint8_t *stg = smem + (g % NST) * L_STAGE + wave * 4096;
         const int rows_left = M - m0, cols_left = N - n0;
         const bool full = vec16 && rows_left >= BMT && cols_left >= L_BN;
-        const int cch = te & 15;
-        uint16_t *yb = static_cast<uint16_t *>(y) + (int64_t)m0 * ldy + n0 + 8 * cch;
+        const int rc = lanee & 7;                           // 16-byte chunk of a row read back
 #pragma unroll
         for (int pass = 0; pass < AF / 2; ++pass) {
-            __syncthreads();                    // the slot (or the previous pass) is free
 #pragma unroll
             for (int jj = 0; jj < 2; ++jj) {
                 const int j = 2 * pass + jj;
                 const int rl = wm * (BMT / 2) + 16 * j + r16e;
                 const float sam = s_sa[rl];
-                const int rs = 32 * wm + 16 * jj + r16e;           // staging row
+                const int rs = 16 * jj + r16e;                    // staging row (0..31)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int nl = wn * 64 + 16 * i + 4 * cqe;
@@ -1022,8 +1022,8 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_pt(const uint8_t *__restri
                         }
                         packed = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
                     }
-                    const int u = (nl >> 2) ^ (r16e << 1);
-                    *reinterpret_cast<uint2 *>(stg + rs * 256 + u * 8) = packed;
+                    const int u = (4 * i + cqe) ^ (2 * ((rs >> 1) & 7));
+                    *reinterpret_cast<uint2 *>(stg + rs * 128 + u * 8) = packed;
                     if constexpr (ACC) {
                         const int m = m0 + rl, nb0 = n0 + nl;
                         if (m < M) {
@@ -1035,23 +1035,27 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_pt(const uint8_t *__restri
                     acc[i][j] = v4i{0, 0, 0, 0};
                 }
             }
-            __syncthreads();
+            // the wave's own 32 x 64 block back as 16-byte chunks: lane l,
+            // step s reads row 8 s + l / 8, chunk l % 8 (LDS operations of one
+            // wave take effect in issue order)
 #pragma unroll
             for (int s4 = 0; s4 < 4; ++s4) {
-                const int rs = 16 * s4 + (te >> 4);
-                const int r = (rs < 32) ? 32 * pass + rs : BMT / 2 + 32 * pass + (rs - 32);
-                const uint4 val = *reinterpret_cast<const uint4 *>(stg + rs * 256 + ((cch ^ (rs & 15)) << 4));
-                uint16_t *dst = yb + (int64_t)r * ldy;
+                const int rs = 8 * s4 + (lanee >> 3);
+                const int cu = (2 * rc) ^ (2 * ((rs >> 1) & 7));     // even: the pair stays in order
+                const uint4 val = *reinterpret_cast<const uint4 *>(stg + rs * 128 + cu * 8);
+                const int rt = wm * (BMT / 2) + 32 * pass + rs;        // tile row
+                const int ct = wn * 64 + 8 * rc;                       // tile column
+                uint16_t *dst = static_cast<uint16_t *>(y) + (int64_t)(m0 + rt) * ldy + n0 + ct;
                 if (full) {
                     *reinterpret_cast<uint4 *>(dst) = val;
-                } else if (r < rows_left) {
-                    if (vec16 && 8 * cch + 8 <= cols_left) {
+                } else if (rt < rows_left) {
+                    if (vec16 && ct + 8 <= cols_left) {
                         *reinterpret_cast<uint4 *>(dst) = val;
                     } else {
                         const uint32_t w4[4] = {val.x, val.y, val.z, val.w};
 #pragma unroll
-                        for (int jj = 0; jj < 8; ++jj)
-                            if (8 * cch + jj < cols_left) dst[jj] = (uint16_t)(w4[jj >> 1] >> (16 * (jj & 1)));
+                        for (int e = 0; e < 8; ++e)
+                            if (ct + e < cols_left) dst[e] = (uint16_t)(w4[e >> 1] >> (16 * (e & 1)));
                     }
                 }
             }
