@@ -325,9 +325,10 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
 //    on equal cosine".  MSD radix select with 11-bit digits from the top of X:
 //    the first digit is sign + exponent + 4 mantissa bits, which spreads the
 //    typical scores (most near zero) over many buckets; the select stops as
-//    soon as the boundary bucket is taken whole, or, when every candidate left
-//    in it carries the same key (a tie), by one ordered scan that keeps the
-//    lowest indices.
+//    soon as the boundary bucket is taken whole; when it holds at most 128
+//    candidates, by ranking them against each other on the whole composite;
+//    or, when every candidate left in it carries the same key (a tie), by one
+//    ordered scan that keeps the lowest indices.
 // ---------------------------------------------------------------------------
 constexpr int kTkThreads = 1024;
 constexpr int kDigit = 11;
@@ -339,6 +340,13 @@ struct Composite {
     uint64_t hi;      // X >> 16
     uint32_t lo;      // X & 0xFFFF
 };
+
+// a boundary-bucket candidate listed for the final ranking (one 16-byte read)
+struct __attribute__((aligned(16))) Ranked {
+    uint64_t hi;
+    uint32_t lo, pad;
+};
+constexpr int kRankMax = kTkThreads / 8;   // largest boundary bucket ranked directly
 
 __device__ __forceinline__ Composite make_composite(int64_t k, int i) {
     const uint64_t u = (uint64_t)(k < 0 ? -k : k);
@@ -389,13 +397,16 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
     __shared__ __attribute__((aligned(16))) uint32_t wtot[kTkThreads / 64];
     __shared__ uint32_t sh_bucket, sh_gt, sh_eq;
     __shared__ unsigned long long sh_hmin, sh_hmax;      // key bits of X above the index
+    __shared__ uint32_t sh_cnt;                          // candidates listed for ranking
+    __shared__ Ranked s_rk[kRankMax];
+    __shared__ uint32_t s_rk_keep[kRankMax];
     __shared__ uint32_t sh_lmin, sh_lmax;
 
     const int b = blockIdx.x;
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     for (int q = t; q < kBins; q += kTkThreads) hist[q] = 0;
-    if (t == 0) { sh_hmin = ~0ull; sh_hmax = 0; sh_lmin = ~0u; sh_lmax = 0; }
+    if (t == 0) { sh_hmin = ~0ull; sh_hmax = 0; sh_lmin = ~0u; sh_lmax = 0; sh_cnt = 0; }
     __syncthreads();
     // tokens kept beforehand: bitmap in the (still unused) histogram
     uint32_t prekept = 0;
@@ -491,6 +502,59 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
             }
             need -= gt;
             if (eq == need || lo == 0) { kept |= cont; break; }   // block-uniform
+            if (eq <= (uint32_t)kRankMax) {                      // block-uniform
+                // Few candidates left in the boundary bucket: list them (one
+                // LDS atomic per wavefront) and rank each against all the
+                // others by the whole composite (unique, so the ranks are
+                // 0 .. eq - 1), 8 threads per candidate; the `need` best are
+                // kept.  Two barriers instead of a tie check and further
+                // digit passes.
+                uint32_t slot[E];
+                uint64_t bal[E];
+                uint32_t wsum = 0;
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    bal[e] = __ballot((cont >> e) & 1u);
+                    wsum += (uint32_t)__popcll(bal[e]);
+                }
+                if (wsum) {                                      // wavefront-uniform
+                    uint32_t base = 0;
+                    if (lane == 0) base = atomicAdd(&sh_cnt, wsum);
+                    base = (uint32_t)__shfl((int)base, 0);
+#pragma unroll
+                    for (int e = 0; e < E; ++e) {
+                        const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+                            (uint32_t)(bal[e] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal[e], 0u));
+                        slot[e] = base + below;
+                        if ((cont >> e) & 1u) s_rk[slot[e]] = Ranked{x[e].hi, x[e].lo, 0u};
+                        base += (uint32_t)__popcll(bal[e]);
+                    }
+                }
+                __syncthreads();
+                {
+                    const uint32_t ci = (uint32_t)t >> 3, sub = (uint32_t)t & 7u;
+                    uint32_t rank = 0;
+                    if (ci < eq) {
+                        const Ranked me = s_rk[ci];
+#pragma unroll 4
+                        for (uint32_t c = sub; c < eq; c += 8) {
+                            const Ranked o = s_rk[c];
+                            rank += (o.hi > me.hi || (o.hi == me.hi && o.lo > me.lo)) ? 1u : 0u;
+                        }
+                    }
+                    rank += (uint32_t)__shfl_xor((int)rank, 1);
+                    rank += (uint32_t)__shfl_xor((int)rank, 2);
+                    rank += (uint32_t)__shfl_xor((int)rank, 4);
+                    if (ci < eq && sub == 0) s_rk_keep[ci] = (rank < need) ? 1u : 0u;
+                }
+                __syncthreads();
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    if (((cont >> e) & 1u) && s_rk_keep[slot[e]]) kept |= 1u << e;
+                // the list is next written after further barriers
+                if (t == 0) sh_cnt = 0;
+                break;
+            }
             // Still ambiguous.  If every remaining candidate has the same key
             // (a tie in cosine), the lower indices win: take the `need` first
             // candidates in token order with one ordered scan instead of
