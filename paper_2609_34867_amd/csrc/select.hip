@@ -343,8 +343,8 @@ struct Composite {
 
 // a boundary-bucket candidate listed for the final ranking (one 16-byte read)
 struct __attribute__((aligned(16))) Ranked {
-    uint64_t hi;
-    uint32_t lo, pad;
+    int64_t key;
+    uint32_t idx, pad;
 };
 constexpr int kRankMax = kTkThreads / 8;   // largest boundary bucket ranked directly
 
@@ -373,6 +373,18 @@ __device__ __forceinline__ uint32_t comp_digit(const Composite &x, int lo, int w
     if (lo >= kLoBits) return (uint32_t)(x.hi >> (lo - kLoBits)) & mask;
     const uint64_t v = (x.hi << (kLoBits - lo)) | (uint64_t)(x.lo >> lo);
     return (uint32_t)v & mask;
+}
+
+// The top 11 bits of X (sign, exponent, 4 mantissa bits) straight from the
+// key, without building the composite.
+__device__ __forceinline__ uint32_t top_digit(int64_t k) {
+    const uint64_t u = (uint64_t)(k < 0 ? -k : k);
+    uint32_t em = 0;                             // e (6 bits) and 4 mantissa bits
+    if (u) {
+        const int lz = __clzll((long long)u);
+        em = ((uint32_t)(64 - lz) << 4) | (uint32_t)(((u << lz) << 1) >> 60);
+    }
+    return (k < 0) ? (~em & 0x3FFu) : (0x400u | em);
 }
 
 // Order-preserving integer key of an fp32 value (finite inputs): larger
@@ -450,24 +462,36 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
     for (int j = 0; j < J; ++j) {
         const uint32_t quota = (uint32_t)(K / J + (j < K % J ? 1 : 0));
         if (!kPrefetch && j > 0) load_keys(j);
-        Composite x[E];
+        int64_t kc[E];                                       // this concept's keys
         uint32_t cont = 0;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const int i = t * E + e;
-            x[e] = make_composite(kn[e], i);
+            kc[e] = kn[e];
             if (i < N && !((kept >> e) & 1u)) cont |= 1u << e;
         }
         if (kPrefetch && j + 1 < J) load_keys(j + 1);
         if (quota == 0) continue;                            // block-uniform
+        // The first digit comes straight from the key; the full composites
+        // are built only if the select goes past the first digit without
+        // reaching the direct ranking.
+        uint32_t dg1[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) dg1[e] = top_digit(kc[e]);
+        Composite x[E];
+        bool have_x = false;                                 // block-uniform
         uint32_t need = quota;
         int pos = kXBits;
         while (true) {
             const int w = min(kDigit, pos);
             const int lo = pos - w;
+            const bool first = (pos == kXBits);
+            auto digit = [&](int e) __attribute__((always_inline)) {
+                return first ? dg1[e] : comp_digit(x[e], lo, w);
+            };
 #pragma unroll
             for (int e = 0; e < E; ++e)
-                if ((cont >> e) & 1u) atomicAdd(&hist[comp_digit(x[e], lo, w)], 1u);
+                if ((cont >> e) & 1u) atomicAdd(&hist[digit(e)], 1u);
             __syncthreads();
             // reverse-order inclusive scan: thread t covers bins kBins-1-2t, kBins-2-2t
             const int b0 = kBins - 1 - 2 * t, b1 = kBins - 2 - 2 * t;
@@ -483,21 +507,12 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
             if (e1 < need && need <= e1 + c1) { sh_bucket = b1; sh_gt = e1; sh_eq = c1; }
             __syncthreads();
             const uint32_t bucket = sh_bucket, gt = sh_gt, eq = sh_eq;
-            // key part of X: hi (67 - 3 bits) and the 3 key bits of lo
-            unsigned long long hmin = ~0ull, hmax = 0;
-            uint32_t lmin = ~0u, lmax = 0;
 #pragma unroll
             for (int e = 0; e < E; ++e) {
                 if ((cont >> e) & 1u) {
-                    const uint32_t dg = comp_digit(x[e], lo, w);
+                    const uint32_t dg = digit(e);
                     if (dg > bucket) { kept |= 1u << e; cont &= ~(1u << e); }
                     else if (dg < bucket) { cont &= ~(1u << e); }
-                    else {
-                        hmin = min(hmin, (unsigned long long)x[e].hi);
-                        hmax = max(hmax, (unsigned long long)x[e].hi);
-                        lmin = min(lmin, x[e].lo >> 13);
-                        lmax = max(lmax, x[e].lo >> 13);
-                    }
                 }
             }
             need -= gt;
@@ -505,10 +520,10 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
             if (eq <= (uint32_t)kRankMax) {                      // block-uniform
                 // Few candidates left in the boundary bucket: list them (one
                 // LDS atomic per wavefront) and rank each against all the
-                // others by the whole composite (unique, so the ranks are
-                // 0 .. eq - 1), 8 threads per candidate; the `need` best are
-                // kept.  Two barriers instead of a tie check and further
-                // digit passes.
+                // others by (key, lower index first), the order of the
+                // composite (so the ranks are 0 .. eq - 1), 8 threads per
+                // candidate; the `need` best are kept.  Two barriers instead
+                // of a tie check and further digit passes.
                 uint32_t slot[E];
                 uint64_t bal[E];
                 uint32_t wsum = 0;
@@ -526,7 +541,7 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
                         const uint32_t below = __builtin_amdgcn_mbcnt_hi(
                             (uint32_t)(bal[e] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal[e], 0u));
                         slot[e] = base + below;
-                        if ((cont >> e) & 1u) s_rk[slot[e]] = Ranked{x[e].hi, x[e].lo, 0u};
+                        if ((cont >> e) & 1u) s_rk[slot[e]] = Ranked{kc[e], (uint32_t)(t * E + e), 0u};
                         base += (uint32_t)__popcll(bal[e]);
                     }
                 }
@@ -539,7 +554,7 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
 #pragma unroll 4
                         for (uint32_t c = sub; c < eq; c += 8) {
                             const Ranked o = s_rk[c];
-                            rank += (o.hi > me.hi || (o.hi == me.hi && o.lo > me.lo)) ? 1u : 0u;
+                            rank += (o.key > me.key || (o.key == me.key && o.idx < me.idx)) ? 1u : 0u;
                         }
                     }
                     rank += (uint32_t)__shfl_xor((int)rank, 1);
@@ -554,6 +569,30 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
                 // the list is next written after further barriers
                 if (t == 0) sh_cnt = 0;
                 break;
+            }
+            if (!have_x) {
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    // opaque copy: keeps the composites inside this rarely
+                    // taken branch instead of being computed for every concept
+                    int64_t k = kc[e];
+                    asm volatile("" : "+v"(k));
+                    x[e] = make_composite(k, t * E + e);
+                }
+                have_x = true;
+            }
+            // key part of X of the candidates left: hi (67 - 3 bits) and the
+            // 3 key bits of lo
+            unsigned long long hmin = ~0ull, hmax = 0;
+            uint32_t lmin = ~0u, lmax = 0;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                if ((cont >> e) & 1u) {
+                    hmin = min(hmin, (unsigned long long)x[e].hi);
+                    hmax = max(hmax, (unsigned long long)x[e].hi);
+                    lmin = min(lmin, x[e].lo >> 13);
+                    lmax = max(lmax, x[e].lo >> 13);
+                }
             }
             // Still ambiguous.  If every remaining candidate has the same key
             // (a tie in cosine), the lower indices win: take the `need` first
