@@ -115,7 +115,7 @@ int p4q_select(p4q_dtype dt, int B, int N, int d,
  *
  * Its workspace is a static device array of P4Q_SELECT_SCRATCH_BYTES (8 MiB)
  * that every device the library runs on holds until the process ends.  A
- * call needs p4q_select_workspace_bytes(B, N, d, J) bytes of it (2.7 MB for
+ * call needs p4q_select_workspace_bytes(B, N, d, J) bytes of it (2.4 MB for
  * 16 images of 2880 tokens, d = 4096, J = 4); a larger request returns
  * P4Q_ERR_WORKSPACE and enqueues nothing.  No part of the array is read
  * before the same call has written it, so nothing needs clearing between

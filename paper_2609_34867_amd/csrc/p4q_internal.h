@@ -70,7 +70,6 @@ hipError_t launch_attention(p4q_dtype dt, int B, int L, int H, const void *q, co
 struct SelectWorkspace {
     int32_t *stats;      // [B][N][J+1]: D_0..D_{J-1}, Nv   (documented)
     int64_t *keys;       // [B][J][N]: exact order keys (internal)
-    int8_t *ccodes;      // [B][J][d]: concept codes (internal)
     uint32_t *vcodes = nullptr;   // [B][N][d/8] packed visual codes, or none
 };
 

@@ -1,18 +1,18 @@
 // Quantization-aware visual-token selection (P4Q Sec. 3.2, Query Relevance
-// with the whole budget), four kernels on one stream:
+// with the whole budget), three kernels on one stream:
 //
-//  1. k_concept_codes: fake-quantize the J concept rows of each sample to
-//     int8 codes (Q4, clip c), one work-group per row.
-//  2. k_select_score: one pass over the visual features.  Each wavefront
-//     holds one token row in registers, takes its absmax, quantizes it
-//     on-chip (the fake-quantized copy is never written), and forms the exact
-//     integer statistics D_ij = <cv_i, cq_j> and Nv_i = |cv_i|^2 with 8-wide
-//     int4 dot products against packed concept codes staged in LDS.  It also turns
-//     (D_ij, Nv_i) into an exact integer order key (see exact_key).
-//  3. k_select_topk: one workgroup per sample.  For each concept in order it
+//  1. k_select_score: one pass over the visual features.  Each block first
+//     fake-quantizes its sample's J concept rows (Q4, clip c) into packed
+//     int4 codes in LDS.  Then each wavefront holds one token row in
+//     registers, takes its absmax, quantizes it on-chip (the fake-quantized
+//     copy is never written), and forms the exact integer statistics
+//     D_ij = <cv_i, cq_j> and Nv_i = |cv_i|^2 with 8-wide int4 dot products
+//     against the concept codes.  It also turns (D_ij, Nv_i) into an exact
+//     integer order key (see exact_key).
+//  2. k_select_topk: one workgroup per sample.  For each concept in order it
 //     radix-selects the quota's largest (key, -index) composites among tokens
 //     not yet kept, then writes the kept indices in ascending order.
-//  4. k_select_gather: copies the ORIGINAL rows of the kept tokens, then the
+//  3. k_select_gather: copies the ORIGINAL rows of the kept tokens, then the
 //     text rows, into the pruned sequence with 16-byte vector copies.
 #include "p4q_internal.h"
 
@@ -49,47 +49,7 @@ __device__ __forceinline__ int64_t exact_key(int32_t D, int32_t Nv, int LS) {
 }
 
 // ---------------------------------------------------------------------------
-// 1. concept codes: one 256-thread work-group per concept row (all of the
-//    row's loads issued at once), int8 codes out
-// ---------------------------------------------------------------------------
-template <int CH, bool BF16, bool CLIP1>
-__global__ __launch_bounds__(256) void k_concept_codes(const uint8_t *__restrict__ con, int d,
-                                                       float clip, int8_t *__restrict__ ccodes) {
-    __shared__ uint32_t s_max[4];
-    const int row = blockIdx.x, t = threadIdx.x;
-    const int nchunk = d / 8;
-    const uint4 *src = reinterpret_cast<const uint4 *>(con + (int64_t)row * d * 2);
-    uint2 *dst = reinterpret_cast<uint2 *>(ccodes + (int64_t)row * d);
-    uint4 v[CH];
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        const int q = t + 256 * c;
-        v[c] = (q < nchunk) ? src[q] : make_uint4(0, 0, 0, 0);
-    }
-    uint32_t m2 = 0;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
-    const uint32_t mw = wave_max_u32(max(m2 & 0xFFFFu, m2 >> 16));
-    if ((t & 63) == 0) s_max[t >> 6] = mw;
-    __syncthreads();
-    const uint32_t mbits = max(max(s_max[0], s_max[1]), max(s_max[2], s_max[3]));
-    const float s = row_scale<CLIP1>(mag_to_f32<BF16>(mbits), clip);
-    const bool tiny = !(s >= kTinyScale);
-    const float r = tiny ? 0.0f : 1.0f / s;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        const int q = t + 256 * c;
-        uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        uint32_t near = 0;
-        if (s != 0.0f && !tiny) q4_chunk_fast<BF16, CLIP1>(v[c], r, w, near);
-        if (s != 0.0f && (tiny || near)) q4_chunk_exact<BF16>(v[c], s, w);   // rare
-        if (q < nchunk) dst[q] = make_uint2(bytes4(w[0], w[1], w[2], w[3]),
-                                            bytes4(w[4], w[5], w[6], w[7]));
-    }
-}
-
-// ---------------------------------------------------------------------------
-// 2. fake-quant + score.  Grid (row blocks, B); 4 wavefronts per block, each
+// 1. fake-quant + score.  Grid (row blocks, B); 4 wavefronts per block, each
 //    wavefront walks `rows_per_wave` consecutive tokens of sample blockIdx.y.
 // ---------------------------------------------------------------------------
 constexpr int kMaxJ = 8;
@@ -129,12 +89,77 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t o
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
 }
 
+// Q4 codes of one row held as CH 16-byte chunks per lane (lane l: chunks
+// l, l + 64, ...; zeros past the row end), packed 8 per word in value order.
+// absmax through the wavefront (no LDS), then the bracketed fast path with a
+// per-chunk exact fallback.  Every lane of the wavefront must be active.
+template <int CH, bool BF16, bool CLIP1>
+__device__ __forceinline__ void q4_row_packed(const uint4 *v, float clip, uint32_t *cv) {
+    uint32_t m2 = 0;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
+    const uint32_t mbits = wave_max_u32(max(m2 & 0xFFFFu, m2 >> 16));
+    const float s = row_scale<CLIP1>(mag_to_f32<BF16>(mbits), clip);
+#pragma unroll
+    for (int c = 0; c < CH; ++c) cv[c] = 0u;
+    if (s != 0.0f) {
+        const bool tiny = !(s >= kTinyScale);
+        const float rc = tiny ? 0.0f : 1.0f / s;
+        // Bracketed fast path: with r = fl32(1/s), x r(1 - 2^-20) and
+        // x r(1 + 2^-20) (products rounded once, inside the fma) enclose
+        // fl32(x/s), since r and fl32(x/s) each err by at most 2^-24
+        // relative.  rne is monotone, so where the two bracket ends round
+        // to the same integer, so does fl32(x/s); where they differ a
+        // half-integer lies inside and the exact path decides.  Two fmas
+        // and one bitwise merge per value.
+        const float rhi = __fmul_rn(rc, 1.0f + 0x1p-20f), rlo = __fmul_rn(rc, 1.0f - 0x1p-20f);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            uint32_t w[8];
+            uint32_t dif = 0u;    // nonzero: a bracket of this chunk straddles a boundary
+            if (!tiny) {
+                const uint32_t x4[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const float x = h ? hi_f32<BF16>(x4[i]) : lo_f32<BF16>(x4[i]);
+                        float tq = __builtin_fmaf(x, rhi, kRneMagic);
+                        const float tl = __builtin_fmaf(x, rlo, kRneMagic);
+                        // (as asm: left to itself the compiler turns the
+                        // merge into a compare and select per value)
+                        uint32_t tlb = __float_as_uint(tl);
+                        asm("v_xor_b32 %1, %1, %2\n\tv_or_b32 %0, %0, %1"
+                            : "+v"(dif), "+v"(tlb)
+                            : "v"(__float_as_uint(tq)));
+                        if constexpr (!CLIP1)
+                            tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
+                        w[2 * i + h] = __float_as_uint(tq);
+                    }
+                }
+            }
+            // wave-uniform and rare: some lane holds a value of this chunk
+            // next to a rounding boundary (exact fp16 ratios such as x = a/2
+            // land on ties), or the scale is tiny.  Only this chunk is
+            // recomputed by exact division.
+            if (tiny || __any(dif != 0u)) {
+                uint4 vc = v[c];
+                // opaque copy: keeps the exact path's fp16 -> fp32 conversions
+                // from being hoisted into (and paid on) the fast path
+                asm volatile("" : "+v"(vc.x), "+v"(vc.y), "+v"(vc.z), "+v"(vc.w));
+                q4_chunk_exact<BF16>(vc, s, w);
+            }
+            cv[c] = pack_nibbles(w);
+        }
+    }
+}
+
 constexpr int kRowsPerWave = 8;   // rows per batch (sums gathered for one key per lane)
 
 template <int CH, int JMAX, bool BF16, bool CLIP1>
 __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uint8_t *__restrict__ vis, int N, int d,
                                                       int J, float clip, int LS, int rpw,
-                                                      const int8_t *__restrict__ ccodes,
+                                                      const uint8_t *__restrict__ concepts,
                                                       int32_t *__restrict__ stats,
                                                       int64_t *__restrict__ keys,
                                                       uint32_t *__restrict__ vcodes) {
@@ -146,23 +171,30 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
     const int nchunk = d / 8;
     constexpr int kChunks = 64 * CH;
 
-    // stage this sample's concept codes in LDS; absent concepts and chunks
-    // past the row end are zeros, so the dot products below need no guards
-    {
-        const uint2 *g = reinterpret_cast<const uint2 *>(ccodes + (int64_t)b * J * d);
-        for (int q = threadIdx.x; q < JMAX * kChunks; q += 256) {
-            const int j = q / kChunks, c = q - j * kChunks;
-            uint32_t pk = 0u;
-            if (j < J && c < nchunk) {
-                const uint2 u = g[j * nchunk + c];
+    // this sample's concept codes into LDS, one concept row per wavefront
+    // at a time, by the same quantizer as the visual rows; absent concepts
+    // and chunks past the row end are zeros, so the dot products below need
+    // no guards
+    uint32_t coff[CH];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    pk |= ((u.x >> (8 * e)) & 0xFu) << (4 * e);
-                    pk |= ((u.y >> (8 * e)) & 0xFu) << (4 * e + 16);
-                }
-            }
-            s_cc[q] = pk;
+    for (int c = 0; c < CH; ++c) {
+        const int q = lane + 64 * c;
+        coff[c] = (q < nchunk) ? (uint32_t)q * 16u : 0x80000000u;
+    }
+    for (int j = wave; j < JMAX; j += 4) {                   // wave-uniform
+        uint32_t cq[CH];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) cq[c] = 0u;
+        if (j < J) {
+            const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+                (void *)(concepts + ((int64_t)b * J + j) * d * 2), 0, d * 2, 0x00020000);
+            uint4 v[CH];
+#pragma unroll
+            for (int c = 0; c < CH; ++c) v[c] = buf_load16(rc, coff[c]);
+            q4_row_packed<CH, BF16, CLIP1>(v, clip, cq);
         }
+#pragma unroll
+        for (int c = 0; c < CH; ++c) s_cc[j * kChunks + lane + 64 * c] = cq[c];
     }
     __syncthreads();
 
@@ -170,12 +202,6 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
     // word and one key per lane and batch)
     const int first = (blockIdx.x * 4 + wave) * rpw;
     const int last = min(first + rpw, N);
-    uint32_t coff[CH];
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        const int q = lane + 64 * c;
-        coff[c] = (q < nchunk) ? (uint32_t)q * 16u : 0x80000000u;
-    }
     for (int row0 = first; row0 < last; row0 += kRowsPerWave) {   // wave-uniform
     const int nrows = min(kRowsPerWave, last - row0);
     const uint8_t *vb = vis + ((int64_t)b * N + row0) * d * 2;
@@ -204,68 +230,11 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
             load_row(r, v);
         }
 
-        uint32_t m2 = 0;
-#pragma unroll
-        for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
-        const uint32_t mbits = wave_max_u32(max(m2 & 0xFFFFu, m2 >> 16));
-        const float s = row_scale<CLIP1>(mag_to_f32<BF16>(mbits), clip);
-
         uint32_t cv[CH];                                     // packed int4 codes, 8 per chunk
-#pragma unroll
-        for (int c = 0; c < CH; ++c) cv[c] = 0u;
+        q4_row_packed<CH, BF16, CLIP1>(v, clip, cv);
         // packed int4 copy of the codes, when asked for (the Gram matrix of
         // the diversity stage is computed from it)
         uint32_t *vrow = vcodes ? vcodes + ((int64_t)b * N + row0 + r) * (d / 8) : nullptr;
-        if (s != 0.0f) {
-            const bool tiny = !(s >= kTinyScale);
-            const float rc = tiny ? 0.0f : 1.0f / s;
-            // Bracketed fast path: with r = fl32(1/s), x r(1 - 2^-20) and
-            // x r(1 + 2^-20) (products rounded once, inside the fma) enclose
-            // fl32(x/s), since r and fl32(x/s) each err by at most 2^-24
-            // relative.  rne is monotone, so where the two bracket ends round
-            // to the same integer, so does fl32(x/s); where they differ a
-            // half-integer lies inside and the exact path decides.  Two fmas
-            // and one bitwise merge per value.
-            const float rhi = __fmul_rn(rc, 1.0f + 0x1p-20f), rlo = __fmul_rn(rc, 1.0f - 0x1p-20f);
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                uint32_t w[8];
-                uint32_t dif = 0u;    // nonzero: a bracket of this chunk straddles a boundary
-                if (!tiny) {
-                    const uint32_t x4[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-                        for (int h = 0; h < 2; ++h) {
-                            const float x = h ? hi_f32<BF16>(x4[i]) : lo_f32<BF16>(x4[i]);
-                            float tq = __builtin_fmaf(x, rhi, kRneMagic);
-                            const float tl = __builtin_fmaf(x, rlo, kRneMagic);
-                            // (as asm: left to itself the compiler turns the
-                            // merge into a compare and select per value)
-                            uint32_t tlb = __float_as_uint(tl);
-                            asm("v_xor_b32 %1, %1, %2\n\tv_or_b32 %0, %0, %1"
-                                : "+v"(dif), "+v"(tlb)
-                                : "v"(__float_as_uint(tq)));
-                            if constexpr (!CLIP1)
-                                tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
-                            w[2 * i + h] = __float_as_uint(tq);
-                        }
-                    }
-                }
-                // wave-uniform and rare: some lane holds a value of this chunk
-                // next to a rounding boundary (exact fp16 ratios such as x = a/2
-                // land on ties), or the scale is tiny.  Only this chunk is
-                // recomputed by exact division.
-                if (tiny || __any(dif != 0u)) {
-                    uint4 vc = v[c];
-                    // opaque copy: keeps the exact path's fp16 -> fp32 conversions
-                    // from being hoisted into (and paid on) the fast path
-                    asm volatile("" : "+v"(vc.x), "+v"(vc.y), "+v"(vc.z), "+v"(vc.w));
-                    q4_chunk_exact<BF16>(vc, s, w);
-                }
-                cv[c] = pack_nibbles(w);
-            }
-        }
         if (vrow) {
 #pragma unroll
             for (int c = 0; c < CH; ++c)
@@ -314,7 +283,7 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
 }
 
 // ---------------------------------------------------------------------------
-// 3. top-K.  One 1024-thread workgroup per sample; thread t owns tokens
+// 2. top-K.  One 1024-thread workgroup per sample; thread t owns tokens
 //    t*E .. t*E+E-1 (E <= 8), so the final compaction is an ordered scan.
 //    Per concept: candidates = tokens not yet kept.  Each exact key k is
 //    mapped to an order-preserving 67-bit code V = [s | e | m]: s = 1 for
@@ -642,7 +611,7 @@ __global__ __launch_bounds__(kTkThreads) void k_select_topk(const void *__restri
 }
 
 // ---------------------------------------------------------------------------
-// 4. gather: one wavefront per output row; all of a row's 16-byte loads are
+// 3. gather: one wavefront per output row; all of a row's 16-byte loads are
 //    issued before its stores (up to 8 KB in flight per wavefront)
 // ---------------------------------------------------------------------------
 constexpr int kGatherMaxCh = 16;      // chunks per lane held in registers (d <= 8192)
@@ -682,7 +651,7 @@ __global__ __launch_bounds__(256) void k_select_gather(const uint4 *__restrict__
 
 template <int CH, int JMAX, bool BF16, bool CLIP1>
 hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const void *vis,
-                        const SelectWorkspace &ws, hipStream_t stream) {
+                        const void *concepts, const SelectWorkspace &ws, hipStream_t stream) {
     const size_t lds = (size_t)JMAX * 64 * CH * 4;
     // Rows per wavefront: enough that the whole grid is resident at once
     // (one wave of blocks, no partly filled last wave).
@@ -699,45 +668,30 @@ hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const vo
     const int rpw = (int)std::max<int64_t>(1, ((int64_t)B * N + waves - 1) / waves);
     const dim3 grid((N + 4 * rpw - 1) / (4 * rpw), B);
     hipLaunchKernelGGL((k_select_score<CH, JMAX, BF16, CLIP1>), grid, dim3(256), lds, stream,
-                       static_cast<const uint8_t *>(vis), N, d, J, clip, LS, rpw, ws.ccodes, ws.stats,
+                       static_cast<const uint8_t *>(vis), N, d, J, clip, LS, rpw,
+                       static_cast<const uint8_t *>(concepts), ws.stats,
                        ws.keys, ws.vcodes);
     return hipGetLastError();
 }
 
 template <int CH, bool BF16, bool CLIP1>
 hipError_t launch_score_j(int B, int N, int d, int J, float clip, int LS, const void *vis,
-                          const SelectWorkspace &ws, hipStream_t stream) {
-    if (J <= 4) return launch_score<CH, 4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    return launch_score<CH, 8, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+                          const void *concepts, const SelectWorkspace &ws, hipStream_t stream) {
+    if (J <= 4) return launch_score<CH, 4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
+    return launch_score<CH, 8, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
 }
 
 template <bool BF16, bool CLIP1>
 hipError_t launch_score_typed(int B, int N, int d, int J, float clip, int LS, const void *vis,
-                              const SelectWorkspace &ws, hipStream_t stream) {
+                              const void *concepts, const SelectWorkspace &ws, hipStream_t stream) {
     const int per_lane = (d / 8 + 63) / 64;
-    if (per_lane <= 1) return launch_score_j<1, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 2) return launch_score_j<2, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 4) return launch_score_j<4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 8) return launch_score_j<8, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 10) return launch_score_j<10, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    if (per_lane <= 16) return launch_score_j<16, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-    return launch_score<32, 4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
-}
-
-template <bool BF16, bool CLIP1>
-hipError_t launch_concepts(int rows, int d, float clip, const void *con, int8_t *cc,
-                           hipStream_t stream) {
-    const int per = (d / 8 + 255) / 256;            // d <= 16384: at most 8 chunks per thread
-    const uint8_t *src = static_cast<const uint8_t *>(con);
-    if (per <= 1)
-        hipLaunchKernelGGL((k_concept_codes<1, BF16, CLIP1>), dim3(rows), dim3(256), 0, stream, src, d, clip, cc);
-    else if (per <= 2)
-        hipLaunchKernelGGL((k_concept_codes<2, BF16, CLIP1>), dim3(rows), dim3(256), 0, stream, src, d, clip, cc);
-    else if (per <= 4)
-        hipLaunchKernelGGL((k_concept_codes<4, BF16, CLIP1>), dim3(rows), dim3(256), 0, stream, src, d, clip, cc);
-    else
-        hipLaunchKernelGGL((k_concept_codes<8, BF16, CLIP1>), dim3(rows), dim3(256), 0, stream, src, d, clip, cc);
-    return hipGetLastError();
+    if (per_lane <= 1) return launch_score_j<1, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
+    if (per_lane <= 2) return launch_score_j<2, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
+    if (per_lane <= 4) return launch_score_j<4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
+    if (per_lane <= 8) return launch_score_j<8, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
+    if (per_lane <= 10) return launch_score_j<10, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
+    if (per_lane <= 16) return launch_score_j<16, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
+    return launch_score<32, 4, BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
 }
 
 template <bool FKEYS>
@@ -764,9 +718,7 @@ hipError_t launch_codes_and_scores(int B, int N, int d, int J, float clip, const
     int lg = 0;
     while ((1ll << lg) < 64ll * d) ++lg;
     const int LS = 2 * lg;
-    hipError_t e = launch_concepts<BF16, CLIP1>(B * J, d, clip, concepts, ws.ccodes, stream);
-    if (e != hipSuccess) return e;
-    return launch_score_typed<BF16, CLIP1>(B, N, d, J, clip, LS, vis, ws, stream);
+    return launch_score_typed<BF16, CLIP1>(B, N, d, J, clip, LS, vis, concepts, ws, stream);
 }
 
 hipError_t launch_gather(int B, int N, int d, const void *vis, const void *text, int T, int K,
@@ -783,8 +735,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 }  // namespace
 
 size_t select_workspace_bytes(int B, int N, int d, int J) {
-    return align256((size_t)B * N * (J + 1) * 4) + align256((size_t)B * J * N * 8) +
-           align256((size_t)B * J * d);
+    return align256((size_t)B * N * (J + 1) * 4) + align256((size_t)B * J * N * 8);
 }
 
 SelectWorkspace select_workspace_carve(void *ws, int B, int N, int d, int J) {
@@ -793,8 +744,6 @@ SelectWorkspace select_workspace_carve(void *ws, int B, int N, int d, int J) {
     w.stats = reinterpret_cast<int32_t *>(p);
     p += align256((size_t)B * N * (J + 1) * 4);
     w.keys = reinterpret_cast<int64_t *>(p);
-    p += align256((size_t)B * J * N * 8);
-    w.ccodes = reinterpret_cast<int8_t *>(p);
     return w;
 }
 
