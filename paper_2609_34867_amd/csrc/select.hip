@@ -89,16 +89,46 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t o
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
 }
 
+// Largest |x| bit pattern (sign bit clear) among this lane's CH chunks.
+// fp16: a running packed maximum and minimum, each three-input op folding
+// two more words, then max(|max|, |min|) per half; bf16: 16-bit maxima of
+// the bit patterns with the sign masked.  Finite inputs.
+template <int CH, bool BF16>
+__device__ __forceinline__ uint32_t lane_absmax_bits(const uint4 *v) {
+    if constexpr (BF16) {
+        uint32_t m2 = 0;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
+        return max(m2 & 0xFFFFu, m2 >> 16);
+    } else {
+        uint32_t w[4 * CH];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            w[4 * c] = v[c].x;
+            w[4 * c + 1] = v[c].y;
+            w[4 * c + 2] = v[c].z;
+            w[4 * c + 3] = v[c].w;
+        }
+        uint32_t hi = w[0], lo = w[0];
+#pragma unroll
+        for (int k = 1; k < 4 * CH; k += 2) {
+            const uint32_t b = (k + 1 < 4 * CH) ? w[k + 1] : w[k];
+            asm("v_pk_maximum3_f16 %0, %0, %1, %2" : "+v"(hi) : "v"(w[k]), "v"(b));
+            asm("v_pk_minimum3_f16 %0, %0, %1, %2" : "+v"(lo) : "v"(w[k]), "v"(b));
+        }
+        // every |x| lies below max(|hi|, |lo|), per half
+        const uint32_t m2 = absmax2(absmax2(0u, hi), lo);
+        return max(m2 & 0xFFFFu, m2 >> 16);
+    }
+}
+
 // Q4 codes of one row held as CH 16-byte chunks per lane (lane l: chunks
 // l, l + 64, ...; zeros past the row end), packed 8 per word in value order.
 // absmax through the wavefront (no LDS), then the bracketed fast path with a
 // per-chunk exact fallback.  Every lane of the wavefront must be active.
 template <int CH, bool BF16, bool CLIP1>
 __device__ __forceinline__ void q4_row_packed(const uint4 *v, float clip, uint32_t *cv) {
-    uint32_t m2 = 0;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
-    const uint32_t mbits = wave_max_u32(max(m2 & 0xFFFFu, m2 >> 16));
+    const uint32_t mbits = wave_max_u32(lane_absmax_bits<CH, BF16>(v));
     const float s = row_scale<CLIP1>(mag_to_f32<BF16>(mbits), clip);
 #pragma unroll
     for (int c = 0; c < CH; ++c) cv[c] = 0u;
@@ -126,12 +156,12 @@ __device__ __forceinline__ void q4_row_packed(const uint4 *v, float clip, uint32
                         const float x = h ? hi_f32<BF16>(x4[i]) : lo_f32<BF16>(x4[i]);
                         float tq = __builtin_fmaf(x, rhi, kRneMagic);
                         const float tl = __builtin_fmaf(x, rlo, kRneMagic);
-                        // (as asm: left to itself the compiler turns the
-                        // merge into a compare and select per value)
-                        uint32_t tlb = __float_as_uint(tl);
-                        asm("v_xor_b32 %1, %1, %2\n\tv_or_b32 %0, %0, %1"
-                            : "+v"(dif), "+v"(tlb)
-                            : "v"(__float_as_uint(tq)));
+                        // dif |= tq ^ tl in one three-input bitwise op (as
+                        // asm: left to itself the compiler turns the merge
+                        // into a compare and select per value)
+                        asm("v_bitop3_b32 %0, %0, %1, %2 bitop3:0xf6"
+                            : "+v"(dif)
+                            : "v"(__float_as_uint(tq)), "v"(__float_as_uint(tl)));
                         if constexpr (!CLIP1)
                             tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
                         w[2 * i + h] = __float_as_uint(tq);
