@@ -186,32 +186,40 @@ __device__ __forceinline__ void q4_row_packed(const uint4 *v, float clip, uint32
 
 constexpr int kRowsPerWave = 8;   // rows per batch (sums gathered for one key per lane)
 
+// Work-group size of the score pass: 16 wavefronts (one work-group per CU)
+// while a wavefront fits in 128 registers, else 8.
+template <int CH>
+constexpr int score_waves() { return CH <= 8 ? 16 : 8; }
+
 template <int CH, int JMAX, bool BF16, bool CLIP1>
-__global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uint8_t *__restrict__ vis, int N, int d,
-                                                      int J, float clip, int LS, int rpw,
-                                                      const uint8_t *__restrict__ concepts,
-                                                      int32_t *__restrict__ stats,
-                                                      int64_t *__restrict__ keys,
-                                                      uint32_t *__restrict__ vcodes) {
+__global__ __launch_bounds__(64 * score_waves<CH>()) void k_select_score(
+    const uint8_t *__restrict__ vis, int N, int d, int J, float clip, int LS, int rpb,
+    const uint8_t *__restrict__ concepts, int32_t *__restrict__ stats,
+    int64_t *__restrict__ keys, uint32_t *__restrict__ vcodes) {
     extern __shared__ uint32_t s_cc[];       // [JMAX][64*CH] packed int4, zero-padded
+    __shared__ uint32_t s_next;              // next unclaimed row of this block
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63;
     // wave-uniform (keeps the row buffer descriptor in SGPRs)
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int nchunk = d / 8;
     constexpr int kChunks = 64 * CH;
+    // this block's rows [row_begin, row_begin + nrb) of sample b
+    const int row_begin = min(blockIdx.x * rpb, N);
+    const int nrb = min(rpb, N - row_begin);
 
-    // this sample's concept codes into LDS, one concept row per wavefront
-    // at a time, by the same quantizer as the visual rows; absent concepts
-    // and chunks past the row end are zeros, so the dot products below need
-    // no guards
     uint32_t coff[CH];
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
         const int q = lane + 64 * c;
         coff[c] = (q < nchunk) ? (uint32_t)q * 16u : 0x80000000u;
     }
-    for (int j = wave; j < JMAX; j += 4) {                   // wave-uniform
+    if (threadIdx.x == 0) s_next = 0;
+    // this sample's concept codes into LDS, one concept row per wavefront, by
+    // the same quantizer as the visual rows; absent concepts and chunks past
+    // the row end are zeros, so the dot products below need no guards
+    if (wave < JMAX) {                                       // wave-uniform
+        const int j = wave;
         uint32_t cq[CH];
 #pragma unroll
         for (int c = 0; c < CH; ++c) cq[c] = 0u;
@@ -228,44 +236,51 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
     }
     __syncthreads();
 
-    // this wavefront's rows [first, last), in batches of up to 8 (one stats
-    // word and one key per lane and batch)
-    const int first = (blockIdx.x * 4 + wave) * rpw;
-    const int last = min(first + rpw, N);
-    for (int row0 = first; row0 < last; row0 += kRowsPerWave) {   // wave-uniform
-    const int nrows = min(kRowsPerWave, last - row0);
-    const uint8_t *vb = vis + ((int64_t)b * N + row0) * d * 2;
-    const __amdgpu_buffer_rsrc_t rv =
-        __builtin_amdgcn_make_buffer_rsrc((void *)vb, 0, nrows * d * 2, 0x00020000);
-    auto load_row = [&](int r, uint4 *v) {
+    // Rows are claimed one at a time from the block's range through an LDS
+    // counter, so every wavefront works until the range is used up: the
+    // sequencer favours older wavefronts, and a fixed share per wavefront
+    // would leave the whole block waiting on its youngest ones.
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(vis + ((int64_t)b * N + row_begin) * d * 2), 0, nrb * d * 2, 0x00020000);
+    auto load_row = [&](int i, uint4 *v) __attribute__((always_inline)) {    // row row_begin + i
 #pragma unroll
-        for (int c = 0; c < CH; ++c) v[c] = buf_load16(rv, coff[c] + (uint32_t)(r * d * 2));
+        for (int c = 0; c < CH; ++c) v[c] = buf_load16(rv, coff[c] + (uint32_t)(i * d * 2));
+    };
+    auto claim = [&]() __attribute__((always_inline)) {
+        uint32_t i = 0;
+        if (lane == 0) i = atomicAdd(&s_next, 1u);
+        return (int)__builtin_amdgcn_readfirstlane(i);
     };
 
     // one-row prefetch only for short rows; wide rows rely on occupancy
     constexpr bool kPrefetch = CH <= 4;
     uint4 nxt[kPrefetch ? CH : 1];
-    if constexpr (kPrefetch) load_row(0, nxt);
-    int myval = 0, mynv = 0;        // lane 8v + r: value v (D_v, or Nv at v = J) of row r
-    for (int r = 0; r < nrows; ++r) {
+    int cur = claim();
+    if constexpr (kPrefetch) {
+        if (cur < nrb) load_row(cur, nxt);
+    }
+    // batch of up to 8 rows: lane 8v + r collects value v (D_v, or Nv at
+    // v = J) of the batch's row r; lane r of rowid holds that row
+    int myval = 0, mynv = 0, rowid = 0, n = 0;
+    while (cur < nrb) {                                      // wave-uniform
         // keeps the concept-code LDS reads inside the loop (hoisting them
         // would cost JMAX * 2 * CH registers and halve the occupancy)
         asm volatile("" ::: "memory");
+        const int nx = claim();                              // the row after this one
         uint4 v[CH];
         if constexpr (kPrefetch) {
 #pragma unroll
             for (int c = 0; c < CH; ++c) v[c] = nxt[c];
-            if (r + 1 < nrows) load_row(r + 1, nxt);       // prefetch next token
+            if (nx < nrb) load_row(nx, nxt);                 // prefetch next token
         } else {
-            load_row(r, v);
+            load_row(cur, v);
         }
-
         uint32_t cv[CH];                                     // packed int4 codes, 8 per chunk
         q4_row_packed<CH, BF16, CLIP1>(v, clip, cv);
         // packed int4 copy of the codes, when asked for (the Gram matrix of
         // the diversity stage is computed from it)
-        uint32_t *vrow = vcodes ? vcodes + ((int64_t)b * N + row0 + r) * (d / 8) : nullptr;
-        if (vrow) {
+        if (vcodes) {
+            uint32_t *vrow = vcodes + ((int64_t)b * N + row_begin + cur) * (d / 8);
 #pragma unroll
             for (int c = 0; c < CH; ++c)
                 if (lane + 64 * c < nchunk) vrow[lane + 64 * c] = cv[c];
@@ -288,27 +303,32 @@ __global__ __launch_bounds__(256, CH <= 8 ? 4 : 2) void k_select_score(const uin
         for (int j = 0; j < 8; ++j) part[j] = (j < JMAX) ? dj[j] : 0;
         if (JMAX < 8) part[JMAX < 8 ? J : 0] = nv;           // slot J holds Nv
         const int tot = reduce8(part, lane);                 // value (lane >> 3) of this row
-        if ((lane & 7) == r) myval = tot;
+        if ((lane & 7) == n) myval = tot;
         if (JMAX == 8) {
             int p2[8] = {nv, 0, 0, 0, 0, 0, 0, 0};
             const int nvt = reduce8(p2, lane);               // Nv in lanes 0..7
-            if ((lane & 7) == r) mynv = nvt;
+            if ((lane & 7) == n) mynv = nvt;
         }
-    }
-    // lane 8v + r now holds value v of row r: one stats word and one key each
-    const int r = lane & 7, vslot = lane >> 3;
-    const int nv_r = (JMAX == 8) ? __shfl(mynv, r) : __shfl(myval, 8 * J + r);
-    if (r < nrows) {
-        const int i = row0 + r;
-        int32_t *st = stats + ((int64_t)b * N + i) * (J + 1);
-        if (vslot < J) {
-            st[vslot] = myval;
-            keys[((int64_t)b * J + vslot) * N + i] = exact_key(myval, nv_r, LS);
-        } else if (vslot == J) {
-            st[J] = myval;
+        if (lane == n) rowid = cur;
+        ++n;
+        cur = nx;
+        if (n == kRowsPerWave || cur >= nrb) {               // wave-uniform
+            // one stats word and one key per lane
+            const int r = lane & 7, vslot = lane >> 3;
+            const int nv_r = (JMAX == 8) ? __shfl(mynv, r) : __shfl(myval, 8 * J + r);
+            const int i = row_begin + __shfl(rowid, r);
+            if (r < n) {
+                int32_t *st = stats + ((int64_t)b * N + i) * (J + 1);
+                if (vslot < J) {
+                    st[vslot] = myval;
+                    keys[((int64_t)b * J + vslot) * N + i] = exact_key(myval, nv_r, LS);
+                } else if (vslot == J) {
+                    st[J] = myval;
+                }
+                if (JMAX == 8 && vslot == 0) st[J] = nv_r;
+            }
+            n = 0;
         }
-        if (JMAX == 8 && vslot == 0) st[J] = nv_r;
-    }
     }
 }
 
@@ -682,25 +702,18 @@ __global__ __launch_bounds__(256) void k_select_gather(const uint4 *__restrict__
 template <int CH, int JMAX, bool BF16, bool CLIP1>
 hipError_t launch_score(int B, int N, int d, int J, float clip, int LS, const void *vis,
                         const void *concepts, const SelectWorkspace &ws, hipStream_t stream) {
+    constexpr int kWaves = score_waves<CH>();
     const size_t lds = (size_t)JMAX * 64 * CH * 4;
-    // Rows per wavefront: enough that the whole grid is resident at once
-    // (one wave of blocks, no partly filled last wave).
-    static std::atomic<int> per_cu_cache[kMaxDevices];   // blocks per CU, per instantiation
-    const int per_cu = per_device_cached(per_cu_cache, [lds](int) {
-        int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_select_score<CH, JMAX, BF16, CLIP1>, 256,
-                                                         lds) != hipSuccess || n <= 0)
-            n = 1;
-        return n;
-    });
-    const int resident = per_cu * device_cus();
-    const int64_t waves = 4LL * resident;
-    const int rpw = (int)std::max<int64_t>(1, ((int64_t)B * N + waves - 1) / waves);
-    const dim3 grid((N + 4 * rpw - 1) / (4 * rpw), B);
-    hipLaunchKernelGGL((k_select_score<CH, JMAX, BF16, CLIP1>), grid, dim3(256), lds, stream,
-                       static_cast<const uint8_t *>(vis), N, d, J, clip, LS, rpw,
-                       static_cast<const uint8_t *>(concepts), ws.stats,
-                       ws.keys, ws.vcodes);
+    // Blocks per sample: together one block per CU for the batch (the
+    // blocks hold the whole CU), at least 2 rows per wavefront.
+    const int cus = device_cus();
+    const int per_sample = (int)std::max<int64_t>(
+        1, std::min<int64_t>(((int64_t)cus + B - 1) / B, ((int64_t)N + 2 * kWaves - 1) / (2 * kWaves)));
+    const int rpb = (N + per_sample - 1) / per_sample;
+    const dim3 grid((N + rpb - 1) / rpb, B);
+    hipLaunchKernelGGL((k_select_score<CH, JMAX, BF16, CLIP1>), grid, dim3(64 * kWaves), lds, stream,
+                       static_cast<const uint8_t *>(vis), N, d, J, clip, LS, rpb,
+                       static_cast<const uint8_t *>(concepts), ws.stats, ws.keys, ws.vcodes);
     return hipGetLastError();
 }
 
