@@ -12,26 +12,39 @@ from gpu_util import Guarded, bits, check_canaries, first_mismatch, to_gpu, to_n
 pytestmark = pytest.mark.gpu
 
 
-def run_gpu(vis, con, text, K, dtype, clip=1.0):
+def run_gpu(vis, con, text, K, dtype, clip=1.0, ws=None, reps=3):
+    """`reps` calls on one workspace (filled with garbage first unless given):
+    nothing of an earlier call may leak into a later one, and rows are
+    claimed dynamically, so every call must give the same outputs bit for
+    bit; the last one's are returned."""
     B, N, d = vis.shape
     J = con.shape[1]
     vt, ct = to_gpu(vis, dtype), to_gpu(con, dtype)
     tt = None if text is None else to_gpu(text, dtype)
     T = 0 if text is None else text.shape[1]
-    ws = p4q.select_workspace(B, N, d, J, vt.device)
-    gi = Guarded((B, K), torch.int32, "idx_out")
-    gt = Guarded((B, K + T, d), vt.dtype, "tokens_out")
-    idx, tok = p4q.select(vt, ct, tt, K, clip, idx_out=gi.t, tokens_out=gt.t, workspace=ws)
-    torch.cuda.synchronize()
-    check_canaries(gi, gt)
-    stats = to_np(ws[: B * N * (J + 1) * 4].view(torch.int32)).reshape(B, N, J + 1)
-    return to_np(idx), to_np(tok), stats
+    if ws is None:
+        ws = p4q.select_workspace(B, N, d, J, vt.device)
+        ws.fill_(0xA5)
+    outs = []
+    for _ in range(reps):
+        gi = Guarded((B, K), torch.int32, "idx_out")
+        gt = Guarded((B, K + T, d), vt.dtype, "tokens_out")
+        idx, tok = p4q.select(vt, ct, tt, K, clip, idx_out=gi.t, tokens_out=gt.t, workspace=ws)
+        torch.cuda.synchronize()
+        check_canaries(gi, gt)
+        stats = to_np(ws[: B * N * (J + 1) * 4].view(torch.int32)).reshape(B, N, J + 1)
+        outs.append((to_np(idx), to_np(tok), stats))
+    for r in range(1, reps):
+        for a, b_, what in zip(outs[0], outs[r], ("idx", "tokens", "stats")):
+            assert np.array_equal(bits(a) if a.dtype.kind == "f" else a,
+                                  bits(b_) if b_.dtype.kind == "f" else b_), f"call {r} {what} differs"
+    return outs[-1]
 
 
-def check(vis, con, text, K, dtype="fp16", clip=1.0, samples=None):
+def check(vis, con, text, K, dtype="fp16", clip=1.0, samples=None, ws=None):
     B = vis.shape[0]
     T = 0 if text is None else text.shape[1]
-    idx, tok, stats = run_gpu(vis, con, text, K, dtype, clip)
+    idx, tok, stats = run_gpu(vis, con, text, K, dtype, clip, ws=ws)
     for b in (range(B) if samples is None else samples):
         tb = text[b] if T else np.zeros((0, vis.shape[2]), dtype=vis.dtype)
         ridx, rtok, D, Nv = oracle.select(vis[b], con[b], tb, K, dtype, clip)
@@ -124,3 +137,17 @@ def test_13b_shape_sampled():
     cfg = CONFIGS["stress13b_b8"]
     si = selector_inputs(cfg, samples=[0, 5])
     check(si.vis, si.concepts, si.text, cfg.K)
+
+
+def test_workspace_reused_for_another_shape():
+    """One workspace buffer for three shapes in turn (B*N kept, so the
+    internal offsets coincide): every call must match the oracle."""
+    d, J = 256, 3
+    ws = p4q.select_workspace(2, 300, d, J, torch.device("cuda:0"))
+    ws.fill_(0x5A)
+    v1, c1, t1 = synth(41, 1, 600, d, J, 4)
+    check(v1, c1, t1, 50, ws=ws)
+    v2, c2, t2 = synth(42, 2, 300, d, J, 4)
+    check(v2, c2, t2, 40, ws=ws)
+    v3, c3, t3 = synth(43, 1, 600, d, J, 4)
+    check(v3, c3, t3, 64, ws=ws)
