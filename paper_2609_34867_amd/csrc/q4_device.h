@@ -136,6 +136,71 @@ __device__ __forceinline__ void q4_chunk_fast(uint4 v, float r, uint32_t *out, u
     }
 }
 
+// Bracketed fast path for the 8 values of one 16-byte chunk.  With
+// r = fl32(1/s), rhi = fl32(r (1 + 2^-20)) and rlo = fl32(r (1 - 2^-20)),
+// x*rhi and x*rlo (each rounded once, inside the fma) enclose fl32(x/s):
+// r and fl32(x/s) each err by at most 2^-24 relative.  rne is monotone, so
+// where the two bracket ends round to the same integer so does fl32(x/s);
+// where they differ a half-integer lies inside and the exact path decides.
+// Two mixed-precision fmas and one three-input bitwise op per value: `dif`
+// collects lo ^ hi (nonzero: some bracket of this chunk straddles).  out[i]
+// low byte = code of value i (two's complement; clamped unless CLIP1, where
+// |x| <= amax keeps |x/s| <= 7).
+template <bool BF16, bool CLIP1>
+__device__ __forceinline__ void q4_chunk_bracket(uint4 v, float rhi, float rlo, uint32_t *out,
+                                                 uint32_t &dif) {
+    const uint32_t x4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const float x = h ? hi_f32<BF16>(x4[i]) : lo_f32<BF16>(x4[i]);
+            float tq = __builtin_fmaf(x, rhi, kRneMagic);
+            const float tl = __builtin_fmaf(x, rlo, kRneMagic);
+            // dif |= tq ^ tl (as asm: left to itself the compiler turns the
+            // merge into a compare and select per value)
+            asm("v_bitop3_b32 %0, %0, %1, %2 bitop3:0xf6"
+                : "+v"(dif)
+                : "v"(__float_as_uint(tq)), "v"(__float_as_uint(tl)));
+            if constexpr (!CLIP1) tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
+            out[2 * i + h] = __float_as_uint(tq);
+        }
+    }
+}
+
+// Largest |x| bit pattern (sign bit clear) among a lane's CH chunks.
+// fp16: a running packed maximum and minimum, each three-input op folding
+// two more words, then max(|max|, |min|) per half; bf16: 16-bit maxima of
+// the bit patterns with the sign masked.  Finite inputs.
+template <int CH, bool BF16>
+__device__ __forceinline__ uint32_t lane_absmax_bits(const uint4 *v) {
+    if constexpr (BF16) {
+        uint32_t m2 = 0;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
+        return max(m2 & 0xFFFFu, m2 >> 16);
+    } else {
+        uint32_t w[4 * CH];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            w[4 * c] = v[c].x;
+            w[4 * c + 1] = v[c].y;
+            w[4 * c + 2] = v[c].z;
+            w[4 * c + 3] = v[c].w;
+        }
+        uint32_t hi = w[0], lo = w[0];
+#pragma unroll
+        for (int k = 1; k < 4 * CH; k += 2) {
+            const uint32_t b = (k + 1 < 4 * CH) ? w[k + 1] : w[k];
+            asm("v_pk_maximum3_f16 %0, %0, %1, %2" : "+v"(hi) : "v"(w[k]), "v"(b));
+            asm("v_pk_minimum3_f16 %0, %0, %1, %2" : "+v"(lo) : "v"(w[k]), "v"(b));
+        }
+        // every |x| lies below max(|hi|, |lo|), per half
+        const uint32_t m2 = absmax2(absmax2(0u, hi), lo);
+        return max(m2 & 0xFFFFu, m2 >> 16);
+    }
+}
+
 template <bool BF16>
 __device__ __forceinline__ void q4_chunk_exact(uint4 v, float s, uint32_t *out) {
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};

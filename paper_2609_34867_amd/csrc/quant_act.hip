@@ -15,28 +15,6 @@ namespace {
 
 constexpr int kThreads = 256;      // one work-group (4 wavefronts) per row
 
-// Fast-path codes of one 16-byte chunk packed to eight nibbles; `fm` keeps
-// the largest |x*r - rne(x*r)| seen, so one comparison per lane afterwards
-// decides whether the exact path is needed (see q4_device.h).
-template <bool BF16, bool CLIP1>
-__device__ __forceinline__ uint32_t chunk_fast(uint4 v, float r, float &fm) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t c[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const float x = h ? hi_f32<BF16>(w[i]) : lo_f32<BF16>(w[i]);
-            float tq = __builtin_fmaf(x, r, kRneMagic);
-            const float q = tq - kRneMagic;
-            fm = __builtin_fmaxf(fm, __builtin_fabsf(__builtin_fmaf(x, r, -q)));
-            if constexpr (!CLIP1) tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
-            c[2 * i + h] = __float_as_uint(tq);
-        }
-    }
-    return pack_nibbles(c);
-}
-
 template <bool BF16>
 __device__ __forceinline__ uint32_t chunk_exact(uint4 v, float s) {
     uint32_t c[8];
@@ -64,10 +42,7 @@ __global__ __launch_bounds__(kThreads) void k_quant_act(const uint8_t *__restric
         const int q = t + kThreads * c;
         v[c] = (q < nchunk) ? load_nt(src + q) : make_uint4(0, 0, 0, 0);
     }
-    uint32_t m2 = 0;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
-    const uint32_t mw = wave_max_u32(max(m2 & 0xFFFFu, m2 >> 16));
+    const uint32_t mw = wave_max_u32(lane_absmax_bits<CH, BF16>(v));
     if ((t & 63) == 0) s_max[t >> 6] = mw;
     __syncthreads();
     const uint32_t mbits = max(max(s_max[0], s_max[1]), max(s_max[2], s_max[3]));
@@ -81,14 +56,19 @@ __global__ __launch_bounds__(kThreads) void k_quant_act(const uint8_t *__restric
     } else {
         const bool tiny = !(s >= kTinyScale);
         const float r = tiny ? 0.0f : 1.0f / s;
+        const float rhi = __fmul_rn(r, 1.0f + 0x1p-20f), rlo = __fmul_rn(r, 1.0f - 0x1p-20f);
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
-            float fm = 0.0f;
-            if (!tiny) packed[c] = chunk_fast<BF16, CLIP1>(v[c], r, fm);
-            // rare: a value of this chunk lies within 2^-19 of a rounding
-            // boundary in some lane (or the scale is tiny): recompute this
-            // chunk by exact division (wave-uniform branch)
-            if (tiny || __any(fm > kNearHalf)) {
+            uint32_t w[8];
+            uint32_t dif = 0u;
+            if (!tiny) {
+                q4_chunk_bracket<BF16, CLIP1>(v[c], rhi, rlo, w, dif);
+                packed[c] = pack_nibbles(w);
+            }
+            // rare: in some lane a bracket of this chunk straddles a
+            // rounding boundary (or the scale is tiny): recompute this chunk
+            // by exact division (wave-uniform branch)
+            if (tiny || __any(dif != 0u)) {
                 uint4 vc = v[c];
                 asm volatile("" : "+v"(vc.x), "+v"(vc.y), "+v"(vc.z), "+v"(vc.w));
                 packed[c] = chunk_exact<BF16>(vc, s);

@@ -89,39 +89,6 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t o
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
 }
 
-// Largest |x| bit pattern (sign bit clear) among this lane's CH chunks.
-// fp16: a running packed maximum and minimum, each three-input op folding
-// two more words, then max(|max|, |min|) per half; bf16: 16-bit maxima of
-// the bit patterns with the sign masked.  Finite inputs.
-template <int CH, bool BF16>
-__device__ __forceinline__ uint32_t lane_absmax_bits(const uint4 *v) {
-    if constexpr (BF16) {
-        uint32_t m2 = 0;
-#pragma unroll
-        for (int c = 0; c < CH; ++c) m2 = absmax_chunk(m2, v[c]);
-        return max(m2 & 0xFFFFu, m2 >> 16);
-    } else {
-        uint32_t w[4 * CH];
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            w[4 * c] = v[c].x;
-            w[4 * c + 1] = v[c].y;
-            w[4 * c + 2] = v[c].z;
-            w[4 * c + 3] = v[c].w;
-        }
-        uint32_t hi = w[0], lo = w[0];
-#pragma unroll
-        for (int k = 1; k < 4 * CH; k += 2) {
-            const uint32_t b = (k + 1 < 4 * CH) ? w[k + 1] : w[k];
-            asm("v_pk_maximum3_f16 %0, %0, %1, %2" : "+v"(hi) : "v"(w[k]), "v"(b));
-            asm("v_pk_minimum3_f16 %0, %0, %1, %2" : "+v"(lo) : "v"(w[k]), "v"(b));
-        }
-        // every |x| lies below max(|hi|, |lo|), per half
-        const uint32_t m2 = absmax2(absmax2(0u, hi), lo);
-        return max(m2 & 0xFFFFu, m2 >> 16);
-    }
-}
-
 // Q4 codes of one row held as CH 16-byte chunks per lane (lane l: chunks
 // l, l + 64, ...; zeros past the row end), packed 8 per word in value order.
 // absmax through the wavefront (no LDS), then the bracketed fast path with a
@@ -135,39 +102,14 @@ __device__ __forceinline__ void q4_row_packed(const uint4 *v, float clip, uint32
     if (s != 0.0f) {
         const bool tiny = !(s >= kTinyScale);
         const float rc = tiny ? 0.0f : 1.0f / s;
-        // Bracketed fast path: with r = fl32(1/s), x r(1 - 2^-20) and
-        // x r(1 + 2^-20) (products rounded once, inside the fma) enclose
-        // fl32(x/s), since r and fl32(x/s) each err by at most 2^-24
-        // relative.  rne is monotone, so where the two bracket ends round
-        // to the same integer, so does fl32(x/s); where they differ a
-        // half-integer lies inside and the exact path decides.  Two fmas
-        // and one bitwise merge per value.
+        // bracketed fast path (q4_chunk_bracket), exact division per chunk
+        // where a bracket straddles a rounding boundary
         const float rhi = __fmul_rn(rc, 1.0f + 0x1p-20f), rlo = __fmul_rn(rc, 1.0f - 0x1p-20f);
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
             uint32_t w[8];
             uint32_t dif = 0u;    // nonzero: a bracket of this chunk straddles a boundary
-            if (!tiny) {
-                const uint32_t x4[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-#pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const float x = h ? hi_f32<BF16>(x4[i]) : lo_f32<BF16>(x4[i]);
-                        float tq = __builtin_fmaf(x, rhi, kRneMagic);
-                        const float tl = __builtin_fmaf(x, rlo, kRneMagic);
-                        // dif |= tq ^ tl in one three-input bitwise op (as
-                        // asm: left to itself the compiler turns the merge
-                        // into a compare and select per value)
-                        asm("v_bitop3_b32 %0, %0, %1, %2 bitop3:0xf6"
-                            : "+v"(dif)
-                            : "v"(__float_as_uint(tq)), "v"(__float_as_uint(tl)));
-                        if constexpr (!CLIP1)
-                            tq = __builtin_amdgcn_fmed3f(tq, kRneMagic - 8.0f, kRneMagic + 7.0f);
-                        w[2 * i + h] = __float_as_uint(tq);
-                    }
-                }
-            }
+            if (!tiny) q4_chunk_bracket<BF16, CLIP1>(v[c], rhi, rlo, w, dif);
             // wave-uniform and rare: some lane holds a value of this chunk
             // next to a rounding boundary (exact fp16 ratios such as x = a/2
             // land on ties), or the scale is tiny.  Only this chunk is
