@@ -494,7 +494,7 @@ __device__ __forceinline__ v4i unpack2(uint32_t w0, uint32_t w1) {
 // blockIdx.y selects one problem of a batch (A, W, acc_out advanced by their
 // strides).
 template <int BMT, bool BF16OUT, bool ACC, bool YOUT, bool SPLIT>
-__global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restrict__ A,
+__global__ __launch_bounds__(256, BMT == 64 ? 4 : 2) void k_w4a4_gemm_2cu(const uint8_t *__restrict__ A,
                                                           const float *__restrict__ sa,
                                                           const uint8_t *__restrict__ W,
                                                           const float *__restrict__ sw, int M,
@@ -505,7 +505,7 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
                                                           int64_t a_bstride, int64_t w_bstride,
                                                           int64_t acc_bstride, int kps,
                                                           int32_t *__restrict__ part) {
-    static_assert(BMT == 256 || (BMT == 128 && YOUT), "tile height");
+    static_assert(BMT == 256 || ((BMT == 128 || BMT == 64) && YOUT), "tile height");
     static_assert(!SPLIT || (YOUT && !ACC), "split-K stores partial sums only");
     constexpr int L_STAGE = l_stage<BMT>();
     constexpr int AI = BMT / 64;          // A DMA instructions per wavefront and stage
@@ -581,9 +581,12 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         if constexpr (BMT == 256) {
             dma4(dSa, (uint32_t)(64 * wave + lane) * 4u, sbase + wave_u * 256);
             if (wave_u < 2) dma4(dSw, (uint32_t)(64 * wave + lane) * 4u, sbase + 1024 + wave_u * 256);
-        } else {                      // 128 + 128 scales: waves 0, 1 and 2, 3
+        } else if constexpr (BMT == 128) {   // 128 + 128 scales: waves 0, 1 and 2, 3
             if (wave_u < 2) dma4(dSa, (uint32_t)(64 * wave + lane) * 4u, sbase + wave_u * 256);
             else dma4(dSw, (uint32_t)(64 * (wave - 2) + lane) * 4u, sbase + 512 + (wave_u - 2) * 256);
+        } else {                             // 64 + 128 scales: wave 0 and waves 1, 2
+            if (wave_u == 0) dma4(dSa, (uint32_t)lane * 4u, sbase);
+            else if (wave_u < 3) dma4(dSw, (uint32_t)(64 * (wave - 1) + lane) * 4u, sbase + 256 + (wave_u - 1) * 256);
         }
     }
     constexpr int NST = l_stages<BMT>();
@@ -637,11 +640,17 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_2cu(const uint8_t *__restr
         if constexpr (BMT == 256) {
             if (ahead >= 1) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
             else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-        } else {
+        } else if constexpr (BMT == 128) {
             static_assert(l_stages<BMT>() <= 5, "wait counts below cover at most 3 tiles ahead");
             if (ahead >= 3) asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
             else if (ahead == 2) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
             else if (ahead == 1) asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+        } else {                                  // BMT = 64: 3 instructions per tile
+            static_assert(l_stages<BMT>() <= 5, "wait counts below cover at most 3 tiles ahead");
+            if (ahead >= 3) asm volatile("s_waitcnt vmcnt(9)\n\ts_barrier" ::: "memory");
+            else if (ahead == 2) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
+            else if (ahead == 1) asm volatile("s_waitcnt vmcnt(3)\n\ts_barrier" ::: "memory");
             else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
         }
         if (kt + NST - 1 < ktiles) issue((kt + NST - 1) % NST, kbeg + kt + NST - 1);
@@ -1252,24 +1261,38 @@ __global__ __launch_bounds__(64 * NW) void k_w4a4_gemv(const uint8_t *__restrict
 // Dispatch of the prefill shapes (M > 16):
 //  * M >= 1024 and N >= 1024: 256 x 128 tiles, two blocks per CU, persistent
 //    over their tiles (k_w4a4_gemm_pt);
-//  * M < 1024 and N >= 1024 (one image's pruned sequence): the same kernel
-//    with 128 x 128 tiles; launches with fewer tiles than CUs split K across
-//    work-groups (mid_splits), given the caller's workspace;
+//  * M < 1024 and N >= 1024 (one image's pruned sequence): k_w4a4_gemm_2cu
+//    with 128 x 128 tiles, or 64 x 128 (mid_bm); launches with fewer tiles
+//    than CUs split K across work-groups (mid_splits), given the caller's
+//    workspace;
 //  * anything narrower: the small-M kernel, split the same way
 //    (small_m_splits).
 static bool use_large_tiles(int M, int N) { return M >= 1024 && N >= 1024; }
 static bool use_mid_tiles(int M, int N) { return M > 16 && M < 1024 && N >= 1024; }
 
-// Mid-tile launches with fewer 128 x 128 tiles than CUs split K into S
-// slices: S = 512 / tiles (two resident work-groups per CU), at most 8, and
-// each slice at least 16 k-tiles of 128: every slice adds M N 4 bytes of
-// partial sums written and read back, which outweighs the extra
-// parallelism below that (measured at M = 384 / 704: o_proj, K = 4096, is
-// fastest at 2 slices; down_proj, K = 11008, at 4-5).  N % 4 == 0
-// (partials are stored 4 at a time).
+// Tile height of the mid path: 128 rows, or 64 where 128-row tiles would
+// leave CUs idle (fewer than 256 tiles) and K_in <= 4096.  64-row tiles
+// are less efficient per tile (their fragment reads per MFMA double), but
+// for short K they beat splitting K: measured at M = 704, N = 4096,
+// K = 4096: 21.5 us unsplit with 352 tiles of 64 rows against 27.7 us
+// with 192 tiles of 128 split in two; at M = 384: 18.8 against 19.6 us.
+// Everywhere else (q|k|v, gate|up, down at M = 384 / 704) 128 rows were
+// faster by 6-17%.
+static int mid_bm(int M, int N, int K) {
+    const int64_t tiles128 = (((int64_t)M + 127) / 128) * (((int64_t)N + L_BN - 1) / L_BN);
+    return (tiles128 < 256 && K <= 4096) ? 64 : 128;
+}
+
+// Mid-tile launches with fewer tiles (of the height above) than CUs split K
+// into S slices: S = 512 / tiles, at most 8, and each slice at least 16
+// k-tiles of 128: every slice adds M N 4 bytes of partial sums written and
+// read back, which outweighs the extra parallelism below that (measured at
+// M = 384 / 704: down_proj, K = 11008, is fastest at 4-5 slices).
+// N % 4 == 0 (partials are stored 4 at a time).
 static int mid_splits(int M, int N, int K) {
     if (!use_mid_tiles(M, N) || N % 4 != 0) return 1;
-    const int64_t tiles = (((int64_t)M + 127) / 128) * (((int64_t)N + L_BN - 1) / L_BN);
+    const int bm = mid_bm(M, N, K);
+    const int64_t tiles = (((int64_t)M + bm - 1) / bm) * (((int64_t)N + L_BN - 1) / L_BN);
     if (tiles >= 256) return 1;
     const int kt_all = (K / 2 + BKB - 1) / BKB;
     int S = (int)(512 / tiles);
@@ -1331,7 +1354,7 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
     const unsigned eb = (unsigned)(((int64_t)M * N / 4 + 255) / 256);   // split-K epilogue blocks
     if (use_large_tiles(M, N) || use_mid_tiles(M, N)) {
         const bool large = use_large_tiles(M, N);
-        const int bm = large ? L_BM : 128;
+        const int bm = large ? L_BM : mid_bm(M, N, K);
         const int tiles_m = (M + bm - 1) / bm, tiles_n = (N + L_BN - 1) / L_BN;
         const int T = tiles_m * tiles_n;
         const int S = large ? 1 : mid_splits(M, N, K);
@@ -1339,9 +1362,14 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
             const int kt_all = (K / 2 + BKB - 1) / BKB, kps = (kt_all + S - 1) / S;
             const int Sr = (kt_all + kps - 1) / kps;          // every slice non-empty
             int32_t *part = static_cast<int32_t *>(ws);
-            hipLaunchKernelGGL((k_w4a4_gemm_2cu<128, false, false, true, true>), dim3(T, Sr),
-                               dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy, acc_out,
-                               tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0, kps, part);
+            if (bm == 64)
+                hipLaunchKernelGGL((k_w4a4_gemm_2cu<64, false, false, true, true>), dim3(T, Sr),
+                                   dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy, acc_out,
+                                   tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0, kps, part);
+            else
+                hipLaunchKernelGGL((k_w4a4_gemm_2cu<128, false, false, true, true>), dim3(T, Sr),
+                                   dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy, acc_out,
+                                   tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0, kps, part);
             if (bf16)
                 hipLaunchKernelGGL(k_splitk_epilogue<true>, dim3(eb), dim3(256), 0, stream, part, Sr,
                                    M, N, sa, sw, y, ldy, acc_out);
@@ -1372,6 +1400,7 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
             if (bf16) return acc_out ? gp(k_w4a4_gemm_pt<true, true>) : gp(k_w4a4_gemm_pt<true, false>);
             return acc_out ? gp(k_w4a4_gemm_pt<false, true>) : gp(k_w4a4_gemm_pt<false, false>);
         }
+        if (bm == 64) { P4Q_TILES(64) }
         P4Q_TILES(128)
 #undef P4Q_TILES
     }

@@ -281,14 +281,16 @@ def test_decode_graph_replay_matches_eager():
         del junk
 
 
-@pytest.mark.parametrize("shape", [(384, 4096, 11008), (256, 4096, 4096), (96, 512, 4096),
-                                   (704, 4096, 4096)])
-def test_small_m_split_k(shape):
+@pytest.mark.parametrize("shape,split", [((384, 4096, 11008), True), ((256, 4096, 4096), True),
+                                         ((96, 512, 4096), True), ((704, 4096, 11008), True),
+                                         ((384, 4096, 4096), True), ((704, 4096, 4096), False)])
+def test_small_m_split_k(shape, split):
     """Batch-1 shapes (one image's pruned sequence): fewer 128 x 128 tiles
-    than CUs, so K is split across work-groups when the workspace is given.
-    Both paths must equal the oracle bit for bit."""
+    than CUs, so K is split across work-groups when the workspace is given,
+    or (K_in <= 4096) 64-row tiles fill the CUs instead, unsplit where they
+    are enough.  Both paths must equal the oracle bit for bit."""
     M, N, K = shape
-    assert p4q.lib().p4q_w4a4_linear_workspace_bytes(M, N, K) > 0
+    assert (p4q.lib().p4q_w4a4_linear_workspace_bytes(M, N, K) > 0) == split
     ap, sa, wp, sw = codes_for(M, N, K, seed=M + N)
     racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
     dev = torch.device("cuda:0")
