@@ -371,11 +371,17 @@ int p4q_calib_block_grad(p4q_dtype dt, int M, int d, int f, int H, const void *x
  *   [N_out]; y [M, ldy] of out_dt; acc_out int32 [M, N_out] or NULL (when
  *   given, the raw accumulators are stored too).
  * Workspace (optional): p4q_w4a4_linear_workspace_bytes(M, N_out, K_in)
- *   bytes, 16-byte aligned.  It is nonzero for small M (fewer 128 x 128
- *   output tiles than CUs, M < 1024): given that much, the call splits K
- *   across work-groups and sums the exact int32 partials in a second kernel;
- *   with ws NULL, smaller or misaligned it runs unsplit.  The results are
- *   identical either way (integer sums).
+ *   bytes, 16-byte aligned.  It is nonzero for M < 1024 when the output
+ *   tiles do not divide evenly over the CUs: given that much, the call
+ *   splits K of the tiles past the last whole round across work-groups,
+ *   which meet in the workspace (exact int32 partial sums; the last to
+ *   arrive writes the tile), or, below 128 x 128 tiles, sums the slices in
+ *   a second kernel.  With ws NULL, smaller or misaligned the call runs
+ *   unsplit.  The results are identical either way (integer sums).  The
+ *   first 4096 bytes hold per-tile arrival counters: they must be zero
+ *   before the first call that uses the workspace (allocate it
+ *   zero-filled), and every call leaves them zero.  Calls that share a
+ *   workspace must not overlap.
  * Limits: M >= 1, N_out >= 1, K_in % 32 == 0, 32 <= K_in <= 131072,
  *   ldy >= N_out; code pointers 16-byte aligned, y 4-byte aligned.
  * ---------------------------------------------------------------------- */

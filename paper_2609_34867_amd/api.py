@@ -441,7 +441,9 @@ def calib_block_grad(x: torch.Tensor, target: torch.Tensor, w_qkv: torch.Tensor,
 # --------------------------------------------------------------------------- W4A4 linear
 def w4a4_linear_workspace(M: int, N_out: int, K_in: int, device) -> Optional[torch.Tensor]:
     n = lib().p4q_w4a4_linear_workspace_bytes(M, N_out, K_in)
-    return None if n == 0 else torch.empty(n, dtype=torch.uint8, device=device)
+    # zero-filled: its head holds arrival counters that must start at zero
+    # (every call leaves them zero again)
+    return None if n == 0 else torch.zeros(n, dtype=torch.uint8, device=device)
 
 
 def w4a4_linear(a_codes: torch.Tensor, a_scales: torch.Tensor, w_codes: torch.Tensor,

@@ -1465,6 +1465,8 @@ hipError_t calib_block_run(int M, int d, int f, int H, const uint16_t *x, const 
     const int rows = H * M;
 
     // ---- forward
+    // the forward GEMMs' split-K arrival counters live in this call's workspace
+    if ((e = gemm_workspace_clear(b.gemm_ws, b.gemm_ws_bytes, stream)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_blk_rmsnorm, dim3(M), dim3(kThreads), 0, stream, x, d, gamma1, eps, b.n1,
                        b.r1);
     if ((e = group_forward(b.g[kGQkv], M, b.n1, w[kGQkv], sg[kGQkv], clip_a[kGQkv],

@@ -133,6 +133,10 @@ hipError_t launch_calib_block(int M, int d, int f, int H, const void *x, const f
 hipError_t launch_code_gram(int B, int n, int k, const uint8_t *codes, int32_t *G,
                             hipStream_t stream);
 size_t gemm_workspace_bytes(int M, int N, int K);
+// Zeroes the arrival counters at the head of a GEMM workspace (a fill kernel
+// on the stream; the GEMM calls leave them zero, so this is needed once per
+// workspace whose contents are not known to be zero).
+hipError_t gemm_workspace_clear(void *ws, size_t ws_bytes, hipStream_t stream);
 hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *sa,
                             const uint8_t *w, const float *sw, p4q_dtype out_dt, void *y,
                             int64_t ldy, int32_t *acc_out, void *ws, size_t ws_bytes,

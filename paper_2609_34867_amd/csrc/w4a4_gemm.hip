@@ -504,9 +504,11 @@ __global__ __launch_bounds__(256, BMT == 64 ? 4 : 2) void k_w4a4_gemm_2cu(const 
                                                           int tiles_m, int tiles_n,
                                                           int64_t a_bstride, int64_t w_bstride,
                                                           int64_t acc_bstride, int kps,
-                                                          int32_t *__restrict__ part) {
+                                                          int32_t *__restrict__ part, int tdp,
+                                                          int nsplit,
+                                                          uint32_t *__restrict__ arrivals) {
     static_assert(BMT == 256 || ((BMT == 128 || BMT == 64) && YOUT), "tile height");
-    static_assert(!SPLIT || (YOUT && !ACC), "split-K stores partial sums only");
+    static_assert(!SPLIT || YOUT, "split-K is a mode of the y-output kernel");
     constexpr int L_STAGE = l_stage<BMT>();
     constexpr int AI = BMT / 64;          // A DMA instructions per wavefront and stage
     constexpr int AF = BMT / 32;          // A fragments (16 rows) per wavefront
@@ -518,14 +520,23 @@ __global__ __launch_bounds__(256, BMT == 64 ? 4 : 2) void k_w4a4_gemm_2cu(const 
         if constexpr (ACC) acc_out += blockIdx.y * acc_bstride;
     }
     const int wm = wave >> 1, wn = wave & 1;
-    int tm, tn, split = 0;
+    int tm, tn, split = 0, rslot = 0;
+    bool slice = false;                   // SPLIT: this block covers one k-range of a tile
     if constexpr (YOUT) {
         const int T = tiles_m * tiles_n;
-        int logical = xcd_logical((int)(blockIdx.x + (SPLIT ? blockIdx.y * gridDim.x : 0u)),
-                                  SPLIT ? T * (int)gridDim.y : T);
+        int logical;
         if constexpr (SPLIT) {
-            split = logical / T;
-            logical -= split * T;
+            const int b = (int)blockIdx.x;
+            if (b < tdp) {
+                logical = xcd_logical(b, tdp);
+            } else {
+                slice = true;
+                rslot = (b - tdp) / nsplit;
+                split = b - tdp - rslot * nsplit;
+                logical = tdp + rslot;
+            }
+        } else {
+            logical = xcd_logical((int)blockIdx.x, T);
         }
         grouped_tile(logical, tiles_m, tiles_n, tm, tn);
     } else {
@@ -534,8 +545,8 @@ __global__ __launch_bounds__(256, BMT == 64 ? 4 : 2) void k_w4a4_gemm_2cu(const 
     const int m0 = tm * BMT, n0 = tn * L_BN;
     // this block's k-tiles [kbeg, kbeg + ktiles); the launch makes every split non-empty
     const int ktiles_all = (Kb + BKB - 1) / BKB;
-    const int kbeg = SPLIT ? split * kps : 0;
-    const int ktiles = SPLIT ? min(ktiles_all - kbeg, kps) : ktiles_all;
+    const int kbeg = slice ? split * kps : 0;
+    const int ktiles = slice ? min(ktiles_all - kbeg, kps) : ktiles_all;
 
     const v4i dA = buffer_desc(A + (int64_t)m0 * Kb, (uint32_t)(min(M - m0, BMT) * Kb));
     const v4i dW = buffer_desc(W + (int64_t)n0 * Kb, (uint32_t)(min(N - n0, L_BN) * Kb));
@@ -574,7 +585,7 @@ __global__ __launch_bounds__(256, BMT == 64 ? 4 : 2) void k_w4a4_gemm_2cu(const 
         }
     };
 
-    if constexpr (YOUT && !SPLIT) {   // the block's scales -> LDS (zeros past M / N), ahead of the stages
+    if constexpr (YOUT) {             // the block's scales -> LDS (zeros past M / N), ahead of the stages
         const v4i dSa = buffer_desc(sa + m0, (uint32_t)(min(M - m0, BMT) * 4));
         const v4i dSw = buffer_desc(sw + n0, (uint32_t)(min(N - n0, L_BN) * 4));
         const uint32_t sbase = lds_addr(smem) + l_scale_off<BMT>();
@@ -674,21 +685,55 @@ __global__ __launch_bounds__(256, BMT == 64 ? 4 : 2) void k_w4a4_gemm_2cu(const 
         __builtin_amdgcn_s_setprio(0);
     }
 
-    if constexpr (SPLIT) {      // this slice's exact partial sums: part[split][m][n]
-        int32_t *pz = part + (int64_t)split * M * N;
+    if constexpr (SPLIT) {
+        // A slice block stores its raw accumulators (256 x the exact partial
+        // sums; each store instruction covers 256 consecutive bytes) to its
+        // own slot of the workspace and
+        // counts itself in on the tile's arrival counter; the block that
+        // arrives last adds the other slices' sums to its own and goes on to
+        // the epilogue, and puts the counter back to zero, so the counters
+        // are zero again after every call.  The partial sums move as
+        // agent-scope (device-coherent) atomic stores and loads, and every
+        // store has completed (vmcnt(0)) before the block counts itself in,
+        // so no L2 write-back or invalidation of the whole cache is needed
+        // (agent-scope fences cost this launch more than twice its time).
+        if (slice) {
+            __shared__ int s_last;
+            constexpr int SLICE_V4 = 32 * BMT;              // v4i per slice (BMT x 128 int32)
+            int32_t *const rp = part + (int64_t)rslot * nsplit * SLICE_V4 * 4;
+            int32_t *const mine = rp + (int64_t)split * SLICE_V4 * 4;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int nb = n0 + wn * 64 + 16 * i + 4 * cq;         // N % 4 == 0
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < AF; ++j) {
-                const int m = m0 + wm * (BMT / 2) + 16 * j + r16;
-                if (m < M && nb < N)
-                    *reinterpret_cast<int4 *>(pz + (int64_t)m * N + nb) =
-                        make_int4(acc[i][j][0] >> 8, acc[i][j][1] >> 8, acc[i][j][2] >> 8,
-                                  acc[i][j][3] >> 8);
+                for (int j = 0; j < AF; ++j)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        __hip_atomic_store(mine + ((((wave * 4 + i) * AF + j) * 4 + e) << 6) + lane,
+                                           acc[i][j][e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            if (t == 0) {
+                const uint32_t before = __hip_atomic_fetch_add(arrivals + rslot, 1u, __ATOMIC_RELAXED,
+                                                               __HIP_MEMORY_SCOPE_AGENT);
+                s_last = (before == (uint32_t)(nsplit - 1));
+                if (s_last) __hip_atomic_store(arrivals + rslot, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            __syncthreads();
+            if (!s_last) return;
+            for (int z = 0; z < nsplit; ++z) {
+                if (z == split) continue;
+                const int32_t *src = rp + (int64_t)z * SLICE_V4 * 4;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < AF; ++j)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            acc[i][j][e] += __hip_atomic_load(
+                                src + ((((wave * 4 + i) * AF + j) * 4 + e) << 6) + lane, __ATOMIC_RELAXED,
+                                __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        return;
     }
 
     if constexpr (!YOUT) {      // Gram mode: int32 accumulators only
@@ -1262,11 +1307,11 @@ __global__ __launch_bounds__(64 * NW) void k_w4a4_gemv(const uint8_t *__restrict
 //  * M >= 1024 and N >= 1024: 256 x 128 tiles, two blocks per CU, persistent
 //    over their tiles (k_w4a4_gemm_pt);
 //  * M < 1024 and N >= 1024 (one image's pruned sequence): k_w4a4_gemm_2cu
-//    with 128 x 128 tiles, or 64 x 128 (mid_bm); launches with fewer tiles
-//    than CUs split K across work-groups (mid_splits), given the caller's
-//    workspace;
-//  * anything narrower: the small-M kernel, split the same way
-//    (small_m_splits).
+//    with 128 x 128 tiles, or 64 x 128 (mid_bm); given the caller's
+//    workspace, the tiles past the last whole round per CU are split along
+//    K and reduced in the kernel (mid_plan);
+//  * anything narrower: the small-M kernel, whose K slices are summed by a
+//    second kernel (small_m_splits).
 static bool use_large_tiles(int M, int N) { return M >= 1024 && N >= 1024; }
 static bool use_mid_tiles(int M, int N) { return M > 16 && M < 1024 && N >= 1024; }
 
@@ -1283,22 +1328,54 @@ static int mid_bm(int M, int N, int K) {
     return (tiles128 < 256 && K <= 4096) ? 64 : 128;
 }
 
-// Mid-tile launches with fewer tiles (of the height above) than CUs split K
-// into S slices: S = 512 / tiles, at most 8, and each slice at least 16
-// k-tiles of 128: every slice adds M N 4 bytes of partial sums written and
-// read back, which outweighs the extra parallelism below that (measured at
-// M = 384 / 704: down_proj, K = 11008, is fastest at 4-5 slices).
-// N % 4 == 0 (partials are stored 4 at a time).
-static int mid_splits(int M, int N, int K) {
-    if (!use_mid_tiles(M, N) || N % 4 != 0) return 1;
-    const int bm = mid_bm(M, N, K);
-    const int64_t tiles = (((int64_t)M + bm - 1) / bm) * (((int64_t)N + L_BN - 1) / L_BN);
-    if (tiles >= 256) return 1;
-    const int kt_all = (K / 2 + BKB - 1) / BKB;
-    int S = (int)(512 / tiles);
-    S = std::min(S, 8);
-    S = std::min(S, kt_all / 16);
-    return std::max(S, 1);
+// Split plan of the mid-tile launches (needs the caller's workspace).  The
+// tiles are dealt as whole tiles per CU as far as they go; the last T % C
+// tiles (C = CUs), or all of them when T < C, are split along K into S slices
+// whose blocks meet in the workspace (the last to arrive adds the others'
+// exact int32 sums and writes the tile), so every CU gets about the same
+// share of k-tiles:
+//  * T < C: S = 512 / T, at most 8, each slice at least 16 k-tiles of 128
+//    (measured at M = 384 / 704: down_proj, K = 11008, is fastest at 4-5
+//    slices; every slice adds 64 KB of partial sums per tile written and
+//    read back);
+//  * T >= C: S = C / (T % C), at most 8, each slice at least 4 k-tiles.
+//    A whole last round of T % C tiles on as many CUs costs a batch-1 layer
+//    ~14 us of ~118 (timed with the remainder tiles left out).
+struct MidPlan {
+    int bm, T, tdp, rem, S, kps;   // tiles [tdp, T) split into S slices of kps k-tiles
+};
+static MidPlan mid_plan(int M, int N, int K) {
+    MidPlan p{};
+    p.bm = mid_bm(M, N, K);
+    const int64_t T64 = (((int64_t)M + p.bm - 1) / p.bm) * (((int64_t)N + L_BN - 1) / L_BN);
+    p.T = (int)std::min<int64_t>(T64, 1 << 30);
+    p.tdp = p.T;
+    p.S = 1;
+    const int kt_all = (int)(((int64_t)K / 2 + BKB - 1) / BKB);
+    p.kps = kt_all;
+    if (!use_mid_tiles(M, N) || T64 >= (1 << 30)) return p;
+    const int cus = device_cus();
+    int S, rem;
+    if (p.T < cus) {
+        rem = p.T;
+        S = std::min(std::min(512 / p.T, 8), kt_all / 16);
+    } else {
+        rem = p.T % cus;
+        if (rem == 0) return p;
+        S = std::min(std::min(cus / rem, 8), kt_all / 4);
+    }
+    if (S < 2) return p;
+    p.kps = (kt_all + S - 1) / S;
+    p.S = (kt_all + p.kps - 1) / p.kps;              // every slice non-empty
+    p.rem = rem;
+    p.tdp = p.T - rem;
+    return p;
+}
+// workspace of a split mid launch: arrival counters (zero between calls),
+// then one BM x 128 int32 slot per slice
+constexpr size_t kArrivalBytes = 4096;
+static size_t mid_split_bytes(const MidPlan &p) {
+    return p.S > 1 ? kArrivalBytes + (size_t)p.rem * p.S * p.bm * L_BN * 4 : 0;
 }
 
 // Small-M shapes with fewer 128 x 128 tiles than CUs split K across
@@ -1317,8 +1394,24 @@ static int small_m_splits(int M, int N, int K) {
     return std::max(S, 1);
 }
 
+namespace {
+__global__ __launch_bounds__(256) void k_clear_words(uint32_t *__restrict__ p, int n) {
+    const int i = (int)(blockIdx.x * 256 + threadIdx.x);
+    if (i < n) p[i] = 0u;
+}
+}  // namespace
+
+hipError_t gemm_workspace_clear(void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (!ws || ws_bytes < kArrivalBytes) return hipSuccess;
+    const int n = (int)(kArrivalBytes / 4);
+    hipLaunchKernelGGL(k_clear_words, dim3((n + 255) / 256), dim3(256), 0, stream,
+                       static_cast<uint32_t *>(ws), n);
+    return hipGetLastError();
+}
+
 size_t gemm_workspace_bytes(int M, int N, int K) {
-    const int S = use_mid_tiles(M, N) ? mid_splits(M, N, K) : small_m_splits(M, N, K);
+    if (use_mid_tiles(M, N)) return mid_split_bytes(mid_plan(M, N, K));
+    const int S = small_m_splits(M, N, K);
     return S > 1 ? (size_t)S * M * N * 4 : 0;
 }
 
@@ -1354,34 +1447,33 @@ hipError_t launch_w4a4_gemm(int M, int N, int K, const uint8_t *a, const float *
     const unsigned eb = (unsigned)(((int64_t)M * N / 4 + 255) / 256);   // split-K epilogue blocks
     if (use_large_tiles(M, N) || use_mid_tiles(M, N)) {
         const bool large = use_large_tiles(M, N);
-        const int bm = large ? L_BM : mid_bm(M, N, K);
+        const MidPlan plan = large ? MidPlan{} : mid_plan(M, N, K);
+        const int bm = large ? L_BM : plan.bm;
         const int tiles_m = (M + bm - 1) / bm, tiles_n = (N + L_BN - 1) / L_BN;
         const int T = tiles_m * tiles_n;
-        const int S = large ? 1 : mid_splits(M, N, K);
-        if (S > 1 && ws_ok) {
-            const int kt_all = (K / 2 + BKB - 1) / BKB, kps = (kt_all + S - 1) / S;
-            const int Sr = (kt_all + kps - 1) / kps;          // every slice non-empty
-            int32_t *part = static_cast<int32_t *>(ws);
-            if (bm == 64)
-                hipLaunchKernelGGL((k_w4a4_gemm_2cu<64, false, false, true, true>), dim3(T, Sr),
-                                   dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy, acc_out,
-                                   tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0, kps, part);
-            else
-                hipLaunchKernelGGL((k_w4a4_gemm_2cu<128, false, false, true, true>), dim3(T, Sr),
-                                   dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy, acc_out,
-                                   tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0, kps, part);
-            if (bf16)
-                hipLaunchKernelGGL(k_splitk_epilogue<true>, dim3(eb), dim3(256), 0, stream, part, Sr,
-                                   M, N, sa, sw, y, ldy, acc_out);
-            else
-                hipLaunchKernelGGL(k_splitk_epilogue<false>, dim3(eb), dim3(256), 0, stream, part, Sr,
-                                   M, N, sa, sw, y, ldy, acc_out);
-            return hipGetLastError();
+        if (!large && plan.S > 1 && ws_ok) {
+            uint32_t *arrivals = static_cast<uint32_t *>(ws);
+            int32_t *part = reinterpret_cast<int32_t *>(static_cast<uint8_t *>(ws) + kArrivalBytes);
+            const dim3 grid((unsigned)(plan.tdp + plan.rem * plan.S));
+            auto gs = [&](auto kern) {
+                hipLaunchKernelGGL(kern, grid, dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy,
+                                   acc_out, tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0,
+                                   plan.kps, part, plan.tdp, plan.S, arrivals);
+                return hipGetLastError();
+            };
+#define P4Q_SPLIT(BMT)                                                                        \
+    if (bf16) return acc_out ? gs(k_w4a4_gemm_2cu<BMT, true, true, true, true>)                \
+                             : gs(k_w4a4_gemm_2cu<BMT, true, false, true, true>);             \
+    return acc_out ? gs(k_w4a4_gemm_2cu<BMT, false, true, true, true>)                         \
+                   : gs(k_w4a4_gemm_2cu<BMT, false, false, true, true>);
+            if (bm == 64) { P4Q_SPLIT(64) }
+            P4Q_SPLIT(128)
+#undef P4Q_SPLIT
         }
         auto go = [&](auto kern) {
             hipLaunchKernelGGL(kern, dim3(T), dim3(256), 0, stream, a, sa, w, sw, M, N, K / 2, y, ldy,
                                acc_out, tiles_m, tiles_n, (int64_t)0, (int64_t)0, (int64_t)0, 0,
-                               (int32_t *)nullptr);
+                               (int32_t *)nullptr, 0, 1, (uint32_t *)nullptr);
             return hipGetLastError();
         };
 #define P4Q_TILES(BMT)                                                                        \
@@ -1445,7 +1537,7 @@ hipError_t launch_code_gram(int B, int n, int k, const uint8_t *codes, int32_t *
         hipLaunchKernelGGL((k_w4a4_gemm_2cu<256, true, true, false, false>), dim3(upper, B),
                            dim3(256), 0, stream, codes, nullptr, codes, nullptr, n, n, kb, nullptr,
                            (int64_t)n, G, upper, tiles_n, (int64_t)n * kb, (int64_t)n * kb,
-                           (int64_t)n * n, 0, (int32_t *)nullptr);
+                           (int64_t)n * n, 0, (int32_t *)nullptr, 0, 1, (uint32_t *)nullptr);
         return hipGetLastError();
     }
     const dim3 grid((n + BN - 1) / BN, (n + BM - 1) / BM);

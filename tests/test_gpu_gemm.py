@@ -283,26 +283,36 @@ def test_decode_graph_replay_matches_eager():
 
 @pytest.mark.parametrize("shape,split", [((384, 4096, 11008), True), ((256, 4096, 4096), True),
                                          ((96, 512, 4096), True), ((704, 4096, 11008), True),
-                                         ((384, 4096, 4096), True), ((704, 4096, 4096), False)])
+                                         ((384, 4096, 4096), True), ((704, 4096, 4096), True),
+                                         ((384, 12288, 4096), True), ((520, 8200, 2080), True),
+                                         ((512, 16384, 4096), False)])
 def test_small_m_split_k(shape, split):
-    """Batch-1 shapes (one image's pruned sequence): fewer 128 x 128 tiles
-    than CUs, so K is split across work-groups when the workspace is given,
-    or (K_in <= 4096) 64-row tiles fill the CUs instead, unsplit where they
-    are enough.  Both paths must equal the oracle bit for bit."""
+    """Batch-1 shapes (one image's pruned sequence).  Given the workspace,
+    the tiles past the last whole round per CU (all of them when there are
+    fewer tiles than CUs) are split along K across work-groups that meet in
+    the workspace; (K_in <= 4096) 64-row tiles fill the CUs where 128-row
+    tiles are too few; 512 tiles of 128 x 128 divide evenly and run
+    unsplit.  (520, 8200, 2080): ragged in M, N and the last k-tile, with
+    256 whole tiles and 69 split in three.  Every path must equal the
+    oracle bit for bit."""
     M, N, K = shape
     assert (p4q.lib().p4q_w4a4_linear_workspace_bytes(M, N, K) > 0) == split
     ap, sa, wp, sw = codes_for(M, N, K, seed=M + N)
     racc, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
     dev = torch.device("cuda:0")
     empty = torch.empty(0, dtype=torch.uint8, device=dev)      # zero bytes: the unsplit path
+    shared = p4q.w4a4_linear_workspace(M, N, K, dev)
     for ws in (None, empty):
-        for with_acc in (True, False):        # the split epilogue with and without acc_out
+        for with_acc in (True, False, True):  # the split epilogue with and without acc_out
             y, acc = run_gpu(ap, sa, wp, sw, "bf16", with_acc=with_acc,
-                             workspace=ws if ws is not None else
-                             p4q.w4a4_linear_workspace(M, N, K, dev))
+                             workspace=ws if ws is not None else shared)
             if with_acc:
                 assert (m := first_mismatch(acc, racc.astype(np.int32))) is None, m
             assert (m := first_mismatch(bits(y), bits(ry))) is None, (with_acc, m)
+            if ws is None and shared is not None and N >= 1024:
+                # the tile kernel's arrival counters are back at zero for the
+                # next call (the small-M kernel's slices have no counters)
+                assert int(shared[:4096].count_nonzero()) == 0
 
 
 @pytest.mark.parametrize("cfg_name", ["next7b_b1_k320", "next7b_b1_k640", "llava15_7b"])
