@@ -772,6 +772,8 @@ __global__ __launch_bounds__(256, BMT == 64 ? 4 : 2) void k_w4a4_gemm_2cu(const 
     // u (4 columns) stored at unit u ^ 2 (m & 15), which keeps both the
     // 8-byte writes and the 16-byte row reads free of bank conflicts.
     __syncthreads();
+    // int32 rows 16-byte aligned: N % 4 == 0 and an aligned base
+    const bool acc_vec = ACC && (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(acc_out) & 15) == 0);
     const float *s_sa = reinterpret_cast<const float *>(smem + l_scale_off<BMT>());
     const float *s_sw = s_sa + BMT;
     float sam[AF];
@@ -812,9 +814,14 @@ __global__ __launch_bounds__(256, BMT == 64 ? 4 : 2) void k_w4a4_gemm_2cu(const 
             if constexpr (ACC) {
                 const int m = m0 + r, nb = n0 + nl;
                 if (m < M) {
+                    int32_t *dst = acc_out + (int64_t)m * N + nb;
+                    if (acc_vec && nb + 3 < N) {      // the lane's 4 columns as one 16-byte store
+                        *reinterpret_cast<v4i *>(dst) = v4i{v[0], v[1], v[2], v[3]};
+                    } else {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (nb + e < N) acc_out[(int64_t)m * N + nb + e] = v[e];
+                        for (int e = 0; e < 4; ++e)
+                            if (nb + e < N) dst[e] = v[e];
+                    }
                 }
             }
         }
@@ -995,6 +1002,7 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_pt(const uint8_t *__restri
                 acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(u[i], u[4 + j], acc[i][j], 0, 0, 0);
     };
     const bool vec16 = ((ldy & 7) == 0) && ((reinterpret_cast<uintptr_t>(y) & 15) == 0);
+    const bool acc_vec = ACC && (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(acc_out) & 15) == 0);
 
     v4i u0[NF], u1[NF];
     int ck = 0, ckt = 0;                        // compute side: tile, k-tile
@@ -1084,9 +1092,14 @@ __global__ __launch_bounds__(256, 2) void k_w4a4_gemm_pt(const uint8_t *__restri
                     if constexpr (ACC) {
                         const int m = m0 + rl, nb0 = n0 + nl;
                         if (m < M) {
+                            int32_t *dst = acc_out + (int64_t)m * N + nb0;
+                            if (acc_vec && nb0 + 3 < N) {
+                                *reinterpret_cast<v4i *>(dst) = v4i{v[0], v[1], v[2], v[3]};
+                            } else {
 #pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                if (nb0 + e < N) acc_out[(int64_t)m * N + nb0 + e] = v[e];
+                                for (int e = 0; e < 4; ++e)
+                                    if (nb0 + e < N) dst[e] = v[e];
+                            }
                         }
                     }
                     acc[i][j] = v4i{0, 0, 0, 0};
