@@ -1329,16 +1329,17 @@ static bool use_large_tiles(int M, int N) { return M >= 1024 && N >= 1024; }
 static bool use_mid_tiles(int M, int N) { return M > 16 && M < 1024 && N >= 1024; }
 
 // Tile height of the mid path: 128 rows, or 64 where 128-row tiles would
-// leave CUs idle (fewer than 256 tiles) and K_in <= 4096.  64-row tiles
-// are less efficient per tile (their fragment reads per MFMA double), but
-// for short K they beat splitting K: measured at M = 704, N = 4096,
-// K = 4096: 21.5 us unsplit with 352 tiles of 64 rows against 27.7 us
-// with 192 tiles of 128 split in two; at M = 384: 18.8 against 19.6 us.
-// Everywhere else (q|k|v, gate|up, down at M = 384 / 704) 128 rows were
-// faster by 6-17%.
+// leave most CUs with a single block (fewer than 1.5 tiles per CU) and
+// K_in <= 4096.  64-row tiles are less efficient per tile (their fragment
+// reads per MFMA double), but there they fill the CUs with 2-3 blocks each:
+// measured with the in-kernel split of the last round, q|k|v at M = 384
+// (288 tiles of 128 rows) 28.4-29.2 -> 26.1-27.3 us; gate|up (516 tiles) and
+// everything at M = 704 were 5-20% slower on 64-row tiles.  Before that
+// split: o_proj at M = 704, 21.5 us unsplit on 352 tiles of 64 rows against
+// 27.7 us on 192 tiles of 128 split in two.
 static int mid_bm(int M, int N, int K) {
     const int64_t tiles128 = (((int64_t)M + 127) / 128) * (((int64_t)N + L_BN - 1) / L_BN);
-    return (tiles128 < 256 && K <= 4096) ? 64 : 128;
+    return (2 * tiles128 < 3 * (int64_t)device_cus() && K <= 4096) ? 64 : 128;
 }
 
 // Split plan of the mid-tile launches (needs the caller's workspace).  The

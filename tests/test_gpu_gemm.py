@@ -293,8 +293,8 @@ def test_small_m_split_k(shape, split):
     the workspace; (K_in <= 4096) 64-row tiles fill the CUs where 128-row
     tiles are too few; 512 tiles of 128 x 128 divide evenly and run
     unsplit.  (520, 8200, 2080): ragged in M, N and the last k-tile, with
-    256 whole tiles and 69 split in three.  Every path must equal the
-    oracle bit for bit."""
+    512 whole tiles of 64 rows and 73 split in three.  Every path must equal
+    the oracle bit for bit."""
     M, N, K = shape
     assert (p4q.lib().p4q_w4a4_linear_workspace_bytes(M, N, K) > 0) == split
     ap, sa, wp, sw = codes_for(M, N, K, seed=M + N)
