@@ -68,17 +68,6 @@ __device__ __forceinline__ float transform(float z, float sg) {
     else return __fmul_rn(z, sg);
 }
 
-__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
-
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o);
-        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o);
-        v = max_u64(v, ((uint64_t)hi << 32) | lo);
-    }
-    return v;
-}
 
 __device__ __forceinline__ double block_sum(double v, double *red) {
 #pragma unroll
@@ -95,8 +84,9 @@ __device__ __forceinline__ double block_sum(double v, double *red) {
 // ---------------------------------------------------------------------------
 // 1. Transformed per-row quantizer.  One 256-thread work-group per row; the
 //    transformed row stays in registers (CH chunks of 8 values per thread,
-//    K <= 2048 CH).  The row maximum and its lowest index come from one
-//    64-bit maximum over (|z'| bits, ~k).
+//    K <= 2048 CH).  The row maximum is a float maximum (non-negative
+//    floats order as their bit patterns); its lowest index is searched for
+//    afterwards, only by the threads that hold the maximum.
 // ---------------------------------------------------------------------------
 template <int CH, bool BF16, bool DIV>
 __global__ __launch_bounds__(kThreads) void k_quant_scaled(
@@ -104,13 +94,13 @@ __global__ __launch_bounds__(kThreads) void k_quant_scaled(
     float clip, const float *__restrict__ clip_rows, uint8_t *__restrict__ codes,
     int64_t ldc_bytes, float *__restrict__ scales, float *__restrict__ absmax,
     int32_t *__restrict__ kstar, float *__restrict__ zprime, uint8_t *__restrict__ inside) {
-    __shared__ uint64_t s_key[kThreads / 64];
-    const int row = blockIdx.x, t = threadIdx.x;
+    __shared__ uint32_t s_red[kThreads / 64];
+    const int row = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const uint4 *src = reinterpret_cast<const uint4 *>(z + (int64_t)row * ldz_bytes);
     const float4 *sg4 = reinterpret_cast<const float4 *>(sigma);
 
     float zp[CH][8];
-    uint64_t key = 0;
+    float am = 0.0f;
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
         const int q = t + kThreads * c;
@@ -130,26 +120,41 @@ __global__ __launch_bounds__(kThreads) void k_quant_scaled(
                 zo[1] = make_float4(zp[c][4], zp[c][5], zp[c][6], zp[c][7]);
             }
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const uint32_t k = (uint32_t)(8 * q + e);
-                key = max_u64(key, ((uint64_t)__float_as_uint(__builtin_fabsf(zp[c][e])) << 32) | ~k);
-            }
+            for (int e = 0; e < 8; ++e) am = __builtin_fmaxf(am, __builtin_fabsf(zp[c][e]));
         } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e) zp[c][e] = 0.0f;
         }
     }
-    key = wave_max_u64(key);
-    if ((t & 63) == 0) s_key[t >> 6] = key;
+    const uint32_t mw = wave_max_u32(__float_as_uint(am));
+    if (lane == 0) s_red[wave] = mw;
     __syncthreads();
-    key = max_u64(max_u64(s_key[0], s_key[1]), max_u64(s_key[2], s_key[3]));
-    const float a = __uint_as_float((uint32_t)(key >> 32));
+    const uint32_t abits = max(max(s_red[0], s_red[1]), max(s_red[2], s_red[3]));
+    const float a = __uint_as_float(abits);
     const float cl = clip_rows ? clip_rows[row] : clip;
     const float s = __fmul_rn(cl, a) / 7.0f;
+    if (kstar) {                                             // block-uniform
+        // lowest k with |z'_k| = a: only threads holding the maximum look
+        uint32_t nk = 0u;                                    // ~k, maximised
+        if (__float_as_uint(am) == abits) {
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                const int q = t + kThreads * c;
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (q < nchunk && __float_as_uint(__builtin_fabsf(zp[c][e])) == abits)
+                        nk = max(nk, ~(uint32_t)(8 * q + e));
+            }
+        }
+        const uint32_t wk = wave_max_u32(nk);
+        __syncthreads();                                     // every read of s_red above is done
+        if (lane == 0) s_red[wave] = wk;
+        __syncthreads();
+        if (t == 0) kstar[row] = (int32_t)~max(max(s_red[0], s_red[1]), max(s_red[2], s_red[3]));
+    }
     if (t == 0) {
         scales[row] = s;
         if (absmax) absmax[row] = a;
-        if (kstar) kstar[row] = (int32_t)~(uint32_t)key;
     }
 
     uint32_t *dst = reinterpret_cast<uint32_t *>(codes + (int64_t)row * ldc_bytes);
