@@ -1355,6 +1355,8 @@ static int mid_bm(int M, int N, int K) {
 //  * T >= C: S = C / (T % C), at most 8, each slice at least 4 k-tiles.
 //    A whole last round of T % C tiles on as many CUs costs a batch-1 layer
 //    ~14 us of ~118 (timed with the remainder tiles left out).
+// bytes of arrival counters at the head of a split launch's workspace
+constexpr size_t kArrivalBytes = 4096;
 struct MidPlan {
     int bm, T, tdp, rem, S, kps;   // tiles [tdp, T) split into S slices of kps k-tiles
 };
@@ -1378,7 +1380,7 @@ static MidPlan mid_plan(int M, int N, int K) {
         if (rem == 0) return p;
         S = std::min(std::min(cus / rem, 8), kt_all / 4);
     }
-    if (S < 2) return p;
+    if (S < 2 || rem > (int)(kArrivalBytes / 4)) return p;   // one arrival counter per split tile
     p.kps = (kt_all + S - 1) / S;
     p.S = (kt_all + p.kps - 1) / p.kps;              // every slice non-empty
     p.rem = rem;
@@ -1387,7 +1389,6 @@ static MidPlan mid_plan(int M, int N, int K) {
 }
 // workspace of a split mid launch: arrival counters (zero between calls),
 // then one BM x 128 int32 slot per slice
-constexpr size_t kArrivalBytes = 4096;
 static size_t mid_split_bytes(const MidPlan &p) {
     return p.S > 1 ? kArrivalBytes + (size_t)p.rem * p.S * p.bm * L_BN * 4 : 0;
 }
