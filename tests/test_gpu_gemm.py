@@ -329,3 +329,35 @@ def test_batch1_layer_launches(cfg_name):
         y, _ = run_gpu(ap, sa, wp, sw, "bf16", with_acc=False,
                        workspace=p4q.w4a4_linear_workspace(cfg.M, N, K, dev))
         assert (m := first_mismatch(bits(y), bits(ry))) is None, ((N, K), m)
+
+
+@pytest.mark.parametrize("shape", [(384, 12288, 4096), (384, 4096, 11008)])
+def test_split_k_graph_replays(shape):
+    """The in-launch split (remainder tiles, and a launch whose tiles are all
+    split) under HIP graph capture: its arrival counters are reset by the
+    kernel itself, with no memset node, so every replay must reproduce the
+    oracle's y, also with eager calls on the same workspace between replays."""
+    M, N, K = shape
+    dev = torch.device("cuda:0")
+    ap, sa, wp, sw = codes_for(M, N, K, seed=7 * M + N)
+    _, ry = oracle.w4a4_linear(ap, sa, wp, sw, "bf16")
+    ws = p4q.w4a4_linear_workspace(M, N, K, dev)
+    assert ws is not None
+    a, s_a, w, s_w = to_gpu(ap), to_gpu(sa), to_gpu(wp), to_gpu(sw)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    p4q.w4a4_linear(a, s_a, w, s_w, y=y, workspace=ws)     # warm-up outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        p4q.w4a4_linear(a, s_a, w, s_w, y=y, workspace=ws)
+    for rep in range(3):
+        y.fill_(0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert (m := first_mismatch(bits(to_np(y)), bits(ry))) is None, (rep, m)
+        assert int(ws[:4096].count_nonzero()) == 0, rep
+        y2 = torch.empty_like(y)
+        p4q.w4a4_linear(a, s_a, w, s_w, y=y2, workspace=ws)   # eager call between replays
+        torch.cuda.synchronize()
+        assert (m := first_mismatch(bits(to_np(y2)), bits(ry))) is None, (rep, m)
+    del g
