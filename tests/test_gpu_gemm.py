@@ -285,7 +285,7 @@ def test_decode_graph_replay_matches_eager():
                                          ((96, 512, 4096), True), ((704, 4096, 11008), True),
                                          ((384, 4096, 4096), True), ((704, 4096, 4096), True),
                                          ((384, 12288, 4096), True), ((520, 8200, 2080), True),
-                                         ((512, 16384, 4096), False)])
+                                         ((300, 8200, 4096), True), ((512, 16384, 4096), False)])
 def test_small_m_split_k(shape, split):
     """Batch-1 shapes (one image's pruned sequence).  Given the workspace,
     the tiles past the last whole round per CU (all of them when there are
@@ -293,8 +293,9 @@ def test_small_m_split_k(shape, split):
     the workspace; (K_in <= 4096) 64-row tiles fill the CUs where 128-row
     tiles are too few; 512 tiles of 128 x 128 divide evenly and run
     unsplit.  (520, 8200, 2080): ragged in M, N and the last k-tile, with
-    512 whole tiles of 64 rows and 73 split in three.  Every path must equal
-    the oracle bit for bit."""
+    512 whole tiles of 64 rows and 73 split in three; (300, 8200, 4096) the
+    same with a ragged last 64-row tile.  Every path must equal the oracle
+    bit for bit, in bf16 and in fp16."""
     M, N, K = shape
     assert (p4q.lib().p4q_w4a4_linear_workspace_bytes(M, N, K) > 0) == split
     ap, sa, wp, sw = codes_for(M, N, K, seed=M + N)
@@ -313,6 +314,13 @@ def test_small_m_split_k(shape, split):
                 # the tile kernel's arrival counters are back at zero for the
                 # next call (the small-M kernel's slices have no counters)
                 assert int(shared[:4096].count_nonzero()) == 0
+    if shared is not None:                    # the fp16-output instances of the split path
+        _, ry16 = oracle.w4a4_linear(ap, sa, wp, sw, "fp16")
+        for with_acc in (False, True):
+            y, acc = run_gpu(ap, sa, wp, sw, "fp16", with_acc=with_acc, workspace=shared)
+            if with_acc:
+                assert (m := first_mismatch(acc, racc.astype(np.int32))) is None, m
+            assert (m := first_mismatch(bits(y), bits(ry16))) is None, ("fp16", with_acc, m)
 
 
 @pytest.mark.parametrize("cfg_name", ["next7b_b1_k320", "next7b_b1_k640", "llava15_7b"])
