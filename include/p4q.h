@@ -381,7 +381,8 @@ int p4q_calib_block_grad(p4q_dtype dt, int M, int d, int f, int H, const void *x
  *   first 4096 bytes hold per-tile arrival counters: they must be zero
  *   before the first call that uses the workspace (allocate it
  *   zero-filled), and every call leaves them zero.  Calls that share a
- *   workspace must not overlap.
+ *   workspace must not overlap.  The size depends on the current device
+ *   (its number of compute units): query it with that device current.
  * Limits: M >= 1, N_out >= 1, K_in % 32 == 0, 32 <= K_in <= 131072,
  *   ldy >= N_out; code pointers 16-byte aligned, y 4-byte aligned.
  * ---------------------------------------------------------------------- */
